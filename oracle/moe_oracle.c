@@ -1,0 +1,291 @@
+/*
+ * moe_oracle.c -- plain fp64 CPU reference of the sparse Mixture-of-Experts
+ * FFN layer (Mixtral-8x7B shape) served by the engine in the paper.
+ *
+ * TEST INFRASTRUCTURE ONLY.  This file is the oracle that the GPU library is
+ * checked against.  Only the test suite, the smoke check and the benchmark's
+ * CPU-baseline leg load it.  It shares no code, header, table or helper with
+ * the HIP library, and the HIP library never loads it.
+ *
+ * What is computed.  The paper (Sec. 4.1, "Optimize Inference Engine") states
+ * that the engine work targets Mixture-of-Experts LLMs, citing Mixtral, and
+ * serves Mixtral-8x7B (Sec. 5, experimental settings).  The Mixtral layer it
+ * cites is, per token x (a row of d values):
+ *
+ *   logits  l_e = sum_i x_i Wr[e,i] (+ b_e)                      router GEMM
+ *   S       = the k experts with the largest logits; exactly equal logits
+ *             rank the lower expert index first                   top-k
+ *   g_j     = exp(l_{S_j}) / sum_{m<k} exp(l_{S_m})               softmax over S
+ *   FFN_e(x)= W2[e] ( silu(W1[e] x) * (W3[e] x) ),
+ *             silu(z) = z / (1 + exp(-z))                         SwiGLU expert
+ *   out     = sum_{j<k} g_j FFN_{S_j}(x)                           weighted combine
+ *
+ * plus, for a stack, a pre-norm residual block around every layer:
+ *   a = RMSNorm(h) * gamma,  h' = h + MoE(a).
+ *
+ * Every value is carried in double.  bf16 inputs are widened exactly (a bf16
+ * bit pattern is the top half of an IEEE float).  Nothing is rounded back to
+ * bf16 or float.  Loops are plain and run in index order, so results do not
+ * depend on the OpenMP thread count.  Work is arranged expert-major (each
+ * expert's weight row is widened once and used for all of its tokens); this is
+ * a loop order, not a change to any sum.
+ *
+ * Weight layout (row-major, reduction index contiguous):
+ *   x [T,d], Wr [E,d], W1 [E,ffn,d], W3 [E,ffn,d], W2 [E,d,ffn], b [E] float.
+ *
+ * Pins: tests compare this file against a pure-Python brute force on tiny
+ * shapes (subset enumeration for top-k, dense all-expert evaluation), against
+ * torch fp64 dense SwiGLU for E=1,k=1 and against a dense softmax mixture for
+ * k=E, against closed forms for one-hot inputs, and against the layer's
+ * invariants (gate weights sum to one, token-permutation equivariance, a
+ * zeroed expert contributes nothing).
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+enum { ORACLE_OK = 0, ORACLE_BAD_ARG = 1, ORACLE_NONFINITE = 2, ORACLE_NO_MEMORY = 3 };
+
+static double widen(uint16_t b)
+{
+    uint32_t u = (uint32_t)b << 16;
+    float f;
+    memcpy(&f, &u, sizeof f);
+    return (double)f;
+}
+
+int oracle_threads(int n)
+{
+#ifdef _OPENMP
+    if (n > 0) omp_set_num_threads(n);
+    return omp_get_max_threads();
+#else
+    (void)n;
+    return 1;
+#endif
+}
+
+/* Inputs must be finite: the layer is undefined otherwise. */
+static int all_finite_bf16(const uint16_t* p, int64_t n)
+{
+    for (int64_t i = 0; i < n; ++i)
+        if ((p[i] & 0x7f80u) == 0x7f80u) return 0;
+    return 1;
+}
+
+/* ---- router GEMM ------------------------------------------------------- */
+
+/* logits[t,e] = sum_i x[t,i] * Wr[e,i]  (+ bias[e] when bias != NULL) */
+int oracle_router_logits(const uint16_t* x, const uint16_t* wr, const float* bias,
+                         int64_t T, int64_t d, int64_t E, double* logits)
+{
+    if (T < 0 || d <= 0 || E <= 0) return ORACLE_BAD_ARG;
+    if (!all_finite_bf16(x, T * d) || !all_finite_bf16(wr, E * d)) return ORACLE_NONFINITE;
+#pragma omp parallel for schedule(static)
+    for (int64_t t = 0; t < T; ++t) {
+        for (int64_t e = 0; e < E; ++e) {
+            double s = 0.0;
+            for (int64_t i = 0; i < d; ++i)
+                s += widen(x[t * d + i]) * widen(wr[e * d + i]);
+            if (bias) s += (double)bias[e];
+            logits[t * E + e] = s;
+        }
+    }
+    return ORACLE_OK;
+}
+
+/* ---- top-k gating -------------------------------------------------------- */
+
+/* Expert a ranks ahead of expert b: larger logit, or an equal logit and a
+ * lower index.  (+0 and -0 compare equal.) */
+static int ranks_ahead(double la, int a, double lb, int b)
+{
+    return la > lb || (la == lb && a < b);
+}
+
+/* ids[t,j]: the j-th ranked expert of token t, j < k.
+ * gates[t,j] = exp(l_{ids[t,j]} - l_{ids[t,0]}) / sum_m exp(l_{ids[t,m]} - l_{ids[t,0]}),
+ * i.e. a softmax over the selected logits (shifted by the largest one, which
+ * leaves the ratio unchanged). */
+int oracle_topk_gate(const double* logits, int64_t T, int E, int k, int32_t* ids, double* gates)
+{
+    if (T < 0 || E <= 0 || k <= 0 || k > E) return ORACLE_BAD_ARG;
+    for (int64_t t = 0; t < T; ++t) {
+        const double* l = logits + t * E;
+        int32_t* s = ids + t * k;
+        for (int j = 0; j < k; ++j) {
+            int best = -1;
+            for (int e = 0; e < E; ++e) {
+                int taken = 0;
+                for (int m = 0; m < j; ++m) taken |= (s[m] == e);
+                if (taken) continue;
+                if (best < 0 || ranks_ahead(l[e], e, l[best], best)) best = e;
+            }
+            s[j] = best;
+        }
+        double top = l[s[0]], denom = 0.0;
+        for (int j = 0; j < k; ++j) denom += exp(l[s[j]] - top);
+        for (int j = 0; j < k; ++j) gates[t * k + j] = exp(l[s[j]] - top) / denom;
+    }
+    return ORACLE_OK;
+}
+
+/* ---- dispatch: histogram, offsets, permutation ---------------------------- */
+
+/* Assignment a = t*k + j goes to expert ids[a].
+ * counts[e]   = number of assignments to e
+ * offsets[e]  = sum_{e' < e} counts[e'],  offsets[E] = T*k
+ * perm[r]     = the r-th assignment in (expert ascending, a ascending) order,
+ *               so rows offsets[e] .. offsets[e+1]-1 hold expert e's tokens
+ *               in ascending token order. */
+int oracle_dispatch(const int32_t* ids, int64_t T, int E, int k,
+                    int32_t* counts, int32_t* offsets, int32_t* perm)
+{
+    if (T < 0 || E <= 0 || k <= 0) return ORACLE_BAD_ARG;
+    const int64_t A = T * k;
+    for (int64_t a = 0; a < A; ++a)
+        if (ids[a] < 0 || ids[a] >= E) return ORACLE_BAD_ARG;
+    for (int e = 0; e < E; ++e) {
+        int32_t c = 0;
+        for (int64_t a = 0; a < A; ++a) c += (ids[a] == e);
+        counts[e] = c;
+    }
+    offsets[0] = 0;
+    for (int e = 0; e < E; ++e) offsets[e + 1] = offsets[e] + counts[e];
+    int64_t r = 0;
+    for (int e = 0; e < E; ++e)
+        for (int64_t a = 0; a < A; ++a)
+            if (ids[a] == e) perm[r++] = (int32_t)a;
+    return ORACLE_OK;
+}
+
+/* ---- expert FFN and combine ---------------------------------------------- */
+
+static double silu(double z) { return z / (1.0 + exp(-z)); }
+
+/* out[t,:] = sum_j gates[t,j] * FFN_{ids[t,j]}(x[t,:]), slots summed in
+ * ascending j.  Optional diagnostics (NULL to skip):
+ *   h_slots [T*k, ffn]: silu(W1 x) * (W3 x) of assignment a = t*k+j
+ *   y_slots [T*k, d]  : W2 h of assignment a (not gate-weighted) */
+int oracle_moe_apply(const uint16_t* x, const uint16_t* w1, const uint16_t* w3,
+                     const uint16_t* w2, const int32_t* ids, const double* gates,
+                     int64_t T, int64_t d, int64_t ffn, int E, int k,
+                     double* out, double* h_slots, double* y_slots)
+{
+    if (T < 0 || d <= 0 || ffn <= 0 || E <= 0 || k <= 0 || k > E) return ORACLE_BAD_ARG;
+    const int64_t A = T * k;
+    for (int64_t a = 0; a < A; ++a)
+        if (ids[a] < 0 || ids[a] >= E) return ORACLE_BAD_ARG;
+    if (!all_finite_bf16(x, T * d)) return ORACLE_NONFINITE;
+
+    double* xd = (double*)malloc(sizeof(double) * (size_t)(T * d + 1));
+    double* h = (double*)malloc(sizeof(double) * (size_t)(A * ffn + 1));
+    double* y = (double*)malloc(sizeof(double) * (size_t)(A * d + 1));
+    int64_t* rows = (int64_t*)malloc(sizeof(int64_t) * (size_t)(A + 1));
+    if (!xd || !h || !y || !rows) {
+        free(xd); free(h); free(y); free(rows);
+        return ORACLE_NO_MEMORY;
+    }
+    for (int64_t i = 0; i < T * d; ++i) xd[i] = widen(x[i]);
+
+    for (int e = 0; e < E; ++e) {
+        /* the assignments routed to expert e, ascending */
+        int64_t n_rows = 0;
+        for (int64_t a = 0; a < A; ++a)
+            if (ids[a] == e) rows[n_rows++] = a;
+        if (n_rows == 0) continue;
+        const uint16_t* W1 = w1 + (int64_t)e * ffn * d;
+        const uint16_t* W3 = w3 + (int64_t)e * ffn * d;
+        const uint16_t* W2 = w2 + (int64_t)e * d * ffn;
+
+        /* h[a,n] = silu(sum_i W1[n,i] x[t,i]) * (sum_i W3[n,i] x[t,i]) */
+#pragma omp parallel
+        {
+            double* r1 = (double*)malloc(sizeof(double) * (size_t)d);
+            double* r3 = (double*)malloc(sizeof(double) * (size_t)d);
+#pragma omp for schedule(static)
+            for (int64_t n = 0; n < ffn; ++n) {
+                for (int64_t i = 0; i < d; ++i) {
+                    r1[i] = widen(W1[n * d + i]);
+                    r3[i] = widen(W3[n * d + i]);
+                }
+                for (int64_t q = 0; q < n_rows; ++q) {
+                    const double* xt = xd + (rows[q] / k) * d;
+                    double u = 0.0, v = 0.0;
+                    for (int64_t i = 0; i < d; ++i) {
+                        u += r1[i] * xt[i];
+                        v += r3[i] * xt[i];
+                    }
+                    h[rows[q] * ffn + n] = silu(u) * v;
+                }
+            }
+            free(r1);
+            free(r3);
+        }
+
+        /* y[a,i] = sum_n W2[i,n] h[a,n] */
+#pragma omp parallel
+        {
+            double* r2 = (double*)malloc(sizeof(double) * (size_t)ffn);
+#pragma omp for schedule(static)
+            for (int64_t i = 0; i < d; ++i) {
+                for (int64_t n = 0; n < ffn; ++n) r2[n] = widen(W2[i * ffn + n]);
+                for (int64_t q = 0; q < n_rows; ++q) {
+                    const double* ha = h + rows[q] * ffn;
+                    double s = 0.0;
+                    for (int64_t n = 0; n < ffn; ++n) s += r2[n] * ha[n];
+                    y[rows[q] * d + i] = s;
+                }
+            }
+            free(r2);
+        }
+    }
+
+    /* out[t,i] = sum_{j ascending} gates[t,j] * y[t*k+j, i] */
+    for (int64_t t = 0; t < T; ++t) {
+        for (int64_t i = 0; i < d; ++i) {
+            double s = 0.0;
+            for (int j = 0; j < k; ++j) s += gates[t * k + j] * y[(t * k + j) * d + i];
+            out[t * d + i] = s;
+        }
+    }
+    if (h_slots) memcpy(h_slots, h, sizeof(double) * (size_t)(A * ffn));
+    if (y_slots) memcpy(y_slots, y, sizeof(double) * (size_t)(A * d));
+    free(xd); free(h); free(y); free(rows);
+    return ORACLE_OK;
+}
+
+/* The whole layer: router GEMM, top-k gating, experts, combine.  ids, gates
+ * and logits are outputs (logits [T,E], ids/gates [T,k]). */
+int oracle_moe_layer(const uint16_t* x, const uint16_t* wr, const float* bias,
+                     const uint16_t* w1, const uint16_t* w3, const uint16_t* w2,
+                     int64_t T, int64_t d, int64_t ffn, int E, int k,
+                     double* out, double* logits, int32_t* ids, double* gates)
+{
+    int rc = oracle_router_logits(x, wr, bias, T, d, E, logits);
+    if (rc) return rc;
+    rc = oracle_topk_gate(logits, T, E, k, ids, gates);
+    if (rc) return rc;
+    return oracle_moe_apply(x, w1, w3, w2, ids, gates, T, d, ffn, E, k, out, NULL, NULL);
+}
+
+/* ---- RMSNorm for the residual stack -------------------------------------- */
+
+/* a[t,i] = h[t,i] / sqrt(mean_i h[t,i]^2 + eps) * gamma[i]; h is the float
+ * residual stream, gamma bf16. */
+int oracle_rmsnorm(const float* h, const uint16_t* gamma, int64_t T, int64_t d, double eps,
+                   double* a)
+{
+    if (T < 0 || d <= 0 || !(eps >= 0.0)) return ORACLE_BAD_ARG;
+    for (int64_t t = 0; t < T; ++t) {
+        double ss = 0.0;
+        for (int64_t i = 0; i < d; ++i) ss += (double)h[t * d + i] * (double)h[t * d + i];
+        double inv = 1.0 / sqrt(ss / (double)d + eps);
+        for (int64_t i = 0; i < d; ++i) a[t * d + i] = (double)h[t * d + i] * inv * widen(gamma[i]);
+    }
+    return ORACLE_OK;
+}

@@ -1,0 +1,169 @@
+"""ctypes front end of the fp64 CPU oracle (``moe_oracle.c``).
+
+TEST INFRASTRUCTURE ONLY: the test suite, the smoke check and the benchmark's
+CPU-baseline leg are its only callers.  It takes host numpy arrays (bf16 as
+raw ``uint16`` bit patterns), never imports the GPU package and never touches
+a device.
+
+Definitions follow the Mixtral MoE layer that the paper's engine serves
+(Sec. 4.1 and Sec. 5 of the paper); the C file's header states them.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "moe_oracle.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+
+_i64, _i32, _f64 = ctypes.c_int64, ctypes.c_int32, ctypes.c_double
+_p = ctypes.c_void_p
+
+
+class OracleError(RuntimeError):
+    pass
+
+
+def build(src: str = _SRC, out: str = _LIB, extra=()) -> str:
+    """Compile the oracle with gcc (OpenMP, no fast-math: sums keep their order)."""
+    cmd = ["gcc", "-O2", "-fopenmp", "-fPIC", "-shared", "-std=c11", "-Wall", "-Werror",
+           *extra, src, "-o", out + ".tmp", "-lm"]
+    subprocess.run(cmd, check=True)
+    os.replace(out + ".tmp", out)
+    return out
+
+
+class Oracle:
+    """One loaded copy of the oracle library (a mutant build may be loaded too)."""
+
+    def __init__(self, lib_path: str = _LIB):
+        if lib_path == _LIB and not os.path.exists(_LIB):
+            build()
+        self.lib = ctypes.CDLL(lib_path)
+        L = self.lib
+        L.oracle_threads.argtypes = [ctypes.c_int]
+        L.oracle_threads.restype = ctypes.c_int
+        L.oracle_router_logits.argtypes = [_p, _p, _p, _i64, _i64, _i64, _p]
+        L.oracle_topk_gate.argtypes = [_p, _i64, ctypes.c_int, ctypes.c_int, _p, _p]
+        L.oracle_dispatch.argtypes = [_p, _i64, ctypes.c_int, ctypes.c_int, _p, _p, _p]
+        L.oracle_moe_apply.argtypes = [_p, _p, _p, _p, _p, _p, _i64, _i64, _i64,
+                                       ctypes.c_int, ctypes.c_int, _p, _p, _p]
+        L.oracle_moe_layer.argtypes = [_p, _p, _p, _p, _p, _p, _i64, _i64, _i64,
+                                       ctypes.c_int, ctypes.c_int, _p, _p, _p, _p]
+        L.oracle_rmsnorm.argtypes = [_p, _p, _i64, _i64, _f64, _p]
+        for f in ("oracle_router_logits", "oracle_topk_gate", "oracle_dispatch",
+                  "oracle_moe_apply", "oracle_moe_layer", "oracle_rmsnorm"):
+            getattr(L, f).restype = ctypes.c_int
+
+    # -- helpers -----------------------------------------------------------
+    @staticmethod
+    def _bits(a, shape=None):
+        a = np.ascontiguousarray(a)
+        if a.dtype != np.uint16:
+            raise TypeError("bf16 operands are passed as uint16 bit patterns")
+        if shape is not None and a.shape != tuple(shape):
+            raise ValueError(f"shape {a.shape} != {tuple(shape)}")
+        return a
+
+    @staticmethod
+    def _ptr(a):
+        return None if a is None else a.ctypes.data
+
+    @staticmethod
+    def _check(rc, what):
+        if rc != 0:
+            raise OracleError(f"{what} failed with code {rc}")
+
+    def threads(self, n: int = 0) -> int:
+        """Set (n>0) and return the OpenMP thread count."""
+        return self.lib.oracle_threads(n)
+
+    # -- API -----------------------------------------------------------------
+    def router_logits(self, x, wr, bias=None):
+        T, d = x.shape
+        E = wr.shape[0]
+        x, wr = self._bits(x), self._bits(wr, (E, d))
+        b = None if bias is None else np.ascontiguousarray(bias, dtype=np.float32)
+        out = np.empty((T, E), np.float64)
+        self._check(self.lib.oracle_router_logits(self._ptr(x), self._ptr(wr), self._ptr(b),
+                                                  T, d, E, self._ptr(out)), "router_logits")
+        return out
+
+    def topk_gate(self, logits, k):
+        logits = np.ascontiguousarray(logits, dtype=np.float64)
+        T, E = logits.shape
+        ids = np.empty((T, k), np.int32)
+        gates = np.empty((T, k), np.float64)
+        self._check(self.lib.oracle_topk_gate(self._ptr(logits), T, E, k, self._ptr(ids),
+                                              self._ptr(gates)), "topk_gate")
+        return ids, gates
+
+    def dispatch(self, ids, E):
+        ids = np.ascontiguousarray(ids, dtype=np.int32)
+        T, k = ids.shape
+        counts = np.empty(E, np.int32)
+        offsets = np.empty(E + 1, np.int32)
+        perm = np.empty(T * k, np.int32)
+        self._check(self.lib.oracle_dispatch(self._ptr(ids), T, E, k, self._ptr(counts),
+                                             self._ptr(offsets), self._ptr(perm)), "dispatch")
+        return counts, offsets, perm
+
+    def moe_apply(self, x, w1, w3, w2, ids, gates, want_slots=False):
+        T, d = x.shape
+        E, ffn, _ = w1.shape
+        ids = np.ascontiguousarray(ids, dtype=np.int32)
+        gates = np.ascontiguousarray(gates, dtype=np.float64)
+        k = ids.shape[1]
+        x = self._bits(x)
+        w1, w3 = self._bits(w1, (E, ffn, d)), self._bits(w3, (E, ffn, d))
+        w2 = self._bits(w2, (E, d, ffn))
+        out = np.empty((T, d), np.float64)
+        h = np.empty((T * k, ffn), np.float64) if want_slots else None
+        y = np.empty((T * k, d), np.float64) if want_slots else None
+        self._check(self.lib.oracle_moe_apply(
+            self._ptr(x), self._ptr(w1), self._ptr(w3), self._ptr(w2), self._ptr(ids),
+            self._ptr(gates), T, d, ffn, E, k, self._ptr(out), self._ptr(h), self._ptr(y)),
+            "moe_apply")
+        return (out, h, y) if want_slots else out
+
+    def moe_layer(self, x, wr, w1, w3, w2, k, bias=None):
+        """Returns dict(out, logits, ids, gates) for the whole layer."""
+        T, d = x.shape
+        E, ffn, _ = w1.shape
+        x, wr = self._bits(x), self._bits(wr, (E, d))
+        w1, w3 = self._bits(w1, (E, ffn, d)), self._bits(w3, (E, ffn, d))
+        w2 = self._bits(w2, (E, d, ffn))
+        b = None if bias is None else np.ascontiguousarray(bias, dtype=np.float32)
+        out = np.empty((T, d), np.float64)
+        logits = np.empty((T, E), np.float64)
+        ids = np.empty((T, k), np.int32)
+        gates = np.empty((T, k), np.float64)
+        self._check(self.lib.oracle_moe_layer(
+            self._ptr(x), self._ptr(wr), self._ptr(b), self._ptr(w1), self._ptr(w3),
+            self._ptr(w2), T, d, ffn, E, k, self._ptr(out), self._ptr(logits), self._ptr(ids),
+            self._ptr(gates)), "moe_layer")
+        return {"out": out, "logits": logits, "ids": ids, "gates": gates}
+
+    def rmsnorm(self, h, gamma, eps):
+        h = np.ascontiguousarray(h, dtype=np.float32)
+        T, d = h.shape
+        gamma = self._bits(gamma, (d,))
+        a = np.empty((T, d), np.float64)
+        self._check(self.lib.oracle_rmsnorm(self._ptr(h), self._ptr(gamma), T, d, float(eps),
+                                            self._ptr(a)), "rmsnorm")
+        return a
+
+
+_default = None
+
+
+def get() -> Oracle:
+    global _default
+    if _default is None:
+        _default = Oracle()
+    return _default
