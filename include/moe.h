@@ -1,0 +1,208 @@
+/*
+ * moe.h -- C ABI of the MI355X (gfx950) Mixture-of-Experts FFN layer library
+ * (libmoe.so).
+ *
+ * The layer is the sparse MoE FFN of Mixtral-8x7B, the model the paper's
+ * serving engine is optimised for (Sec. 4.1, "Optimize Inference Engine";
+ * Sec. 5, experimental settings).  Per token x (d values):
+ *
+ *   logits  l_e = sum_i x_i Wr[e,i] (+ b_e)                   router GEMM
+ *   S       = the k largest logits; equal logits rank the lower expert first
+ *   g_j     = softmax over the k selected logits (slot 0 = largest)
+ *   FFN_e(x)= W2[e] (silu(W1[e] x) * (W3[e] x)),  silu(z) = z/(1+exp(-z))
+ *   out     = sum_{j<k} g_j FFN_{S_j}(x)
+ *
+ * The engine batches requests continuously (Sec. 4.1, "Continuous Batching and
+ * Batch Scheduler"), so T -- the tokens in this engine step, one per decoding
+ * request or a prefill chunk -- changes on every call.  Every entry point takes
+ * T at run time; nothing is recompiled and no call waits on the device.
+ *
+ * Conventions shared by every entry point:
+ *   - Tensors are caller-owned DEVICE pointers, row-major, reduction index
+ *     contiguous (the nn.Linear layout of Mixtral checkpoints):
+ *       x [T,d] bf16, router_w [E,d] bf16, router_bias [E] f32,
+ *       w1, w3 [E,ffn,d] bf16, w2 [E,d,ffn] bf16.
+ *     The library keeps no reference after the call returns.
+ *   - bf16 is passed as raw bits (moe_bf16_t).  Arithmetic: bf16 operands,
+ *     f32 accumulation; logits, gate weights and slot outputs are f32; the
+ *     SwiGLU intermediate h and the layer output are rounded to bf16 (RNE).
+ *   - Calls are asynchronous and ordered on `stream` (NULL = the null
+ *     stream).  Buffers must stay valid until that work has run.
+ *   - Assignment a = t*k + j is slot j of token t.  Rows of the permuted
+ *     (expert-major) order are r = 0..T*k-1; expert e owns rows
+ *     [expert_offsets[e], expert_offsets[e+1]), in ascending a.
+ *   - Limits: 1 <= E <= 64, 1 <= k <= min(E, 8), d and ffn multiples of 64
+ *     with d <= 65536 and ffn <= 65536, 0 <= T and T*k < 2^31.  Device
+ *     pointers must be 16-byte aligned.  T = 0 returns MOE_OK and launches
+ *     nothing; buffers whose size scales with T may then be NULL.
+ *   - Errors: every argument is checked before anything is enqueued; on
+ *     error nothing is enqueued and a message is available from
+ *     moe_last_error() (thread-local).  A failed launch returns MOE_ERR_HIP.
+ *     Faults inside kernels surface at the caller's next synchronisation.
+ *     No C++ exception crosses this interface.
+ */
+#ifndef MOE_MI355X_H
+#define MOE_MI355X_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef uint16_t moe_bf16_t; /* raw bfloat16 bits */
+
+typedef enum {
+    MOE_OK = 0,
+    MOE_ERR_INVALID_ARG = 1, /* null/misaligned pointer, bad size, aliasing */
+    MOE_ERR_UNSUPPORTED = 2, /* outside the limits above */
+    MOE_ERR_NO_MEMORY = 3,   /* workspace too small or allocation failed */
+    MOE_ERR_HIP = 4          /* a HIP runtime call or kernel launch failed */
+} moe_status_t;
+
+/*
+ * Router GEMM + top-k gating + dispatch (Sec. 4.1: the MoE router of the
+ * Mixtral model the engine serves).
+ *   logits[t,e]   = sum_i x[t,i] router_w[e,i] in f32 (+ router_bias[e], f32,
+ *                   added after the sum; NULL = no bias).  Never rounded to bf16.
+ *   topk_ids[t,j] = j-th ranked expert of token t (larger logit first; equal
+ *                   logits: lower index first).                         [T,k] i32
+ *   topk_w[t,j]   = exp(l_{S_j} - l_{S_0}) / sum_m exp(l_{S_m} - l_{S_0}) [T,k] f32
+ *   expert_offsets[e] = number of assignments to experts < e; [E] = T*k. [E+1] i32
+ *   perm[r]       = assignment a of permuted row r (expert-major, then a). [T*k] i32
+ *   logits        = optional [T,E] f32 copy of the router logits (NULL to skip).
+ */
+moe_status_t moe_route(const moe_bf16_t* x, const moe_bf16_t* router_w, const float* router_bias,
+                       int64_t T, int32_t d, int32_t E, int32_t k, int32_t* topk_ids,
+                       float* topk_w, int32_t* expert_offsets, int32_t* perm, float* logits,
+                       hipStream_t stream);
+
+/*
+ * Token-to-expert permutation (Sec. 4.1, MoE layer): gather token rows into
+ * per-expert contiguous rows.  x_perm[r,:] = x[perm[r] / k, :].  [T*k,d] bf16.
+ * x_perm must not overlap x.
+ */
+moe_status_t moe_permute(const moe_bf16_t* x, const int32_t* perm, int64_t T, int32_t d,
+                         int32_t k, moe_bf16_t* x_perm, hipStream_t stream);
+
+/*
+ * First half of the per-expert SwiGLU FFN (Sec. 4.1, Mixtral experts):
+ * for every expert e and row r in [expert_offsets[e], expert_offsets[e+1]):
+ *   h[r,n] = bf16( silu(sum_i w1[e,n,i] xr[i]) * sum_i w3[e,n,i] xr[i] )
+ * where the token row xr is x[perm[r] / k, :] when perm is given (the gather
+ * of moe_permute fused into the GEMM; x is then [T,d]) and x[r, :] when perm
+ * is NULL (x is then the permuted [T*k,d] rows).  h [T*k,ffn] bf16.
+ */
+moe_status_t moe_swiglu_up(const moe_bf16_t* x, const int32_t* perm,
+                           const int32_t* expert_offsets, const moe_bf16_t* w1,
+                           const moe_bf16_t* w3, int64_t T, int32_t d, int32_t ffn, int32_t E,
+                           int32_t k, moe_bf16_t* h, hipStream_t stream);
+
+/*
+ * Second half of the expert FFN with the gate-weighted scatter fused in:
+ * for every expert e and row r of e, with a = perm[r]:
+ *   y[a,i] = topk_w[a] * sum_n w2[e,i,n] h[r,n]        (f32, assignment order)
+ * If topk_w or perm is NULL the plain result is written in row order instead:
+ *   y[r,i] = sum_n w2[e,i,n] h[r,n].
+ * h [T*k,ffn] bf16, y [T*k,d] f32.
+ */
+moe_status_t moe_swiglu_down(const moe_bf16_t* h, const int32_t* expert_offsets,
+                             const moe_bf16_t* w2, const float* topk_w, const int32_t* perm,
+                             int64_t T, int32_t d, int32_t ffn, int32_t E, int32_t k, float* y,
+                             hipStream_t stream);
+
+/*
+ * The grouped SwiGLU expert FFN on permuted rows: moe_swiglu_up(x_perm,
+ * perm = NULL) into h_ws, then moe_swiglu_down into y (same meaning of
+ * topk_w / perm as there).
+ * h_ws is caller scratch of T*k*ffn bf16.
+ */
+moe_status_t moe_grouped_swiglu(const moe_bf16_t* x_perm, const int32_t* expert_offsets,
+                                const moe_bf16_t* w1, const moe_bf16_t* w3,
+                                const moe_bf16_t* w2, const float* topk_w, const int32_t* perm,
+                                int64_t T, int32_t d, int32_t ffn, int32_t E, int32_t k,
+                                moe_bf16_t* h_ws, float* y, hipStream_t stream);
+
+/*
+ * Gate-weighted un-permute/combine: slots of a token are summed in ascending j
+ * in f32, after the optional residual:
+ *   s = (residual ? residual[t,i] : 0) + y[t*k+0,i] + ... + y[t*k+k-1,i]
+ *   out[t,i] = bf16(s) (if out), out_f32[t,i] = s (if out_f32).
+ * y [T*k,d] f32 in assignment order (already gate-weighted), residual/out_f32
+ * [T,d] f32, out [T,d] bf16.  At least one of out/out_f32.  out_f32 may equal
+ * residual (in-place residual update); nothing else may overlap.
+ */
+moe_status_t moe_combine(const float* y, const float* residual, int64_t T, int32_t d, int32_t k,
+                         moe_bf16_t* out, float* out_f32, hipStream_t stream);
+
+/*
+ * The whole layer: route -> SwiGLU experts (the gather of token rows is fused
+ * into the first expert GEMM) -> combine.  out [T,d] bf16, must not overlap
+ * any input.  Scratch is owned by the library, cached per device and grown on
+ * demand (a growth is refused with MOE_ERR_NO_MEMORY while `stream` is being
+ * captured into a graph; call once outside capture first).
+ */
+moe_status_t moe_forward(const moe_bf16_t* x, const moe_bf16_t* router_w, const moe_bf16_t* w1,
+                         const moe_bf16_t* w3, const moe_bf16_t* w2, int64_t T, int32_t d,
+                         int32_t ffn, int32_t E, int32_t k, moe_bf16_t* out, hipStream_t stream);
+
+/*
+ * moe_forward with the options of a residual block:
+ *   router_bias  [E] f32 or NULL;
+ *   residual     [T,d] f32 or NULL, added before rounding (see moe_combine);
+ *   out          [T,d] bf16 or NULL; out_f32 [T,d] f32 or NULL (at least one;
+ *                out_f32 may equal residual);
+ *   workspace    caller device scratch of at least
+ *                moe_workspace_size(T,d,ffn,E,k) bytes, 256-byte aligned, or
+ *                NULL for the library-owned scratch.
+ */
+moe_status_t moe_forward_ex(const moe_bf16_t* x, const moe_bf16_t* router_w,
+                            const float* router_bias, const moe_bf16_t* w1,
+                            const moe_bf16_t* w3, const moe_bf16_t* w2, int64_t T, int32_t d,
+                            int32_t ffn, int32_t E, int32_t k, const float* residual,
+                            moe_bf16_t* out, float* out_f32, void* workspace,
+                            size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * RMSNorm of the f32 residual stream, as in front of each MoE block of a
+ * pre-norm residual stack (Mixtral's layer structure, Sec. 4.1 citation):
+ *   a[t,i] = bf16( h[t,i] / sqrt(mean_i h[t,i]^2 + eps) * gamma[i] )
+ * h [T,d] f32, gamma [d] bf16, a [T,d] bf16, eps >= 0.
+ */
+moe_status_t moe_rmsnorm(const float* h, const moe_bf16_t* gamma, int64_t T, int32_t d, float eps,
+                         moe_bf16_t* a, hipStream_t stream);
+
+/* Bytes of scratch moe_forward_ex needs for these sizes (0 for invalid sizes). */
+size_t moe_workspace_size(int64_t T, int32_t d, int32_t ffn, int32_t E, int32_t k);
+
+/*
+ * Expert-GEMM kernel family used by moe_swiglu_up/down and the forward calls:
+ *   0 = automatic (by rows per expert, T*k/E), 1 = weight-streaming (decode
+ *   shapes), 2 = tiled (prefill shapes).  Process-wide; returns the previous
+ *   value, or -1 for an unknown value (nothing changed).  For testing and
+ *   measurement.
+ */
+int moe_set_gemm_variant(int variant);
+
+/* The kernel family (1 = weight-streaming, 2 = tiled) the expert GEMMs use
+ * for these sizes under the current moe_set_gemm_variant setting; 0 for
+ * invalid sizes.  Host-only, enqueues nothing. */
+int moe_gemm_variant_for(int64_t T, int32_t d, int32_t ffn, int32_t E, int32_t k);
+
+/* Static text of a status code. */
+const char* moe_status_string(int status);
+
+/* Message of the last error on the calling thread ("" if none). */
+const char* moe_last_error(void);
+
+/* Library version as major*10000 + minor*100 + patch. */
+int moe_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MOE_MI355X_H */

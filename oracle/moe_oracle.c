@@ -134,6 +134,24 @@ int oracle_topk_gate(const double* logits, int64_t T, int E, int k, int32_t* ids
     return ORACLE_OK;
 }
 
+/* Gate weights of a given expert choice (e.g. one made elsewhere):
+ * gates[t,j] = exp(l[t,ids[t,j]] - l[t,ids[t,0]]) / sum_m exp(l[t,ids[t,m]] - l[t,ids[t,0]]). */
+int oracle_gates_for_ids(const double* logits, const int32_t* ids, int64_t T, int E, int k,
+                         double* gates)
+{
+    if (T < 0 || E <= 0 || k <= 0 || k > E) return ORACLE_BAD_ARG;
+    for (int64_t t = 0; t < T; ++t) {
+        const double* l = logits + t * E;
+        const int32_t* s = ids + t * k;
+        for (int j = 0; j < k; ++j)
+            if (s[j] < 0 || s[j] >= E) return ORACLE_BAD_ARG;
+        double top = l[s[0]], denom = 0.0;
+        for (int j = 0; j < k; ++j) denom += exp(l[s[j]] - top);
+        for (int j = 0; j < k; ++j) gates[t * k + j] = exp(l[s[j]] - top) / denom;
+    }
+    return ORACLE_OK;
+}
+
 /* ---- dispatch: histogram, offsets, permutation ---------------------------- */
 
 /* Assignment a = t*k + j goes to expert ids[a].

@@ -50,13 +50,14 @@ class Oracle:
         L.oracle_threads.restype = ctypes.c_int
         L.oracle_router_logits.argtypes = [_p, _p, _p, _i64, _i64, _i64, _p]
         L.oracle_topk_gate.argtypes = [_p, _i64, ctypes.c_int, ctypes.c_int, _p, _p]
+        L.oracle_gates_for_ids.argtypes = [_p, _p, _i64, ctypes.c_int, ctypes.c_int, _p]
         L.oracle_dispatch.argtypes = [_p, _i64, ctypes.c_int, ctypes.c_int, _p, _p, _p]
         L.oracle_moe_apply.argtypes = [_p, _p, _p, _p, _p, _p, _i64, _i64, _i64,
                                        ctypes.c_int, ctypes.c_int, _p, _p, _p]
         L.oracle_moe_layer.argtypes = [_p, _p, _p, _p, _p, _p, _i64, _i64, _i64,
                                        ctypes.c_int, ctypes.c_int, _p, _p, _p, _p]
         L.oracle_rmsnorm.argtypes = [_p, _p, _i64, _i64, _f64, _p]
-        for f in ("oracle_router_logits", "oracle_topk_gate", "oracle_dispatch",
+        for f in ("oracle_router_logits", "oracle_topk_gate", "oracle_gates_for_ids", "oracle_dispatch",
                   "oracle_moe_apply", "oracle_moe_layer", "oracle_rmsnorm"):
             getattr(L, f).restype = ctypes.c_int
 
@@ -102,6 +103,16 @@ class Oracle:
         self._check(self.lib.oracle_topk_gate(self._ptr(logits), T, E, k, self._ptr(ids),
                                               self._ptr(gates)), "topk_gate")
         return ids, gates
+
+    def gates_for_ids(self, logits, ids):
+        logits = np.ascontiguousarray(logits, dtype=np.float64)
+        ids = np.ascontiguousarray(ids, dtype=np.int32)
+        T, E = logits.shape
+        k = ids.shape[1]
+        gates = np.empty((T, k), np.float64)
+        self._check(self.lib.oracle_gates_for_ids(self._ptr(logits), self._ptr(ids), T, E, k,
+                                                  self._ptr(gates)), "gates_for_ids")
+        return gates
 
     def dispatch(self, ids, E):
         ids = np.ascontiguousarray(ids, dtype=np.int32)

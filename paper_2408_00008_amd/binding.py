@@ -1,0 +1,199 @@
+"""ctypes binding of libmoe.so.
+
+Argument marshalling only: each function takes torch tensors that already live
+on the GPU, checks dtype/shape/contiguity, passes raw device pointers and the
+current HIP stream to the C ABI of the same name, and raises ``MoeError`` on a
+non-zero status.  Every step of the layer runs in the library's HIP kernels;
+there is no fallback path.  PyTorch provides device memory and streams only.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.environ.get("MOE_LIB", os.path.join(_PKG, "libmoe.so"))
+
+MOE_OK, MOE_ERR_INVALID_ARG, MOE_ERR_UNSUPPORTED, MOE_ERR_NO_MEMORY, MOE_ERR_HIP = range(5)
+VARIANT_AUTO, VARIANT_STREAM, VARIANT_TILED = 0, 1, 2
+
+EXPORTS = (
+    "moe_route", "moe_permute", "moe_swiglu_up", "moe_swiglu_down", "moe_grouped_swiglu",
+    "moe_combine", "moe_forward", "moe_forward_ex", "moe_rmsnorm", "moe_workspace_size",
+    "moe_set_gemm_variant", "moe_gemm_variant_for", "moe_status_string", "moe_last_error", "moe_version",
+)
+
+
+class MoeError(RuntimeError):
+    def __init__(self, status: int, fn: str, msg: str):
+        self.status = status
+        super().__init__(f"{fn}: {_status_name(status)}: {msg}")
+
+
+_lib = None
+
+
+def _status_name(s: int) -> str:
+    return lib().moe_status_string(s).decode()
+
+
+def lib() -> ctypes.CDLL:
+    """Load libmoe.so (built by ``python -m paper_2408_00008_amd.build``)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is missing: build it with "
+                          "`python -m paper_2408_00008_amd.build` (hipcc, gfx950)")
+    L = ctypes.CDLL(LIB_PATH)
+    p, i64, i32, f32, sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_float, ctypes.c_size_t
+    sig = {
+        "moe_route": [p, p, p, i64, i32, i32, i32, p, p, p, p, p, p],
+        "moe_permute": [p, p, i64, i32, i32, p, p],
+        "moe_swiglu_up": [p, p, p, p, p, i64, i32, i32, i32, i32, p, p],
+        "moe_swiglu_down": [p, p, p, p, p, i64, i32, i32, i32, i32, p, p],
+        "moe_grouped_swiglu": [p, p, p, p, p, p, p, i64, i32, i32, i32, i32, p, p, p],
+        "moe_combine": [p, p, i64, i32, i32, p, p, p],
+        "moe_forward": [p, p, p, p, p, i64, i32, i32, i32, i32, p, p],
+        "moe_forward_ex": [p, p, p, p, p, p, i64, i32, i32, i32, i32, p, p, p, p, sz, p],
+        "moe_rmsnorm": [p, p, i64, i32, f32, p, p],
+    }
+    for name, args in sig.items():
+        fn = getattr(L, name)
+        fn.argtypes = args
+        fn.restype = ctypes.c_int
+    L.moe_workspace_size.argtypes = [i64, i32, i32, i32, i32]
+    L.moe_workspace_size.restype = sz
+    L.moe_gemm_variant_for.argtypes = [i64, i32, i32, i32, i32]
+    L.moe_gemm_variant_for.restype = ctypes.c_int
+    L.moe_set_gemm_variant.argtypes = [ctypes.c_int]
+    L.moe_set_gemm_variant.restype = ctypes.c_int
+    L.moe_status_string.argtypes = [ctypes.c_int]
+    L.moe_status_string.restype = ctypes.c_char_p
+    L.moe_last_error.argtypes = []
+    L.moe_last_error.restype = ctypes.c_char_p
+    L.moe_version.argtypes = []
+    L.moe_version.restype = ctypes.c_int
+    _lib = L
+    return L
+
+
+def _check(status: int, fn: str):
+    if status != MOE_OK:
+        raise MoeError(status, fn, lib().moe_last_error().decode())
+
+
+def _ptr(t: Optional[torch.Tensor], dtype=None, name="tensor"):
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a GPU tensor")
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return t.data_ptr()
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, torch.cuda.Stream):
+        return stream.cuda_stream
+    return int(stream)
+
+
+bf16, f32, i32 = torch.bfloat16, torch.float32, torch.int32
+
+
+def moe_route(x, router_w, k, topk_ids, topk_w, expert_offsets, perm, router_bias=None,
+              logits=None, stream=None):
+    T, d = x.shape
+    E = router_w.shape[0]
+    _check(lib().moe_route(_ptr(x, bf16, "x"), _ptr(router_w, bf16, "router_w"),
+                           _ptr(router_bias, f32, "router_bias"), T, d, E, k,
+                           _ptr(topk_ids, i32, "topk_ids"), _ptr(topk_w, f32, "topk_w"),
+                           _ptr(expert_offsets, i32, "expert_offsets"), _ptr(perm, i32, "perm"),
+                           _ptr(logits, f32, "logits"), _stream(stream)), "moe_route")
+
+
+def moe_permute(x, perm, k, x_perm, stream=None):
+    T, d = x.shape
+    _check(lib().moe_permute(_ptr(x, bf16, "x"), _ptr(perm, i32, "perm"), T, d, k,
+                             _ptr(x_perm, bf16, "x_perm"), _stream(stream)), "moe_permute")
+
+
+def moe_swiglu_up(x, expert_offsets, w1, w3, T, k, h, perm=None, stream=None):
+    """x: permuted rows [T*k,d] (perm None) or token rows [T,d] gathered via perm."""
+    E, ffn, d = w1.shape
+    _check(lib().moe_swiglu_up(_ptr(x, bf16, "x"), _ptr(perm, i32, "perm"),
+                               _ptr(expert_offsets, i32, "offsets"), _ptr(w1, bf16, "w1"),
+                               _ptr(w3, bf16, "w3"), T, d, ffn, E, k, _ptr(h, bf16, "h"),
+                               _stream(stream)), "moe_swiglu_up")
+
+
+def moe_swiglu_down(h, expert_offsets, w2, T, k, y, topk_w=None, perm=None, stream=None):
+    E, d, ffn = w2.shape
+    _check(lib().moe_swiglu_down(_ptr(h, bf16, "h"), _ptr(expert_offsets, i32, "offsets"),
+                                 _ptr(w2, bf16, "w2"), _ptr(topk_w, f32, "topk_w"),
+                                 _ptr(perm, i32, "perm"), T, d, ffn, E, k, _ptr(y, f32, "y"),
+                                 _stream(stream)), "moe_swiglu_down")
+
+
+def moe_grouped_swiglu(x_perm, expert_offsets, w1, w3, w2, T, k, h_ws, y, topk_w=None,
+                       perm=None, stream=None):
+    E, ffn, d = w1.shape
+    _check(lib().moe_grouped_swiglu(
+        _ptr(x_perm, bf16, "x_perm"), _ptr(expert_offsets, i32, "offsets"), _ptr(w1, bf16, "w1"),
+        _ptr(w3, bf16, "w3"), _ptr(w2, bf16, "w2"), _ptr(topk_w, f32, "topk_w"),
+        _ptr(perm, i32, "perm"), T, d, ffn, E, k, _ptr(h_ws, bf16, "h_ws"), _ptr(y, f32, "y"),
+        _stream(stream)), "moe_grouped_swiglu")
+
+
+def moe_combine(y, T, d, k, out=None, out_f32=None, residual=None, stream=None):
+    _check(lib().moe_combine(_ptr(y, f32, "y"), _ptr(residual, f32, "residual"), T, d, k,
+                             _ptr(out, bf16, "out"), _ptr(out_f32, f32, "out_f32"),
+                             _stream(stream)), "moe_combine")
+
+
+def moe_forward(x, router_w, w1, w3, w2, k, out, stream=None):
+    T, d = x.shape
+    E, ffn, _ = w1.shape
+    _check(lib().moe_forward(_ptr(x, bf16, "x"), _ptr(router_w, bf16, "router_w"),
+                             _ptr(w1, bf16, "w1"), _ptr(w3, bf16, "w3"), _ptr(w2, bf16, "w2"),
+                             T, d, ffn, E, k, _ptr(out, bf16, "out"), _stream(stream)),
+           "moe_forward")
+
+
+def moe_forward_ex(x, router_w, w1, w3, w2, k, out=None, out_f32=None, router_bias=None,
+                   residual=None, workspace=None, stream=None):
+    T, d = x.shape
+    E, ffn, _ = w1.shape
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(lib().moe_forward_ex(
+        _ptr(x, bf16, "x"), _ptr(router_w, bf16, "router_w"), _ptr(router_bias, f32, "router_bias"),
+        _ptr(w1, bf16, "w1"), _ptr(w3, bf16, "w3"), _ptr(w2, bf16, "w2"), T, d, ffn, E, k,
+        _ptr(residual, f32, "residual"), _ptr(out, bf16, "out"), _ptr(out_f32, f32, "out_f32"),
+        _ptr(workspace, None, "workspace"), ws_bytes, _stream(stream)), "moe_forward_ex")
+
+
+def moe_rmsnorm(h, gamma, eps, a, stream=None):
+    T, d = h.shape
+    _check(lib().moe_rmsnorm(_ptr(h, f32, "h"), _ptr(gamma, bf16, "gamma"), T, d, float(eps),
+                             _ptr(a, bf16, "a"), _stream(stream)), "moe_rmsnorm")
+
+
+def moe_workspace_size(T, d, ffn, E, k) -> int:
+    return int(lib().moe_workspace_size(T, d, ffn, E, k))
+
+
+def moe_gemm_variant_for(T, d, ffn, E, k) -> int:
+    return int(lib().moe_gemm_variant_for(T, d, ffn, E, k))
+
+
+def moe_set_gemm_variant(v: int) -> int:
+    return int(lib().moe_set_gemm_variant(v))

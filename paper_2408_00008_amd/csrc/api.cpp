@@ -1,0 +1,510 @@
+// C ABI of libmoe: argument validation, scratch management and kernel
+// sequencing.  Every check runs before the first HIP call, so a rejected call
+// enqueues nothing and touches no device state.
+#include "moe.h"
+
+#include <hip/hip_runtime.h>
+
+#include <atomic>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+#include <string>
+#include <unordered_map>
+
+#include "launch.hpp"
+
+namespace moe {
+hipError_t launch_stream_up(const UpArgs& a, int64_t rows_max, hipStream_t stream);
+hipError_t launch_stream_down(const DownArgs& a, int64_t rows_max, hipStream_t stream);
+hipError_t launch_tiled_up(const UpArgs& a, hipStream_t stream);
+hipError_t launch_tiled_down(const DownArgs& a, hipStream_t stream);
+bool tiled_supported(int d, int ffn);
+}  // namespace moe
+
+namespace {
+
+thread_local std::string g_last_error;
+std::atomic<int> g_variant{moe::VARIANT_AUTO};
+
+moe_status_t fail(moe_status_t s, const char* fmt, ...)
+{
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_last_error = buf;
+    return s;
+}
+
+moe_status_t ok()
+{
+    g_last_error.clear();
+    return MOE_OK;
+}
+
+moe_status_t hip_fail(hipError_t e, const char* what)
+{
+    return fail(MOE_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+struct Range {
+    const void* p;
+    size_t bytes;
+};
+
+bool overlap(Range a, Range b)
+{
+    if (!a.p || !b.p || a.bytes == 0 || b.bytes == 0) return false;
+    const uintptr_t a0 = reinterpret_cast<uintptr_t>(a.p), b0 = reinterpret_cast<uintptr_t>(b.p);
+    return a0 < b0 + b.bytes && b0 < a0 + a.bytes;
+}
+
+constexpr int kMaxE = 64, kMaxK = 8, kMaxDim = 65536;
+
+moe_status_t check_T(int64_t T, int32_t k)
+{
+    if (T < 0) return fail(MOE_ERR_INVALID_ARG, "T=%lld must be >= 0", (long long)T);
+    if (k >= 1 && T * (int64_t)k >= (int64_t(1) << 31))
+        return fail(MOE_ERR_UNSUPPORTED, "T*k=%lld must be < 2^31", (long long)(T * k));
+    return MOE_OK;
+}
+
+moe_status_t check_Ek(int32_t E, int32_t k)
+{
+    if (E < 1) return fail(MOE_ERR_INVALID_ARG, "E=%d must be >= 1", E);
+    if (E > kMaxE) return fail(MOE_ERR_UNSUPPORTED, "E=%d exceeds %d", E, kMaxE);
+    if (k < 1) return fail(MOE_ERR_INVALID_ARG, "k=%d must be >= 1", k);
+    if (k > E) return fail(MOE_ERR_INVALID_ARG, "k=%d exceeds E=%d", k, E);
+    if (k > kMaxK) return fail(MOE_ERR_UNSUPPORTED, "k=%d exceeds %d", k, kMaxK);
+    return MOE_OK;
+}
+
+moe_status_t check_dim(const char* name, int32_t v)
+{
+    if (v < 1) return fail(MOE_ERR_INVALID_ARG, "%s=%d must be >= 1", name, v);
+    if (v % 64 != 0) return fail(MOE_ERR_UNSUPPORTED, "%s=%d must be a multiple of 64", name, v);
+    if (v > kMaxDim) return fail(MOE_ERR_UNSUPPORTED, "%s=%d exceeds %d", name, v, kMaxDim);
+    return MOE_OK;
+}
+
+#define TRY(expr)                      \
+    do {                               \
+        moe_status_t s_ = (expr);      \
+        if (s_ != MOE_OK) return s_;   \
+    } while (0)
+
+moe_status_t need(const void* p, const char* name)
+{
+    if (!p) return fail(MOE_ERR_INVALID_ARG, "%s is NULL", name);
+    if (!aligned16(p)) return fail(MOE_ERR_INVALID_ARG, "%s is not 16-byte aligned", name);
+    return MOE_OK;
+}
+
+moe_status_t maybe(const void* p, const char* name)
+{
+    if (p && !aligned16(p)) return fail(MOE_ERR_INVALID_ARG, "%s is not 16-byte aligned", name);
+    return MOE_OK;
+}
+
+// a buffer whose size scales with T: may be NULL when T == 0
+moe_status_t need_rows(const void* p, const char* name, int64_t T)
+{
+    return T == 0 ? maybe(p, name) : need(p, name);
+}
+
+moe_status_t no_overlap(const char* oname, Range o, std::initializer_list<std::pair<const char*, Range>> ins)
+{
+    for (const auto& in : ins)
+        if (overlap(o, in.second))
+            return fail(MOE_ERR_INVALID_ARG, "%s overlaps %s", oname, in.first);
+    return MOE_OK;
+}
+
+// ---- workspace ------------------------------------------------------------
+
+size_t align256(size_t v) { return (v + 255) & ~size_t(255); }
+
+struct Layout {
+    size_t ids, w, off, perm, h, y, total;
+};
+
+Layout layout(int64_t T, int32_t d, int32_t ffn, int32_t E, int32_t k)
+{
+    const size_t A = static_cast<size_t>(T) * k;
+    Layout L{};
+    size_t o = 0;
+    L.ids = o;  o += align256(A * 4);
+    L.w = o;    o += align256(A * 4);
+    L.off = o;  o += align256(static_cast<size_t>(E + 1) * 4);
+    L.perm = o; o += align256(A * 4);
+    L.h = o;    o += align256(A * static_cast<size_t>(ffn) * 2);
+    L.y = o;    o += align256(A * static_cast<size_t>(d) * 4);
+    L.total = o;
+    return L;
+}
+
+struct DeviceScratch {
+    void* ptr = nullptr;
+    size_t bytes = 0;
+};
+std::mutex g_ws_mu;
+std::unordered_map<int, DeviceScratch> g_ws;
+
+moe_status_t library_workspace(size_t need_bytes, hipStream_t stream, void** out)
+{
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    std::lock_guard<std::mutex> lk(g_ws_mu);
+    DeviceScratch& s = g_ws[dev];
+    if (s.bytes < need_bytes) {
+        hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+        e = hipStreamIsCapturing(stream, &cs);
+        if (e != hipSuccess) return hip_fail(e, "hipStreamIsCapturing");
+        if (cs != hipStreamCaptureStatusNone)
+            return fail(MOE_ERR_NO_MEMORY,
+                        "library scratch must grow to %zu bytes while the stream is being "
+                        "captured; call once outside capture first",
+                        need_bytes);
+        if (s.ptr) {
+            // earlier work on any stream may still use the old buffer
+            e = hipDeviceSynchronize();
+            if (e != hipSuccess) return hip_fail(e, "hipDeviceSynchronize");
+            (void)hipFree(s.ptr);
+            s.ptr = nullptr;
+            s.bytes = 0;
+        }
+        const size_t grow = need_bytes + need_bytes / 4;
+        e = hipMalloc(&s.ptr, grow);
+        if (e != hipSuccess) {
+            s.ptr = nullptr;
+            return fail(MOE_ERR_NO_MEMORY, "hipMalloc(%zu) failed: %s", grow, hipGetErrorString(e));
+        }
+        s.bytes = grow;
+    }
+    *out = s.ptr;
+    return MOE_OK;
+}
+
+int64_t rows_bound(int64_t T, int32_t) { return T; }
+
+hipError_t run_up(const moe::UpArgs& a, int64_t T, hipStream_t stream)
+{
+    const int v = moe::resolve_variant(g_variant.load(), a.A, a.E);
+    if (v == moe::VARIANT_TILED && moe::tiled_supported(a.d, a.ffn))
+        return moe::launch_tiled_up(a, stream);
+    return moe::launch_stream_up(a, rows_bound(T, a.kslots), stream);
+}
+
+hipError_t run_down(const moe::DownArgs& a, int64_t T, int32_t k, hipStream_t stream)
+{
+    const int v = moe::resolve_variant(g_variant.load(), a.A, a.E);
+    if (v == moe::VARIANT_TILED && moe::tiled_supported(a.d, a.ffn))
+        return moe::launch_tiled_down(a, stream);
+    return moe::launch_stream_down(a, rows_bound(T, k), stream);
+}
+
+}  // namespace
+
+namespace moe {
+int resolve_variant(int requested, int64_t A, int E)
+{
+    if (requested == VARIANT_STREAM || requested == VARIANT_TILED) return requested;
+    // weight streaming while an expert's rows are few: rows/expert below the
+    // point where MFMA work, not weight bytes, dominates
+    return (A <= 128LL * E) ? VARIANT_STREAM : VARIANT_TILED;
+}
+}  // namespace moe
+
+extern "C" {
+
+moe_status_t moe_route(const moe_bf16_t* x, const moe_bf16_t* router_w, const float* router_bias,
+                       int64_t T, int32_t d, int32_t E, int32_t k, int32_t* topk_ids,
+                       float* topk_w, int32_t* expert_offsets, int32_t* perm, float* logits,
+                       hipStream_t stream)
+{
+    TRY(check_Ek(E, k));
+    TRY(check_T(T, k));
+    TRY(check_dim("d", d));
+    TRY(need_rows(x, "x", T));
+    TRY(need(router_w, "router_w"));
+    TRY(maybe(router_bias, "router_bias"));
+    TRY(need_rows(topk_ids, "topk_ids", T));
+    TRY(need_rows(topk_w, "topk_w", T));
+    TRY(need(expert_offsets, "expert_offsets"));
+    TRY(need_rows(perm, "perm", T));
+    TRY(maybe(logits, "logits"));
+    const size_t A = static_cast<size_t>(T) * k;
+    TRY(no_overlap("topk_ids", {topk_ids, A * 4}, {{"topk_w", {topk_w, A * 4}}, {"perm", {perm, A * 4}},
+                   {"expert_offsets", {expert_offsets, (size_t)(E + 1) * 4}}}));
+    TRY(no_overlap("perm", {perm, A * 4}, {{"topk_w", {topk_w, A * 4}},
+                   {"expert_offsets", {expert_offsets, (size_t)(E + 1) * 4}}}));
+    if (T == 0) return ok();
+    hipError_t e = moe::launch_router_topk(x, router_w, router_bias, T, d, E, k, topk_ids, topk_w,
+                                           logits, stream);
+    if (e != hipSuccess) return hip_fail(e, "router kernel launch");
+    e = moe::launch_dispatch(topk_ids, static_cast<int64_t>(A), E, expert_offsets, perm, stream);
+    if (e != hipSuccess) return hip_fail(e, "dispatch kernel launch");
+    return ok();
+}
+
+moe_status_t moe_permute(const moe_bf16_t* x, const int32_t* perm, int64_t T, int32_t d,
+                         int32_t k, moe_bf16_t* x_perm, hipStream_t stream)
+{
+    if (k < 1 || k > kMaxK) return fail(k < 1 ? MOE_ERR_INVALID_ARG : MOE_ERR_UNSUPPORTED,
+                                        "k=%d out of range", k);
+    TRY(check_T(T, k));
+    TRY(check_dim("d", d));
+    TRY(need_rows(x, "x", T));
+    TRY(need_rows(perm, "perm", T));
+    TRY(need_rows(x_perm, "x_perm", T));
+    const size_t A = static_cast<size_t>(T) * k;
+    TRY(no_overlap("x_perm", {x_perm, A * d * 2}, {{"x", {x, (size_t)T * d * 2}}, {"perm", {perm, A * 4}}}));
+    if (T == 0) return ok();
+    hipError_t e = moe::launch_permute(x, perm, static_cast<int64_t>(A), d, k, x_perm, stream);
+    return e == hipSuccess ? ok() : hip_fail(e, "permute kernel launch");
+}
+
+moe_status_t moe_swiglu_up(const moe_bf16_t* x_perm, const int32_t* perm,
+                           const int32_t* expert_offsets, const moe_bf16_t* w1,
+                           const moe_bf16_t* w3, int64_t T, int32_t d, int32_t ffn, int32_t E,
+                           int32_t k, moe_bf16_t* h, hipStream_t stream)
+{
+    TRY(check_Ek(E, k));
+    TRY(check_T(T, k));
+    TRY(check_dim("d", d));
+    TRY(check_dim("ffn", ffn));
+    TRY(need_rows(x_perm, "x_perm", T));
+    TRY(need(expert_offsets, "expert_offsets"));
+    TRY(need(w1, "w1"));
+    TRY(need(w3, "w3"));
+    TRY(need_rows(h, "h", T));
+    TRY(maybe(perm, "perm"));
+    const size_t A = static_cast<size_t>(T) * k;
+    const size_t wbytes = (size_t)E * ffn * d * 2;
+    const size_t xrows = perm ? static_cast<size_t>(T) : A;
+    TRY(no_overlap("h", {h, A * ffn * 2}, {{"x", {x_perm, xrows * d * 2}}, {"w1", {w1, wbytes}},
+                   {"w3", {w3, wbytes}}, {"expert_offsets", {expert_offsets, (size_t)(E + 1) * 4}},
+                   {"perm", {perm, A * 4}}}));
+    if (T == 0) return ok();
+    moe::UpArgs a{x_perm, perm, k, expert_offsets, w1, w3, h, (int64_t)A, d, ffn, E};
+    hipError_t e = run_up(a, T, stream);
+    return e == hipSuccess ? ok() : hip_fail(e, "expert up kernel launch");
+}
+
+moe_status_t moe_swiglu_down(const moe_bf16_t* h, const int32_t* expert_offsets,
+                             const moe_bf16_t* w2, const float* topk_w, const int32_t* perm,
+                             int64_t T, int32_t d, int32_t ffn, int32_t E, int32_t k, float* y,
+                             hipStream_t stream)
+{
+    TRY(check_Ek(E, k));
+    TRY(check_T(T, k));
+    TRY(check_dim("d", d));
+    TRY(check_dim("ffn", ffn));
+    TRY(need_rows(h, "h", T));
+    TRY(need(expert_offsets, "expert_offsets"));
+    TRY(need(w2, "w2"));
+    TRY(maybe(topk_w, "topk_w"));
+    TRY(maybe(perm, "perm"));
+    TRY(need_rows(y, "y", T));
+    const size_t A = static_cast<size_t>(T) * k;
+    TRY(no_overlap("y", {y, A * d * 4}, {{"h", {h, A * ffn * 2}}, {"w2", {w2, (size_t)E * d * ffn * 2}},
+                   {"topk_w", {topk_w, A * 4}}, {"perm", {perm, A * 4}},
+                   {"expert_offsets", {expert_offsets, (size_t)(E + 1) * 4}}}));
+    if (T == 0) return ok();
+    const bool scatter = topk_w && perm;
+    moe::DownArgs a{h, expert_offsets, w2, scatter ? topk_w : nullptr, scatter ? perm : nullptr,
+                    y, (int64_t)A, d, ffn, E};
+    hipError_t e = run_down(a, T, k, stream);
+    return e == hipSuccess ? ok() : hip_fail(e, "expert down kernel launch");
+}
+
+moe_status_t moe_grouped_swiglu(const moe_bf16_t* x_perm, const int32_t* expert_offsets,
+                                const moe_bf16_t* w1, const moe_bf16_t* w3,
+                                const moe_bf16_t* w2, const float* topk_w, const int32_t* perm,
+                                int64_t T, int32_t d, int32_t ffn, int32_t E, int32_t k,
+                                moe_bf16_t* h_ws, float* y, hipStream_t stream)
+{
+    TRY(check_Ek(E, k));
+    TRY(check_T(T, k));
+    TRY(check_dim("d", d));
+    TRY(check_dim("ffn", ffn));
+    TRY(need(w2, "w2"));
+    TRY(need_rows(y, "y", T));
+    TRY(maybe(topk_w, "topk_w"));
+    TRY(maybe(perm, "perm"));
+    const size_t A = static_cast<size_t>(T) * k;
+    TRY(no_overlap("y", {y, A * d * 4}, {{"h_ws", {h_ws, A * ffn * 2}}, {"x_perm", {x_perm, A * d * 2}}}));
+    moe_status_t s =
+        moe_swiglu_up(x_perm, nullptr, expert_offsets, w1, w3, T, d, ffn, E, k, h_ws, stream);
+    if (s != MOE_OK) return s;
+    return moe_swiglu_down(h_ws, expert_offsets, w2, topk_w, perm, T, d, ffn, E, k, y, stream);
+}
+
+moe_status_t moe_combine(const float* y, const float* residual, int64_t T, int32_t d, int32_t k,
+                         moe_bf16_t* out, float* out_f32, hipStream_t stream)
+{
+    if (k < 1 || k > kMaxK) return fail(k < 1 ? MOE_ERR_INVALID_ARG : MOE_ERR_UNSUPPORTED,
+                                        "k=%d out of range", k);
+    TRY(check_T(T, k));
+    TRY(check_dim("d", d));
+    TRY(need_rows(y, "y", T));
+    TRY(maybe(residual, "residual"));
+    TRY(maybe(out, "out"));
+    TRY(maybe(out_f32, "out_f32"));
+    if (!out && !out_f32) return fail(MOE_ERR_INVALID_ARG, "out and out_f32 are both NULL");
+    const size_t A = static_cast<size_t>(T) * k;
+    const size_t td = static_cast<size_t>(T) * d;
+    TRY(no_overlap("out", {out, td * 2}, {{"y", {y, A * d * 4}}, {"residual", {residual, td * 4}},
+                   {"out_f32", {out_f32, td * 4}}}));
+    if (out_f32 != residual)
+        TRY(no_overlap("out_f32", {out_f32, td * 4}, {{"y", {y, A * d * 4}}, {"residual", {residual, td * 4}}}));
+    else
+        TRY(no_overlap("out_f32", {out_f32, td * 4}, {{"y", {y, A * d * 4}}}));
+    if (T == 0) return ok();
+    hipError_t e = moe::launch_combine(y, residual, T, d, k, out, out_f32, stream);
+    return e == hipSuccess ? ok() : hip_fail(e, "combine kernel launch");
+}
+
+size_t moe_workspace_size(int64_t T, int32_t d, int32_t ffn, int32_t E, int32_t k)
+{
+    if (T < 0 || E < 1 || E > kMaxE || k < 1 || k > E || k > kMaxK || d < 1 || ffn < 1 ||
+        T * (int64_t)k >= (int64_t(1) << 31))
+        return 0;
+    return layout(T, d, ffn, E, k).total;
+}
+
+moe_status_t moe_forward_ex(const moe_bf16_t* x, const moe_bf16_t* router_w,
+                            const float* router_bias, const moe_bf16_t* w1,
+                            const moe_bf16_t* w3, const moe_bf16_t* w2, int64_t T, int32_t d,
+                            int32_t ffn, int32_t E, int32_t k, const float* residual,
+                            moe_bf16_t* out, float* out_f32, void* workspace,
+                            size_t workspace_bytes, hipStream_t stream)
+{
+    TRY(check_Ek(E, k));
+    TRY(check_T(T, k));
+    TRY(check_dim("d", d));
+    TRY(check_dim("ffn", ffn));
+    TRY(need_rows(x, "x", T));
+    TRY(need(router_w, "router_w"));
+    TRY(maybe(router_bias, "router_bias"));
+    TRY(need(w1, "w1"));
+    TRY(need(w3, "w3"));
+    TRY(need(w2, "w2"));
+    TRY(maybe(residual, "residual"));
+    TRY(maybe(out, "out"));
+    TRY(maybe(out_f32, "out_f32"));
+    if (!out && !out_f32) return fail(MOE_ERR_INVALID_ARG, "out and out_f32 are both NULL");
+    if (workspace && (reinterpret_cast<uintptr_t>(workspace) & 255u))
+        return fail(MOE_ERR_INVALID_ARG, "workspace is not 256-byte aligned");
+    const size_t td = static_cast<size_t>(T) * d;
+    const size_t wbytes = (size_t)E * ffn * d * 2;
+    const std::initializer_list<std::pair<const char*, Range>> ins = {
+        {"x", {x, td * 2}}, {"router_w", {router_w, (size_t)E * d * 2}},
+        {"router_bias", {router_bias, (size_t)E * 4}}, {"w1", {w1, wbytes}},
+        {"w3", {w3, wbytes}}, {"w2", {w2, wbytes}}};
+    TRY(no_overlap("out", {out, td * 2}, ins));
+    TRY(no_overlap("out", {out, td * 2}, {{"residual", {residual, td * 4}}, {"out_f32", {out_f32, td * 4}}}));
+    TRY(no_overlap("out_f32", {out_f32, td * 4}, ins));
+    if (residual && out_f32 != residual)
+        TRY(no_overlap("out_f32", {out_f32, td * 4}, {{"residual", {residual, td * 4}}}));
+    const Layout L = layout(T, d, ffn, E, k);
+    if (workspace && workspace_bytes < L.total)
+        return fail(MOE_ERR_NO_MEMORY, "workspace of %zu bytes is smaller than the %zu needed",
+                    workspace_bytes, L.total);
+    if (workspace) {
+        const Range ws{workspace, L.total};
+        TRY(no_overlap("workspace", ws, ins));
+        TRY(no_overlap("workspace", ws, {{"out", {out, td * 2}}, {"out_f32", {out_f32, td * 4}},
+                       {"residual", {residual, td * 4}}}));
+    }
+    if (T == 0) return ok();
+
+    void* base = workspace;
+    if (!base) TRY(library_workspace(L.total, stream, &base));
+    char* b = static_cast<char*>(base);
+    int32_t* ids = reinterpret_cast<int32_t*>(b + L.ids);
+    float* gw = reinterpret_cast<float*>(b + L.w);
+    int32_t* offs = reinterpret_cast<int32_t*>(b + L.off);
+    int32_t* perm = reinterpret_cast<int32_t*>(b + L.perm);
+    moe::bf16_t* h = reinterpret_cast<moe::bf16_t*>(b + L.h);
+    float* y = reinterpret_cast<float*>(b + L.y);
+    const int64_t A = T * k;
+
+    hipError_t e = moe::launch_router_topk(x, router_w, router_bias, T, d, E, k, ids, gw, nullptr,
+                                           stream);
+    if (e != hipSuccess) return hip_fail(e, "router kernel launch");
+    e = moe::launch_dispatch(ids, A, E, offs, perm, stream);
+    if (e != hipSuccess) return hip_fail(e, "dispatch kernel launch");
+    moe::UpArgs ua{x, perm, k, offs, w1, w3, h, A, d, ffn, E};
+    e = run_up(ua, T, stream);
+    if (e != hipSuccess) return hip_fail(e, "expert up kernel launch");
+    moe::DownArgs da{h, offs, w2, gw, perm, y, A, d, ffn, E};
+    e = run_down(da, T, k, stream);
+    if (e != hipSuccess) return hip_fail(e, "expert down kernel launch");
+    e = moe::launch_combine(y, residual, T, d, k, out, out_f32, stream);
+    if (e != hipSuccess) return hip_fail(e, "combine kernel launch");
+    return ok();
+}
+
+moe_status_t moe_forward(const moe_bf16_t* x, const moe_bf16_t* router_w, const moe_bf16_t* w1,
+                         const moe_bf16_t* w3, const moe_bf16_t* w2, int64_t T, int32_t d,
+                         int32_t ffn, int32_t E, int32_t k, moe_bf16_t* out, hipStream_t stream)
+{
+    TRY(need_rows(out, "out", T));
+    return moe_forward_ex(x, router_w, nullptr, w1, w3, w2, T, d, ffn, E, k, nullptr, out,
+                          nullptr, nullptr, 0, stream);
+}
+
+moe_status_t moe_rmsnorm(const float* h, const moe_bf16_t* gamma, int64_t T, int32_t d, float eps,
+                         moe_bf16_t* a, hipStream_t stream)
+{
+    if (T < 0) return fail(MOE_ERR_INVALID_ARG, "T=%lld must be >= 0", (long long)T);
+    TRY(check_dim("d", d));
+    if (!(eps >= 0.0f)) return fail(MOE_ERR_INVALID_ARG, "eps must be >= 0");
+    TRY(need_rows(h, "h", T));
+    TRY(need(gamma, "gamma"));
+    TRY(need_rows(a, "a", T));
+    const size_t td = static_cast<size_t>(T) * d;
+    TRY(no_overlap("a", {a, td * 2}, {{"h", {h, td * 4}}, {"gamma", {gamma, (size_t)d * 2}}}));
+    if (T == 0) return ok();
+    hipError_t e = moe::launch_rmsnorm(h, gamma, T, d, eps, a, stream);
+    return e == hipSuccess ? ok() : hip_fail(e, "rmsnorm kernel launch");
+}
+
+int moe_gemm_variant_for(int64_t T, int32_t d, int32_t ffn, int32_t E, int32_t k)
+{
+    if (moe_workspace_size(T, d, ffn, E, k) == 0 || d % 64 || ffn % 64) return 0;
+    const int v = moe::resolve_variant(g_variant.load(), T * k, E);
+    return (v == moe::VARIANT_TILED && moe::tiled_supported(d, ffn)) ? moe::VARIANT_TILED
+                                                                     : moe::VARIANT_STREAM;
+}
+
+int moe_set_gemm_variant(int variant)
+{
+    if (variant < moe::VARIANT_AUTO || variant > moe::VARIANT_TILED) return -1;
+    return g_variant.exchange(variant);
+}
+
+const char* moe_status_string(int status)
+{
+    switch (status) {
+    case MOE_OK: return "MOE_OK";
+    case MOE_ERR_INVALID_ARG: return "MOE_ERR_INVALID_ARG";
+    case MOE_ERR_UNSUPPORTED: return "MOE_ERR_UNSUPPORTED";
+    case MOE_ERR_NO_MEMORY: return "MOE_ERR_NO_MEMORY";
+    case MOE_ERR_HIP: return "MOE_ERR_HIP";
+    default: return "MOE_ERR_UNKNOWN";
+    }
+}
+
+const char* moe_last_error(void) { return g_last_error.c_str(); }
+
+int moe_version(void) { return 100; }
+
+}  // extern "C"

@@ -1,0 +1,130 @@
+// Row gather, slot combine and RMSNorm for gfx950: HBM-bound copies, written
+// as grid-stride loops of 16-byte vector accesses so consecutive lanes touch
+// consecutive bytes of a row.
+#include "common.hpp"
+#include "launch.hpp"
+
+namespace moe {
+
+namespace {
+
+// x_perm[r,:] = x[perm[r] / k, :]
+__global__ __launch_bounds__(256) void permute_kernel(const bf16_t* __restrict__ x,
+                                                      const int32_t* __restrict__ perm, int64_t A,
+                                                      int d, int k, bf16_t* __restrict__ x_perm)
+{
+    const int cpr = d >> 3;  // 16-byte chunks per row
+    const int64_t total = A * cpr;
+    for (int64_t q = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; q < total;
+         q += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t r = q / cpr;
+        const int c = static_cast<int>(q - r * cpr);
+        const int64_t t = perm[r] / k;
+        *reinterpret_cast<uint4*>(x_perm + r * d + c * 8) = ldg16(x + t * d + c * 8);
+    }
+}
+
+// s = residual + sum_{j ascending} y[t*k+j]; out = bf16(s), out_f32 = s
+__global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ y,
+                                                      const float* residual, int64_t T, int d,
+                                                      int k, bf16_t* __restrict__ out,
+                                                      float* out_f32)
+{
+    const int cpr = d >> 2;  // float4 per row
+    const int64_t total = T * cpr;
+    for (int64_t q = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; q < total;
+         q += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t t = q / cpr;
+        const int c = static_cast<int>(q - t * cpr);
+        float4 s = residual ? *reinterpret_cast<const float4*>(residual + t * d + c * 4)
+                            : make_float4(0.f, 0.f, 0.f, 0.f);
+        for (int j = 0; j < k; ++j) {
+            const float4 v = *reinterpret_cast<const float4*>(y + (t * k + j) * d + c * 4);
+            s.x += v.x;
+            s.y += v.y;
+            s.z += v.z;
+            s.w += v.w;
+        }
+        if (out) {
+            uint2 p;
+            p.x = pack_bf16x2(s.x, s.y);
+            p.y = pack_bf16x2(s.z, s.w);
+            *reinterpret_cast<uint2*>(out + t * d + c * 4) = p;
+        }
+        if (out_f32) *reinterpret_cast<float4*>(out_f32 + t * d + c * 4) = s;
+    }
+}
+
+// a = bf16(h * rsqrt(mean(h^2) + eps) * gamma), one workgroup per row
+__global__ __launch_bounds__(256) void rmsnorm_kernel(const float* __restrict__ h,
+                                                      const bf16_t* __restrict__ gamma, int64_t T,
+                                                      int d, float eps, bf16_t* __restrict__ a)
+{
+    __shared__ float red[4];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    for (int64_t t = blockIdx.x; t < T; t += gridDim.x) {
+        const float* hr = h + t * d;
+        float ss = 0.0f;
+        for (int c = tid; c < (d >> 2); c += 256) {
+            const float4 v = *reinterpret_cast<const float4*>(hr + c * 4);
+            ss = fmaf(v.x, v.x, ss);
+            ss = fmaf(v.y, v.y, ss);
+            ss = fmaf(v.z, v.z, ss);
+            ss = fmaf(v.w, v.w, ss);
+        }
+#pragma unroll
+        for (int m = 32; m >= 1; m >>= 1) ss += __shfl_xor(ss, m, 64);
+        if (lane == 0) red[wave] = ss;
+        __syncthreads();
+        const float tot = (red[0] + red[1]) + (red[2] + red[3]);
+        const float inv = 1.0f / sqrtf(tot / static_cast<float>(d) + eps);
+        for (int c = tid; c < (d >> 2); c += 256) {
+            const float4 v = *reinterpret_cast<const float4*>(hr + c * 4);
+            const uint2 g = *reinterpret_cast<const uint2*>(gamma + c * 4);
+            uint2 p;
+            p.x = pack_bf16x2(v.x * inv * __uint_as_float(g.x << 16),
+                              v.y * inv * __uint_as_float(g.x & 0xffff0000u));
+            p.y = pack_bf16x2(v.z * inv * __uint_as_float(g.y << 16),
+                              v.w * inv * __uint_as_float(g.y & 0xffff0000u));
+            *reinterpret_cast<uint2*>(a + t * d + c * 4) = p;
+        }
+        __syncthreads();
+    }
+}
+
+unsigned grid_for(int64_t work, int threads)
+{
+    int64_t b = (work + threads - 1) / threads;
+    if (b > 65536) b = 65536;
+    return static_cast<unsigned>(b < 1 ? 1 : b);
+}
+
+}  // namespace
+
+hipError_t launch_permute(const bf16_t* x, const int32_t* perm, int64_t A, int d, int k,
+                          bf16_t* x_perm, hipStream_t stream)
+{
+    if (A == 0) return hipSuccess;
+    permute_kernel<<<grid_for(A * (d / 8), 256), 256, 0, stream>>>(x, perm, A, d, k, x_perm);
+    return hipGetLastError();
+}
+
+hipError_t launch_combine(const float* y, const float* residual, int64_t T, int d, int k,
+                          bf16_t* out, float* out_f32, hipStream_t stream)
+{
+    if (T == 0) return hipSuccess;
+    combine_kernel<<<grid_for(T * (d / 4), 256), 256, 0, stream>>>(y, residual, T, d, k, out,
+                                                                   out_f32);
+    return hipGetLastError();
+}
+
+hipError_t launch_rmsnorm(const float* h, const bf16_t* gamma, int64_t T, int d, float eps,
+                          bf16_t* a, hipStream_t stream)
+{
+    if (T == 0) return hipSuccess;
+    const unsigned grid = static_cast<unsigned>(T < 65536 ? T : 65536);
+    rmsnorm_kernel<<<grid, 256, 0, stream>>>(h, gamma, T, d, eps, a);
+    return hipGetLastError();
+}
+
+}  // namespace moe

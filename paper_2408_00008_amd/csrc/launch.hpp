@@ -1,0 +1,66 @@
+// Host-side launchers of the gfx950 kernels.  Arguments are validated by the
+// C ABI layer (api.cpp) before any of these is called; each launcher only
+// enqueues work on `stream` and returns the launch status.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace moe {
+
+typedef uint16_t bf16_t;
+
+// Router GEMM (f32) + top-k + softmax over the selected logits, one token per
+// workgroup slot.  logits may be null.
+hipError_t launch_router_topk(const bf16_t* x, const bf16_t* router_w, const float* bias,
+                              int64_t T, int d, int E, int k, int32_t* topk_ids, float* topk_w,
+                              float* logits, hipStream_t stream);
+
+// Expert histogram, exclusive scan and the stable expert-major permutation.
+hipError_t launch_dispatch(const int32_t* topk_ids, int64_t A, int E, int32_t* offsets,
+                           int32_t* perm, hipStream_t stream);
+
+hipError_t launch_permute(const bf16_t* x, const int32_t* perm, int64_t A, int d, int k,
+                          bf16_t* x_perm, hipStream_t stream);
+
+hipError_t launch_combine(const float* y, const float* residual, int64_t T, int d, int k,
+                          bf16_t* out, float* out_f32, hipStream_t stream);
+
+hipError_t launch_rmsnorm(const float* h, const bf16_t* gamma, int64_t T, int d, float eps,
+                          bf16_t* a, hipStream_t stream);
+
+// Expert GEMMs.  `rows_hint` = T*k (an upper bound of any expert's rows) picks
+// the tile shape; the real per-expert row counts are read on the device.
+struct UpArgs {
+    const bf16_t* x;         // token rows: x[gather ? gather[r]/kslots : r]
+    const int32_t* gather;   // null = identity
+    int kslots;
+    const int32_t* offsets;  // [E+1]
+    const bf16_t* w1;        // [E,ffn,d]
+    const bf16_t* w3;        // [E,ffn,d]
+    bf16_t* h;               // [A,ffn]
+    int64_t A;
+    int d, ffn, E;
+};
+
+struct DownArgs {
+    const bf16_t* h;         // [A,ffn]
+    const int32_t* offsets;  // [E+1]
+    const bf16_t* w2;        // [E,d,ffn]
+    const float* topk_w;     // [A] or null
+    const int32_t* perm;     // [A] or null
+    float* y;                // [A,d]
+    int64_t A;
+    int d, ffn, E;
+};
+
+enum GemmVariant { VARIANT_AUTO = 0, VARIANT_STREAM = 1, VARIANT_TILED = 2 };
+
+// Chooses the kernel family for these sizes (resolves VARIANT_AUTO).
+int resolve_variant(int requested, int64_t A, int E);
+
+hipError_t launch_up(const UpArgs& a, int variant, hipStream_t stream);
+hipError_t launch_down(const DownArgs& a, int variant, hipStream_t stream);
+
+}  // namespace moe

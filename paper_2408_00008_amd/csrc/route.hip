@@ -1,0 +1,238 @@
+// Router GEMM, top-k gating and token-to-expert dispatch for gfx950.
+//
+// The router of a Mixtral MoE layer (the model of the paper's engine, Sec. 4.1)
+// scores every token against every expert, keeps the k best experts and
+// weights them with a softmax over the kept scores.  Here:
+//   * one workgroup (4 wave64) per token: each lane multiplies 16-byte chunks
+//     of x against the same chunk of every expert's router row, accumulating
+//     in f32; partial sums are combined with a fixed butterfly + LDS order, so
+//     results are bitwise reproducible;
+//   * wave 0 then selects the top k with a wave-wide arg-max butterfly on the
+//     key (logit, -expert) -- equal logits pick the lower expert -- and forms
+//     the softmax over the selected logits in f32;
+//   * a single-workgroup dispatch kernel builds the expert histogram (LDS
+//     atomics), its exclusive scan, and the stable expert-major permutation
+//     with wave ballots (rank among equal experts = popcount of lower lanes).
+#include "common.hpp"
+#include "launch.hpp"
+
+#include <math.h>
+
+namespace moe {
+
+namespace {
+
+constexpr int ROUTE_THREADS = 256;
+
+struct Cand {
+    float v;
+    int i;
+};
+
+__device__ __forceinline__ bool ahead(const Cand& a, const Cand& b)
+{
+    return a.v > b.v || (a.v == b.v && a.i < b.i);
+}
+
+template <int EMAX>
+__global__ __launch_bounds__(ROUTE_THREADS) void router_topk_kernel(
+    const bf16_t* __restrict__ x, const bf16_t* __restrict__ wr, const float* __restrict__ bias,
+    int64_t T, int d, int E, int k, int32_t* __restrict__ topk_ids, float* __restrict__ topk_w,
+    float* __restrict__ logits_out)
+{
+    __shared__ float red[ROUTE_THREADS / 64][EMAX];
+    __shared__ float lg[EMAX];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int nchunk = d >> 3;  // 16-byte chunks per row
+
+    for (int64_t t = blockIdx.x; t < T; t += gridDim.x) {
+        float acc[EMAX];
+#pragma unroll
+        for (int e = 0; e < EMAX; ++e) acc[e] = 0.0f;
+        const bf16_t* xr = x + t * (int64_t)d;
+        for (int c = tid; c < nchunk; c += ROUTE_THREADS) {
+            uint4 xv = ldg16(xr + c * 8);
+            float xf[8];
+            const uint32_t xw[4] = {xv.x, xv.y, xv.z, xv.w};
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                xf[2 * q] = __uint_as_float(xw[q] << 16);
+                xf[2 * q + 1] = __uint_as_float(xw[q] & 0xffff0000u);
+            }
+#pragma unroll
+            for (int e = 0; e < EMAX; ++e) {
+                if (e < E) {
+                    uint4 wv = ldg16(wr + (int64_t)e * d + c * 8);
+                    const uint32_t ww[4] = {wv.x, wv.y, wv.z, wv.w};
+                    float s = acc[e];
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        s = fmaf(xf[2 * q], __uint_as_float(ww[q] << 16), s);
+                        s = fmaf(xf[2 * q + 1], __uint_as_float(ww[q] & 0xffff0000u), s);
+                    }
+                    acc[e] = s;
+                }
+            }
+        }
+        // wave butterfly, then a fixed-order sum over the 4 waves
+#pragma unroll
+        for (int e = 0; e < EMAX; ++e) {
+            if (e < E) {
+                float v = acc[e];
+#pragma unroll
+                for (int m = 32; m >= 1; m >>= 1) v += wave_shfl_xor(v, m);
+                if (lane == 0) red[wave][e] = v;
+            }
+        }
+        __syncthreads();
+        if (tid < E) {
+            float s = red[0][tid];
+#pragma unroll
+            for (int w = 1; w < ROUTE_THREADS / 64; ++w) s += red[w][tid];
+            if (bias) s += bias[tid];
+            lg[tid] = s;
+            if (logits_out) logits_out[t * E + tid] = s;
+        }
+        __syncthreads();
+        if (wave == 0) {
+            Cand me;
+            me.v = lane < E ? lg[lane] : -INFINITY;
+            me.i = lane < E ? lane : 0x7fffffff;
+            float selv[8];
+            int seli[8];
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                if (j < k) {
+                    Cand b = me;
+#pragma unroll
+                    for (int m = 32; m >= 1; m >>= 1) {
+                        Cand o;
+                        o.v = wave_shfl_xor(b.v, m);
+                        o.i = wave_shfl_xor(b.i, m);
+                        if (ahead(o, b)) b = o;
+                    }
+                    selv[j] = b.v;
+                    seli[j] = b.i;
+                    if (lane == b.i) {
+                        me.v = -INFINITY;
+                        me.i = 0x7fffffff;
+                    }
+                }
+            }
+            if (lane == 0) {
+                float den = 0.0f;
+                float ex[8];
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    if (j < k) {
+                        ex[j] = expf(selv[j] - selv[0]);
+                        den += ex[j];
+                    }
+                }
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    if (j < k) {
+                        topk_ids[t * k + j] = seli[j];
+                        topk_w[t * k + j] = ex[j] / den;
+                    }
+                }
+            }
+        }
+        __syncthreads();
+    }
+}
+
+constexpr int DISPATCH_THREADS = 1024;
+constexpr int DISPATCH_WAVES = DISPATCH_THREADS / 64;
+
+// One workgroup.  offsets[0..E], perm[0..A-1].
+__global__ __launch_bounds__(DISPATCH_THREADS) void dispatch_kernel(
+    const int32_t* __restrict__ ids, int64_t A, int E, int32_t* __restrict__ offsets,
+    int32_t* __restrict__ perm)
+{
+    __shared__ int cnt[64];
+    __shared__ int base[64];    // running start of each expert's next rows
+    __shared__ int wcnt[DISPATCH_WAVES][64];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    if (tid < 64) cnt[tid] = 0;
+    __syncthreads();
+    for (int64_t a = tid; a < A; a += DISPATCH_THREADS) atomicAdd(&cnt[ids[a]], 1);
+    __syncthreads();
+    if (wave == 0) {
+        int c = lane < E ? cnt[lane] : 0;
+        int incl = c;
+#pragma unroll
+        for (int m = 1; m < 64; m <<= 1) {
+            int o = __shfl_up(incl, m, 64);
+            if (lane >= m) incl += o;
+        }
+        if (lane < E) {
+            base[lane] = incl - c;
+            offsets[lane] = incl - c;
+        }
+        if (lane == E - 1) offsets[E] = incl;
+    }
+    __syncthreads();
+    const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+    for (int64_t b0 = 0; b0 < A; b0 += DISPATCH_THREADS) {
+        const int64_t a = b0 + tid;
+        const int e = a < A ? ids[a] : -1;
+        if (lane < 64) wcnt[wave][lane] = 0;
+        // rank among lanes of this wave with the same expert
+        int rank = 0;
+        uint64_t todo = __ballot(e >= 0);
+        while (todo) {
+            const int leader = __ffsll(static_cast<unsigned long long>(todo)) - 1;
+            const int le = __shfl(e, leader, 64);
+            const uint64_t same = __ballot(e == le);
+            if (e == le) rank = __popcll(same & lt_mask);
+            if (lane == 0) wcnt[wave][le] = __popcll(same);
+            todo &= ~same;
+        }
+        __syncthreads();
+        if (e >= 0) {
+            int before = 0;
+            for (int w = 0; w < wave; ++w) before += wcnt[w][e];
+            perm[base[e] + before + rank] = static_cast<int32_t>(a);
+        }
+        __syncthreads();
+        if (tid < E) {
+            int tot = 0;
+            for (int w = 0; w < DISPATCH_WAVES; ++w) tot += wcnt[w][tid];
+            base[tid] += tot;
+        }
+        __syncthreads();
+    }
+}
+
+}  // namespace
+
+hipError_t launch_router_topk(const bf16_t* x, const bf16_t* router_w, const float* bias,
+                              int64_t T, int d, int E, int k, int32_t* topk_ids, float* topk_w,
+                              float* logits, hipStream_t stream)
+{
+    if (T == 0) return hipSuccess;
+    const unsigned grid = static_cast<unsigned>(T < 16384 ? T : 16384);
+    if (E <= 8)
+        router_topk_kernel<8><<<grid, ROUTE_THREADS, 0, stream>>>(x, router_w, bias, T, d, E, k,
+                                                                  topk_ids, topk_w, logits);
+    else if (E <= 16)
+        router_topk_kernel<16><<<grid, ROUTE_THREADS, 0, stream>>>(x, router_w, bias, T, d, E, k,
+                                                                   topk_ids, topk_w, logits);
+    else if (E <= 32)
+        router_topk_kernel<32><<<grid, ROUTE_THREADS, 0, stream>>>(x, router_w, bias, T, d, E, k,
+                                                                   topk_ids, topk_w, logits);
+    else
+        router_topk_kernel<64><<<grid, ROUTE_THREADS, 0, stream>>>(x, router_w, bias, T, d, E, k,
+                                                                   topk_ids, topk_w, logits);
+    return hipGetLastError();
+}
+
+hipError_t launch_dispatch(const int32_t* topk_ids, int64_t A, int E, int32_t* offsets,
+                           int32_t* perm, hipStream_t stream)
+{
+    dispatch_kernel<<<1, DISPATCH_THREADS, 0, stream>>>(topk_ids, A, E, offsets, perm);
+    return hipGetLastError();
+}
+
+}  // namespace moe

@@ -1,0 +1,133 @@
+"""Shared pieces of the GPU parity tests: device copies of seeded workloads,
+calls through the C ABI binding, and the oracle reference of the same bits."""
+
+from __future__ import annotations
+
+import functools
+import sys
+
+import numpy as np
+import torch
+
+from oracle import oracle as oracle_mod
+from paper_2408_00008_amd import binding as B
+from paper_2408_00008_amd import inputs
+
+DEV = "cuda:0"
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+@functools.lru_cache(maxsize=1)
+def orc():
+    return oracle_mod.get()
+
+
+class Case:
+    """One MoE layer's inputs on the GPU plus their host bit patterns."""
+
+    def __init__(self, T, d, ffn, E, k, x, router_w, w1, w3, w2, router_bias=None, name="case"):
+        self.T, self.d, self.ffn, self.E, self.k = T, d, ffn, E, k
+        self.name = name
+        self.x, self.router_w, self.w1, self.w3, self.w2 = x, router_w, w1, w3, w2
+        self.router_bias = router_bias
+        self._bits = {}
+
+    def bits(self, name):
+        if name not in self._bits:
+            self._bits[name] = inputs.bf16_bits(getattr(self, name))
+        return self._bits[name]
+
+    @property
+    def bias_np(self):
+        return None if self.router_bias is None else self.router_bias.cpu().numpy()
+
+    def with_x(self, x):
+        c = Case(x.shape[0], self.d, self.ffn, self.E, self.k, x, self.router_w, self.w1, self.w3,
+                 self.w2, self.router_bias, self.name)
+        for n in ("router_w", "w1", "w3", "w2"):
+            if n in self._bits:
+                c._bits[n] = self._bits[n]
+        return c
+
+
+def workload_case(name, T=None, seed=0) -> Case:
+    w = inputs.WORKLOADS[name].replace(seed=seed)
+    if T is not None:
+        w = w.replace(T=T)
+    lay = inputs.make_layer(w, 0, DEV)
+    x = inputs.make_x(w, DEV)
+    return Case(w.T, w.d, w.ffn, w.E, w.k, x, lay["router_w"], lay["w1"], lay["w3"], lay["w2"],
+                lay["router_bias"], name)
+
+
+def small_case(T, d, ffn, E, k, seed=0, std=None, bias=None) -> Case:
+    std_w = (1.0 / np.sqrt(d)) if std is None else std
+    w = inputs.Workload("small", T, d, ffn, E, k, 1.0, std_w, std_w, std_w,
+                        1.0 / np.sqrt(ffn) if std is None else std, seed=seed)
+    lay = inputs.make_layer(w, 0, DEV)
+    x = inputs.make_x(w, DEV)
+    b = None if bias is None else torch.tensor(bias, dtype=torch.float32, device=DEV)
+    return Case(T, d, ffn, E, k, x, lay["router_w"], lay["w1"], lay["w3"], lay["w2"], b,
+                f"small{T}x{d}x{ffn}x{E}k{k}")
+
+
+# ---- GPU side (through the C ABI) -------------------------------------------
+
+def gpu_route(c: Case):
+    T, E, k = c.T, c.E, c.k
+    ids = torch.empty(T, k, dtype=torch.int32, device=DEV)
+    gw = torch.empty(T, k, dtype=torch.float32, device=DEV)
+    offs = torch.empty(E + 1, dtype=torch.int32, device=DEV)
+    perm = torch.empty(max(T * k, 1), dtype=torch.int32, device=DEV)[:T * k]
+    logits = torch.empty(T, E, dtype=torch.float32, device=DEV)
+    B.moe_route(c.x, c.router_w, k, ids, gw, offs, perm, router_bias=c.router_bias,
+                logits=logits)
+    torch.cuda.synchronize()
+    return ids, gw, offs, perm, logits
+
+
+def gpu_forward(c: Case, variant=None, out_f32=False):
+    prev = B.moe_set_gemm_variant(variant) if variant is not None else None
+    try:
+        out = torch.empty(c.T, c.d, dtype=torch.bfloat16, device=DEV)
+        if c.router_bias is None and not out_f32:
+            B.moe_forward(c.x, c.router_w, c.w1, c.w3, c.w2, c.k, out)
+            torch.cuda.synchronize()
+            return out
+        of = torch.empty(c.T, c.d, dtype=torch.float32, device=DEV) if out_f32 else None
+        B.moe_forward_ex(c.x, c.router_w, c.w1, c.w3, c.w2, c.k, out=out, out_f32=of,
+                         router_bias=c.router_bias)
+        torch.cuda.synchronize()
+        return (out, of) if out_f32 else out
+    finally:
+        if prev is not None:
+            B.moe_set_gemm_variant(prev)
+
+
+def bf16_to_f64(t: torch.Tensor) -> np.ndarray:
+    return t.float().cpu().numpy().astype(np.float64)
+
+
+# ---- oracle side ----------------------------------------------------------------
+
+def oracle_logits(c: Case, rows=None):
+    x = c.bits("x") if rows is None else c.bits("x")[rows]
+    return orc().router_logits(x, c.bits("router_w"), c.bias_np)
+
+
+def oracle_out(c: Case, rows, gpu_ids_rows=None):
+    """Oracle output of tokens `rows`; routing from the oracle, except that
+    tokens flagged ambiguous use the GPU's ids (gates from oracle logits)."""
+    o = orc()
+    x = c.bits("x")[rows]
+    logits = o.router_logits(x, c.bits("router_w"), c.bias_np)
+    ids, gates = o.topk_gate(logits, c.k)
+    if gpu_ids_rows is not None:
+        ids = np.ascontiguousarray(gpu_ids_rows, dtype=np.int32)
+        gates = o.gates_for_ids(logits, ids)
+    out = o.moe_apply(x, c.bits("w1"), c.bits("w3"), c.bits("w2"), ids, gates)
+    return out, logits, ids, gates

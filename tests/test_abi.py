@@ -1,0 +1,144 @@
+"""The C ABI library loads, exports every declared symbol, and rejects bad
+arguments before touching the GPU (CPU only: every call here fails validation
+or has T = 0, so no HIP call is made)."""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2408_00008_amd import binding as B
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "moe.h")
+
+
+def declared():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(moe_[a-z0-9_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(B.LIB_PATH):
+        from paper_2408_00008_amd import build
+        build.build()
+    return B.lib()
+
+
+def test_exports_every_declared_symbol(L):
+    names = declared()
+    assert len(names) >= 14
+    for n in names:
+        assert hasattr(L, n), f"{n} declared in moe.h but not exported"
+    assert set(names) == set(B.EXPORTS)
+
+
+def test_status_strings(L):
+    assert L.moe_status_string(0) == b"MOE_OK"
+    assert L.moe_status_string(1) == b"MOE_ERR_INVALID_ARG"
+    assert L.moe_status_string(2) == b"MOE_ERR_UNSUPPORTED"
+    assert L.moe_status_string(3) == b"MOE_ERR_NO_MEMORY"
+    assert L.moe_status_string(4) == b"MOE_ERR_HIP"
+    assert L.moe_status_string(99) == b"MOE_ERR_UNKNOWN"
+    assert L.moe_version() >= 100
+
+
+# fake device addresses: never dereferenced because every call below is
+# rejected by validation (or is empty)
+X, RW, W1, W3, W2, OUT = (0x10000 * (i + 1) for i in range(6))
+BIG = 1 << 40  # far apart so no two fake ranges overlap
+
+
+def fwd(L, x=X, rw=RW, w1=W1 * BIG // 0x10000, w3=W3 * BIG // 0x10000, w2=W2 * BIG // 0x10000,
+        T=4, d=128, ffn=256, E=8, k=2, out=OUT * BIG // 0x10000):
+    return L.moe_forward(x, rw, w1, w3, w2, T, d, ffn, E, k, out, None)
+
+
+@pytest.mark.parametrize("kw,status,msg", [
+    (dict(E=65), B.MOE_ERR_UNSUPPORTED, "E=65"),
+    (dict(E=0), B.MOE_ERR_INVALID_ARG, "E=0"),
+    (dict(k=0), B.MOE_ERR_INVALID_ARG, "k=0"),
+    (dict(k=9, E=16), B.MOE_ERR_UNSUPPORTED, "k=9"),
+    (dict(k=3, E=2), B.MOE_ERR_INVALID_ARG, "exceeds E"),
+    (dict(d=100), B.MOE_ERR_UNSUPPORTED, "multiple of 64"),
+    (dict(ffn=96), B.MOE_ERR_UNSUPPORTED, "multiple of 64"),
+    (dict(d=0), B.MOE_ERR_INVALID_ARG, "d=0"),
+    (dict(d=65536 + 64), B.MOE_ERR_UNSUPPORTED, "exceeds"),
+    (dict(T=-1), B.MOE_ERR_INVALID_ARG, "T=-1"),
+    (dict(T=1 << 30, k=2), B.MOE_ERR_UNSUPPORTED, "2^31"),
+    (dict(x=0), B.MOE_ERR_INVALID_ARG, "x is NULL"),
+    (dict(x=X + 2), B.MOE_ERR_INVALID_ARG, "aligned"),
+    (dict(out=0), B.MOE_ERR_INVALID_ARG, "out is NULL"),
+    (dict(out=X), B.MOE_ERR_INVALID_ARG, "overlaps x"),
+])
+def test_forward_rejects(L, kw, status, msg):
+    st = fwd(L, **kw)
+    assert st == status, (st, L.moe_last_error())
+    assert msg in L.moe_last_error().decode()
+
+
+def test_forward_empty_is_ok(L):
+    assert fwd(L, T=0) == B.MOE_OK
+    assert L.moe_last_error() == b""
+
+
+def test_route_and_stage_rejects(L):
+    p = ctypes.c_void_p
+    # k > E
+    st = L.moe_route(X, RW, None, 4, 128, 2, 3, 0x100000, 0x200000, 0x300000, 0x400000, None, None)
+    assert st == B.MOE_ERR_INVALID_ARG
+    # overlapping outputs
+    st = L.moe_route(X, RW, None, 4, 128, 8, 2, 0x100000, 0x100000, 0x300000, 0x400000, None, None)
+    assert st == B.MOE_ERR_INVALID_ARG and b"overlaps" in L.moe_last_error()
+    # misaligned bias
+    st = L.moe_route(X, RW, 0x500004, 4, 128, 8, 2, 0x100000, 0x200000, 0x300000, 0x400000,
+                     None, None)
+    assert st == B.MOE_ERR_INVALID_ARG and b"router_bias" in L.moe_last_error()
+    assert L.moe_route(X, RW, None, 0, 128, 8, 2, 0x100000, 0x200000, 0x300000, 0x400000,
+                       None, None) == B.MOE_OK
+    # combine needs an output
+    assert L.moe_combine(X, None, 4, 128, 2, None, None, None) == B.MOE_ERR_INVALID_ARG
+    # rmsnorm eps
+    assert L.moe_rmsnorm(X, RW, 4, 128, ctypes.c_float(-1.0), OUT, None) == B.MOE_ERR_INVALID_ARG
+    # swiglu: h overlapping a weight
+    w = 1 << 36
+    st = L.moe_swiglu_up(X, None, 0x700000, w, 2 * w, 4, 128, 256, 8, 2, w + 64, None)
+    assert st == B.MOE_ERR_INVALID_ARG and b"overlaps w1" in L.moe_last_error()
+    # permute into its own input
+    assert L.moe_permute(X, 0x700000, 4, 128, 2, X, None) == B.MOE_ERR_INVALID_ARG
+    del p
+
+
+def test_forward_ex_workspace_checks(L):
+    big = 1 << 40
+    args = [X, RW, None, big, 2 * big, 3 * big, 4, 128, 256, 8, 2, None, 4 * big, None]
+    need = L.moe_workspace_size(4, 128, 256, 8, 2)
+    assert need > 0
+    st = L.moe_forward_ex(*args, 5 * big + 16, need, None)
+    assert st == B.MOE_ERR_INVALID_ARG and b"256-byte" in L.moe_last_error()
+    st = L.moe_forward_ex(*args, 5 * big, need - 1, None)
+    assert st == B.MOE_ERR_NO_MEMORY
+    st = L.moe_forward_ex(X, RW, None, big, 2 * big, 3 * big, 4, 128, 256, 8, 2, None, None,
+                          None, None, 0, None)
+    assert st == B.MOE_ERR_INVALID_ARG and b"both NULL" in L.moe_last_error()
+
+
+def test_workspace_size(L):
+    assert L.moe_workspace_size(0, 128, 256, 8, 2) > 0  # offsets still have E+1 entries
+    assert L.moe_workspace_size(4, 128, 256, 8, 9) == 0
+    T, d, f, E, k = 64, 4096, 14336, 8, 2
+    ws = L.moe_workspace_size(T, d, f, E, k)
+    A = T * k
+    assert ws >= A * f * 2 + A * d * 4 + 3 * A * 4
+
+
+def test_variant_switch(L):
+    assert L.moe_gemm_variant_for(64, 4096, 14336, 8, 2) == 1
+    assert L.moe_gemm_variant_for(64, 4096, 14336, 8, 9) == 0
+    prev = L.moe_set_gemm_variant(1)
+    assert L.moe_set_gemm_variant(2) == 1
+    assert L.moe_set_gemm_variant(7) == -1
+    assert L.moe_set_gemm_variant(prev) == 2

@@ -1,0 +1,231 @@
+"""GPU path (through the C ABI) against the fp64 oracle on the same bits."""
+
+import numpy as np
+import pytest
+import torch
+
+from gpu_common import (DEV, bf16_to_f64, gpu_forward, gpu_route, oracle_logits, oracle_out, orc,
+                        say, small_case, workload_case)
+from parity import OUT_TOL, check_routing, rowwise_rel
+from paper_2408_00008_amd import binding as B
+from paper_2408_00008_amd import inputs
+
+pytestmark = pytest.mark.gpu
+
+_cases = {}
+
+
+def wl(name):
+    if name not in _cases:
+        say(f"[gen] {name}")
+        _cases[name] = workload_case(name)
+    return _cases[name]
+
+
+def _route_checks(c, sample=None):
+    ids, gw, offs, perm, logits = gpu_route(c)
+    rows = np.arange(c.T) if sample is None else sample
+    ref_logits = oracle_logits(c, rows)
+    g_ids = ids.cpu().numpy()
+    amb = check_routing(g_ids[rows], ref_logits, c.k)
+    # f32 logits against f64: relative to the row's logit scale
+    gl = logits.cpu().numpy().astype(np.float64)[rows]
+    scale = np.abs(ref_logits).max(axis=1, keepdims=True) + 1e-30
+    assert np.max(np.abs(gl - ref_logits) / scale) < 1e-5
+    # gates: softmax of the GPU's logits over the GPU's ids, in f32
+    ref_g = orc().gates_for_ids(ref_logits, g_ids[rows])
+    assert np.max(np.abs(gw.cpu().numpy()[rows] - ref_g)) < 2e-5
+    assert np.all(np.abs(gw.cpu().numpy().sum(1) - 1.0) < 4e-7)
+    # dispatch: exact integers, recomputed by the oracle from the GPU's ids
+    _, r_off, r_perm = orc().dispatch(g_ids, c.E)
+    assert np.array_equal(offs.cpu().numpy(), r_off)
+    assert np.array_equal(perm.cpu().numpy(), r_perm)
+    return amb, g_ids
+
+
+@pytest.mark.parametrize("name", ["tiny_t16", "decode_t64", "decode_t256_skew", "prefill_t4096"])
+def test_route(name):
+    say(f"[route] {name}")
+    c = wl(name)
+    amb, _ = _route_checks(c)
+    say(f"  ambiguous tokens: {int(amb.sum())} of {c.T}")
+    assert amb.sum() <= max(2, c.T // 500)
+
+
+@pytest.mark.parametrize("shape", [(1, 64, 64, 1, 1), (37, 192, 320, 8, 2), (5, 128, 128, 4, 4),
+                                   (300, 64, 128, 64, 8), (129, 256, 64, 3, 2)])
+def test_route_shapes(shape):
+    say(f"[route] shape {shape}")
+    c = small_case(*shape, seed=5)
+    _route_checks(c)
+
+
+def test_route_ties_lower_index():
+    """Experts with identical router rows tie exactly: the lower index wins."""
+    say("[route] ties")
+    c = small_case(64, 128, 128, 8, 2, seed=9)
+    rw = c.router_w.clone()
+    rw[5] = rw[1]
+    rw[7] = rw[0]
+    c.router_w = rw
+    c._bits.pop("router_w", None)
+    ids, _, _, _, logits = gpu_route(c)
+    ids = ids.cpu().numpy()
+    ref_ids, _ = orc().topk_gate(oracle_logits(c), 2)
+    for t in range(c.T):
+        row = ids[t].tolist()
+        for lo, hi in ((1, 5), (0, 7)):
+            if hi in row:
+                assert lo in row and row.index(lo) < row.index(hi)
+    check_routing(ids, oracle_logits(c), 2)
+    del ref_ids
+
+
+def test_permute_bitwise():
+    say("[permute]")
+    c = small_case(37, 192, 64, 8, 2, seed=3)
+    ids, gw, offs, perm, _ = gpu_route(c)
+    xp = torch.empty(c.T * c.k, c.d, dtype=torch.bfloat16, device=DEV)
+    B.moe_permute(c.x, perm, c.k, xp)
+    torch.cuda.synchronize()
+    ref = c.bits("x")[perm.cpu().numpy() // c.k]
+    assert np.array_equal(inputs.bf16_bits(xp), ref)
+
+
+@pytest.mark.parametrize("name", ["tiny_t16", "decode_t64"])
+@pytest.mark.parametrize("variant", [1, 2])
+def test_stages_teacher_forced(name, variant):
+    """up/down/combine fed the oracle's routing, compared stage by stage."""
+    say(f"[stages] {name} variant {variant}")
+    c = wl(name)
+    o = orc()
+    x = c.bits("x")
+    logits = o.router_logits(x, c.bits("router_w"), c.bias_np)
+    ids, gates = o.topk_gate(logits, c.k)
+    _, offs, perm = o.dispatch(ids, c.E)
+    out_ref, h_ref, y_ref = o.moe_apply(x, c.bits("w1"), c.bits("w3"), c.bits("w2"), ids, gates,
+                                        want_slots=True)
+    A = c.T * c.k
+    d_offs = torch.from_numpy(offs).to(DEV)
+    d_perm = torch.from_numpy(perm).to(DEV)
+    d_gw = torch.from_numpy(gates.astype(np.float32).reshape(-1)).to(DEV)
+    xp = torch.empty(A, c.d, dtype=torch.bfloat16, device=DEV)
+    B.moe_permute(c.x, d_perm, c.k, xp)
+    h = torch.empty(A, c.ffn, dtype=torch.bfloat16, device=DEV)
+    y = torch.empty(A, c.d, dtype=torch.float32, device=DEV)
+    prev = B.moe_set_gemm_variant(variant)
+    try:
+        B.moe_swiglu_up(xp, d_offs, c.w1, c.w3, c.T, c.k, h)
+        B.moe_swiglu_down(h, d_offs, c.w2, c.T, c.k, y, topk_w=d_gw, perm=d_perm)
+        y_plain = torch.empty_like(y)
+        B.moe_swiglu_down(h, d_offs, c.w2, c.T, c.k, y_plain)
+    finally:
+        B.moe_set_gemm_variant(prev)
+    out = torch.empty(c.T, c.d, dtype=torch.bfloat16, device=DEV)
+    B.moe_combine(y, c.T, c.d, c.k, out=out)
+    torch.cuda.synchronize()
+    # h rows are in permuted order r; the oracle's are in assignment order a = perm[r]
+    e_h = rowwise_rel(bf16_to_f64(h), h_ref[perm])
+    e_y = rowwise_rel(y.cpu().numpy(), y_ref * gates.reshape(-1, 1))
+    e_yp = rowwise_rel(y_plain.cpu().numpy(), y_ref[perm])
+    e_o = rowwise_rel(bf16_to_f64(out), out_ref)
+    say(f"  rowwise rel: h {e_h:.2e} y {e_y:.2e} y_plain {e_yp:.2e} out {e_o:.2e}")
+    assert e_h < OUT_TOL and e_y < OUT_TOL and e_yp < OUT_TOL and e_o < OUT_TOL
+
+
+def _forward_check(c, rows=None, variant=None):
+    out = gpu_forward(c, variant)
+    ids, *_ = gpu_route(c)
+    rows = np.arange(c.T) if rows is None else np.asarray(rows)
+    g_ids = ids.cpu().numpy()
+    ref_logits = oracle_logits(c, rows)
+    check_routing(g_ids[rows], ref_logits, c.k)
+    ref, *_ = oracle_out(c, rows, g_ids[rows])
+    err = rowwise_rel(bf16_to_f64(out)[rows], ref)
+    say(f"  {c.name} T={c.T} variant={variant}: rowwise rel {err:.3e} over {len(rows)} tokens")
+    assert err < OUT_TOL
+    return out
+
+
+@pytest.mark.parametrize("name", ["tiny_t16", "decode_t64"])
+def test_forward_full(name):
+    say(f"[forward] {name} (every token)")
+    _forward_check(wl(name))
+
+
+@pytest.mark.parametrize("name", ["decode_t256_skew", "prefill_t4096"])
+@pytest.mark.parametrize("variant", [0, 1])
+def test_forward_sampled(name, variant):
+    say(f"[forward] {name} variant {variant} (sampled tokens)")
+    c = wl(name)
+    rng = np.random.default_rng(11)
+    rows = np.sort(np.concatenate([[0, c.T - 1], rng.choice(c.T, 30, replace=False)]))
+    rows = np.unique(rows)
+    _forward_check(c, rows, variant)
+
+
+@pytest.mark.parametrize("shape", [
+    (1, 64, 64, 1, 1),        # single token, single expert
+    (37, 192, 320, 8, 2),     # ragged T, d/ffn not multiples of 128
+    (5, 128, 128, 4, 4),      # k = E: every expert on every token
+    (200, 64, 128, 16, 2),    # many experts, several tiles of rows
+    (300, 128, 192, 64, 8),   # E = 64, k = 8 limits
+    (513, 256, 512, 8, 2),    # rows per expert > 64
+])
+@pytest.mark.parametrize("variant", [1, 2])
+def test_forward_shapes(shape, variant):
+    say(f"[forward] shape {shape} variant {variant}")
+    _forward_check(small_case(*shape, seed=13), variant=variant)
+
+
+def test_forward_empty_experts():
+    """A bias that sends every token to experts 2 and 5 leaves the rest idle."""
+    say("[forward] empty experts")
+    bias = [0.0] * 8
+    bias[2], bias[5] = 50.0, 40.0
+    c = small_case(48, 128, 256, 8, 2, seed=17, bias=bias)
+    ids, _, offs, _, _ = gpu_route(c)
+    o = offs.cpu().numpy()
+    assert (np.diff(o) > 0).sum() == 2
+    _forward_check(c)
+
+
+def test_forward_t0():
+    c = small_case(3, 64, 64, 4, 2)
+    out = torch.zeros(0, 64, dtype=torch.bfloat16, device=DEV)
+    B.moe_forward(c.x[:0], c.router_w, c.w1, c.w3, c.w2, 2, out)
+    torch.cuda.synchronize()
+
+
+def test_rmsnorm_within_one_ulp():
+    say("[rmsnorm]")
+    from parity import bf16_ulp_diff, round_bf16_bits
+    T, d = 64, 4096
+    g = torch.Generator(device=DEV).manual_seed(5)
+    h = torch.randn(T, d, device=DEV, generator=g) * 3
+    w = inputs.Workload("g", T, d, 64, 1, 1, 1, 1, 1, 1, 1)
+    gamma = inputs.make_gamma(w, 0, DEV, random=True)
+    a = torch.empty(T, d, dtype=torch.bfloat16, device=DEV)
+    B.moe_rmsnorm(h, gamma, 1e-5, a)
+    torch.cuda.synchronize()
+    ref = orc().rmsnorm(h.cpu().numpy(), inputs.bf16_bits(gamma), 1e-5)
+    ulps = bf16_ulp_diff(inputs.bf16_bits(a), round_bf16_bits(ref))
+    assert ulps.max() <= 1
+
+
+def test_combine_residual_inplace():
+    say("[combine]")
+    T, d, k = 33, 192, 3
+    g = torch.Generator(device=DEV).manual_seed(8)
+    y = torch.randn(T * k, d, device=DEV, generator=g)
+    res = torch.randn(T, d, device=DEV, generator=g)
+    res0 = res.clone()
+    out = torch.empty(T, d, dtype=torch.bfloat16, device=DEV)
+    B.moe_combine(y, T, d, k, out=out, out_f32=res, residual=res)
+    torch.cuda.synchronize()
+    yy = y.cpu().numpy().reshape(T, k, d)
+    ref = res0.cpu().numpy().copy()
+    for j in range(k):  # same f32 order: residual, then slots ascending
+        ref = (ref + yy[:, j]).astype(np.float32)
+    assert np.array_equal(res.cpu().numpy(), ref)
+    assert np.array_equal(out.float().cpu().numpy(), torch.from_numpy(ref).bfloat16().float().numpy())
