@@ -357,7 +357,8 @@ moe_status_t moe_combine(const float* y, const float* residual, int64_t T, int32
     TRY(maybe(residual, "residual"));
     TRY(maybe(out, "out"));
     TRY(maybe(out_f32, "out_f32"));
-    if (!out && !out_f32) return fail(MOE_ERR_INVALID_ARG, "out and out_f32 are both NULL");
+    if (!out && !out_f32 && T > 0)
+        return fail(MOE_ERR_INVALID_ARG, "out and out_f32 are both NULL");
     const size_t A = static_cast<size_t>(T) * k;
     const size_t td = static_cast<size_t>(T) * d;
     TRY(no_overlap("out", {out, td * 2}, {{"y", {y, A * d * 4}}, {"residual", {residual, td * 4}},
@@ -399,7 +400,8 @@ moe_status_t moe_forward_ex(const moe_bf16_t* x, const moe_bf16_t* router_w,
     TRY(maybe(residual, "residual"));
     TRY(maybe(out, "out"));
     TRY(maybe(out_f32, "out_f32"));
-    if (!out && !out_f32) return fail(MOE_ERR_INVALID_ARG, "out and out_f32 are both NULL");
+    if (!out && !out_f32 && T > 0)
+        return fail(MOE_ERR_INVALID_ARG, "out and out_f32 are both NULL");
     if (workspace && (reinterpret_cast<uintptr_t>(workspace) & 255u))
         return fail(MOE_ERR_INVALID_ARG, "workspace is not 256-byte aligned");
     const size_t td = static_cast<size_t>(T) * d;

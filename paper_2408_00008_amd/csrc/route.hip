@@ -3,13 +3,15 @@
 // The router of a Mixtral MoE layer (the model of the paper's engine, Sec. 4.1)
 // scores every token against every expert, keeps the k best experts and
 // weights them with a softmax over the kept scores.  Here:
-//   * one workgroup (4 wave64) per token: each lane multiplies 16-byte chunks
+//   * one workgroup (8 wave64) per token: each lane multiplies 16-byte chunks
 //     of x against the same chunk of every expert's router row, accumulating
-//     in f32; partial sums are combined with a fixed butterfly + LDS order, so
-//     results are bitwise reproducible;
-//   * wave 0 then selects the top k with a wave-wide arg-max butterfly on the
-//     key (logit, -expert) -- equal logits pick the lower expert -- and forms
-//     the softmax over the selected logits in f32;
+//     in f32; the per-expert partial sums are combined by a transposed wave
+//     butterfly and a fixed-order sum over the waves, so results are bitwise
+//     reproducible;
+//   * the top k are then ranked on the key (logit, -expert) -- equal logits
+//     pick the lower expert -- by one lane for up to 16 experts, or by a
+//     wave-wide arg-max butterfly for more, and the softmax over the selected
+//     logits is formed in f32;
 //   * a single-workgroup dispatch kernel builds the expert histogram (LDS
 //     atomics), its exclusive scan, and the stable expert-major permutation
 //     with wave ballots (rank among equal experts = popcount of lower lanes).
@@ -22,7 +24,7 @@ namespace moe {
 
 namespace {
 
-constexpr int ROUTE_THREADS = 256;
+constexpr int ROUTE_THREADS = 512;  // one 16-byte chunk per lane at d = 4096
 
 struct Cand {
     float v;
@@ -74,16 +76,30 @@ __global__ __launch_bounds__(ROUTE_THREADS) void router_topk_kernel(
                 }
             }
         }
-        // wave butterfly, then a fixed-order sum over the 4 waves
+        // Transposed butterfly: at each exchange a lane keeps half of its
+        // per-expert partial sums and ships the other half to its partner, so
+        // after log2(EMAX) exchanges lane l holds expert (l / (64/EMAX)) summed
+        // over 2^log2(EMAX) lanes; the remaining lane bits are then folded.
+        // EMAX-1 + log2(64/EMAX) shuffles instead of EMAX * 6.
+        float v[EMAX];
 #pragma unroll
-        for (int e = 0; e < EMAX; ++e) {
-            if (e < E) {
-                float v = acc[e];
+        for (int e = 0; e < EMAX; ++e) v[e] = acc[e];
 #pragma unroll
-                for (int m = 32; m >= 1; m >>= 1) v += wave_shfl_xor(v, m);
-                if (lane == 0) red[wave][e] = v;
+        for (int half = EMAX / 2, m = 32; half >= 1; half >>= 1, m >>= 1) {
+            const bool hi = (lane & m) != 0;
+#pragma unroll
+            for (int i = 0; i < half; ++i) {
+                const float send = hi ? v[i] : v[i + half];
+                const float keep = hi ? v[i + half] : v[i];
+                v[i] = keep + wave_shfl_xor(send, m);
             }
         }
+        constexpr int LANES_PER_E = 64 / EMAX;
+        float tot = v[0];
+#pragma unroll
+        for (int m = LANES_PER_E / 2; m >= 1; m >>= 1) tot += wave_shfl_xor(tot, m);
+        const int my_e = lane / LANES_PER_E;
+        if ((lane % LANES_PER_E) == 0 && my_e < E) red[wave][my_e] = tot;
         __syncthreads();
         if (tid < E) {
             float s = red[0][tid];
@@ -94,6 +110,52 @@ __global__ __launch_bounds__(ROUTE_THREADS) void router_topk_kernel(
             if (logits_out) logits_out[t * E + tid] = s;
         }
         __syncthreads();
+        if (EMAX <= 16) {
+            // few experts: one lane ranks them directly
+            if (tid == 0) {
+                int seli[8];
+                float selv[8];
+                uint32_t taken = 0;
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    if (j < k) {
+                        int best = -1;
+                        float bv = 0.0f;
+#pragma unroll
+                        for (int e = 0; e < EMAX; ++e) {
+                            if (e < E && !(taken & (1u << e))) {
+                                const float le = lg[e];
+                                // strict: an equal logit keeps the lower index
+                                if (best < 0 || le > bv) {
+                                    best = e;
+                                    bv = le;
+                                }
+                            }
+                        }
+                        taken |= 1u << best;
+                        seli[j] = best;
+                        selv[j] = bv;
+                    }
+                }
+                float ex[8], den = 0.0f;
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    if (j < k) {
+                        ex[j] = expf(selv[j] - selv[0]);
+                        den += ex[j];
+                    }
+                }
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    if (j < k) {
+                        topk_ids[t * k + j] = seli[j];
+                        topk_w[t * k + j] = ex[j] / den;
+                    }
+                }
+            }
+            __syncthreads();
+            continue;
+        }
         if (wave == 0) {
             Cand me;
             me.v = lane < E ? lg[lane] : -INFINITY;
