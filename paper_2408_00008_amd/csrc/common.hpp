@@ -30,7 +30,13 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi)
     return static_cast<uint32_t>(f32_to_bf16(lo)) | (static_cast<uint32_t>(f32_to_bf16(hi)) << 16);
 }
 
-__device__ __forceinline__ float silu(float z) { return z / (1.0f + expf(-z)); }
+// silu(z) = z / (1 + exp(-z)) with the hardware exp2 and reciprocal (a few
+// ulp in f32; the result is rounded to bf16).  Large negative z: exp -> inf,
+// reciprocal -> 0, silu -> -0.
+__device__ __forceinline__ float silu(float z)
+{
+    return z * __builtin_amdgcn_rcpf(1.0f + __expf(-z));
+}
 
 // 16x16x32 bf16 MFMA, f32 accumulate (gfx950).  Operand A: lane l holds row
 // (l % 16), reduction elements 8*(l/16) .. +7; operand B: lane l holds column

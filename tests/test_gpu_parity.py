@@ -171,6 +171,9 @@ def test_forward_sampled(name, variant):
     (200, 64, 128, 16, 2),    # many experts, several tiles of rows
     (300, 128, 192, 64, 8),   # E = 64, k = 8 limits
     (513, 256, 512, 8, 2),    # rows per expert > 64
+    (700, 256, 256, 4, 2),    # several ragged 256-row token tiles per expert
+    (1000, 512, 384, 8, 2),   # odd count of 128-column output blocks
+    (96, 256, 128, 64, 8),    # E = 64 with 1..20 rows per expert
 ])
 @pytest.mark.parametrize("variant", [1, 2])
 def test_forward_shapes(shape, variant):
