@@ -43,7 +43,23 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="target wall time of the oracle baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration-mib", type=int, default=0,
+                    help="only run a plain device copy of this many MiB (3 times), for "
+                         "scaling rocprofv3 FETCH_SIZE/WRITE_SIZE counters")
     return ap.parse_args()
+
+
+def copy_calibration(mib: int):
+    import torch
+
+    n = mib * 1024 * 1024
+    src = torch.empty(n, dtype=torch.uint8, device="cuda:0").fill_(1)
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration_bytes": n, "launches": 3}), flush=True)
 
 
 def source_digest(path: str) -> str:
@@ -66,6 +82,8 @@ def load_traffic(workload: str, kernel: str, family: str):
 
 def main():
     args = parse()
+    if args.copy_calibration_mib:
+        return copy_calibration(args.copy_calibration_mib)
     if args.gpus != 1:
         print(f"bench.py: this build runs on exactly one GPU (asked for --gpus {args.gpus}); "
               "the MoE layer is measured at N=1 only", file=sys.stderr)

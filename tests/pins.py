@@ -300,6 +300,22 @@ def pin_rmsnorm(o):
     _close(a, ref.numpy(), rtol=1e-13, atol=1e-15)
 
 
+def pin_gates_for_ids(o):
+    """Gates of a given expert choice: equal to the routed gates for the
+    oracle's own choice, and to brute-force softmax values for another one."""
+    c = tiny_case(12, 16, 8, 6, 3, seed=47)
+    r = _run(o, c)
+    g = o.gates_for_ids(r["logits"], r["ids"])
+    assert np.array_equal(g, r["gates"])
+    other = np.array([[5, 0, 2]] * 12, np.int32)
+    g2 = o.gates_for_ids(r["logits"], other)
+    for t in range(12):
+        lg = r["logits"][t]
+        ex = [math.exp(lg[e] - lg[5]) for e in (5, 0, 2)]
+        ref = [v / sum(ex) for v in ex]
+        _close(g2[t], ref, rtol=1e-14, atol=1e-16)
+
+
 def pin_empty(o):
     """T = 0 is a valid, empty layer."""
     c = tiny_case(1, 8, 8, 4, 2, seed=43)
@@ -322,5 +338,6 @@ ALL_PINS = [
     pin_hand_example,
     pin_dispatch,
     pin_rmsnorm,
+    pin_gates_for_ids,
     pin_empty,
 ]
