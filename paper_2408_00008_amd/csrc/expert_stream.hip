@@ -51,7 +51,7 @@ struct StreamCfg {
     static constexpr int MT = 16 * G;             // token rows per pass (at most)
     static constexpr int LDK = KC + 8;            // padded LDS row (bf16 elements)
     static constexpr int NMAT = UP ? 2 : 1;
-    static constexpr int TILE_BYTES = KS * MT * LDK * 2;
+    static constexpr int TILE_BYTES = 2 * KS * MT * LDK * 2;  // double-buffered
     static constexpr int RED_BYTES = (KS - 1) * NS * 64 * G * 4 * NMAT * 4;
     static constexpr int LDS_BYTES = TILE_BYTES > RED_BYTES ? TILE_BYTES : RED_BYTES;
 };
@@ -83,7 +83,8 @@ __device__ __forceinline__ void stream_pass(const StreamParams& p, unsigned char
     constexpr int GT = 64 * NS;  // threads that stage one token tile
     constexpr int TILE_LOADS = 16 * GA * KC / 8;
     constexpr int TPT = (TILE_LOADS + GT - 1) / GT;
-    bf16_t* tile = reinterpret_cast<bf16_t*>(smem) + x.ks * C::MT * C::LDK;
+    // two token tiles per reduction share, used by alternate chunks
+    bf16_t* tiles = reinterpret_cast<bf16_t*>(smem) + x.ks * 2 * C::MT * C::LDK;
     const int lane = x.lane;
 
     const bf16_t* src[TPT];
@@ -123,9 +124,11 @@ __device__ __forceinline__ void stream_pass(const StreamParams& p, unsigned char
     // stage chunk c's tokens, start loading chunk c+1, multiply chunk c.  The
     // load is unconditional (the last chunk re-reads itself) so that the
     // compiler's memory-counter waits stay exact and the loads of chunk c+1
-    // remain in flight while chunk c is multiplied.
+    // remain in flight while chunk c is multiplied.  Chunk c's tile is the
+    // one chunk c-2 read; every wave finished those reads before it reached
+    // chunk c-1's barrier, so one barrier per chunk suffices.
     auto step = [&](int c, R& cur, R& nxt) {
-        __syncthreads();
+        bf16_t* tile = tiles + (c & 1) * C::MT * C::LDK;
 #pragma unroll
         for (int it = 0; it < TPT; ++it)
             if (ldsoff[it] >= 0) *reinterpret_cast<uint4*>(tile + ldsoff[it]) = cur.t[it];
@@ -145,6 +148,7 @@ __device__ __forceinline__ void stream_pass(const StreamParams& p, unsigned char
 
     R r0, r1;
     load(r0, 0);
+    __syncthreads();  // the previous pass (or reduction) is done with the LDS
     for (int c = 0; c < x.nchunks; c += 2) {
         step(c, r0, r1);
         if (c + 1 < x.nchunks) step(c + 1, r1, r0);
@@ -302,9 +306,15 @@ hipError_t launch_stream_up(const UpArgs& a, int64_t, hipStream_t stream)
     p.E = a.E;
     p.h_out = a.h;
     const int G = stream_groups(a.A, a.E);
-    const bool k128 = a.d % 128 == 0;
-    if (G == 2) return k128 ? run<true, 4, 1, 2, 128>(p, stream) : run<true, 4, 1, 2, 64>(p, stream);
-    if (G == 4) return k128 ? run<true, 4, 1, 4, 128>(p, stream) : run<true, 4, 1, 4, 64>(p, stream);
+    if (G == 2) {
+        if (a.d % 256 == 0) return run<true, 4, 1, 2, 256>(p, stream);
+        if (a.d % 128 == 0) return run<true, 4, 1, 2, 128>(p, stream);
+        return run<true, 4, 1, 2, 64>(p, stream);
+    }
+    if (G == 4) {
+        if (a.d % 128 == 0) return run<true, 4, 1, 4, 128>(p, stream);
+        return run<true, 4, 1, 4, 64>(p, stream);
+    }
     return run<true, 4, 1, 8, 64>(p, stream);
 }
 
@@ -322,14 +332,14 @@ hipError_t launch_stream_down(const DownArgs& a, int64_t, hipStream_t stream)
     p.perm = a.perm;
     const int G = stream_groups(a.A, a.E);
     if (G == 2) {
-        if (a.ffn % 256 == 0) return run<false, 4, 1, 2, 256>(p, stream);
+        if (a.d % 128 == 0 && a.ffn % 128 == 0) return run<false, 8, 1, 2, 128>(p, stream);
         return run<false, 4, 1, 2, 64>(p, stream);
     }
     if (G == 4) {
         if (a.ffn % 128 == 0) return run<false, 4, 1, 4, 128>(p, stream);
         return run<false, 4, 1, 4, 64>(p, stream);
     }
-    return run<false, 2, 1, 8, 64>(p, stream);
+    return run<false, 4, 1, 8, 64>(p, stream);
 }
 
 }  // namespace moe
