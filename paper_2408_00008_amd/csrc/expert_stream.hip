@@ -6,16 +6,19 @@
 // intensity = rows per expert flop/byte, far below the MFMA/HBM ridge).  The
 // kernels therefore read every weight byte exactly once:
 //
-//   * a workgroup owns one expert e and a slab of 16*NS weight rows; each wave
-//     of the slab owns 16 rows and a 1/KS share of the reduction dimension;
+//   * a workgroup owns one expert e and a slab of weight rows; each wave owns
+//     16 rows (of w1 or w3 in UP, of w2 in DOWN) and a 1/KS share of the
+//     reduction dimension;
 //   * weights go straight from HBM into registers as the A operand of a
 //     16x16x32 bf16 MFMA (lane l reads 16 contiguous bytes of row l%16), one
 //     chunk of KC reduction elements ahead of the MFMAs that consume them;
 //   * the expert's token rows (<= 16*G per pass) are staged through LDS once
 //     per chunk and shared by the NS waves of a reduction share (B operand);
-//   * UP fuses w1 and w3 (two accumulators over the same token fragment) and
-//     the SiLU*mul epilogue, writing h in bf16; DOWN fuses the gate-weighted
-//     scatter of each row back to its (token, slot) position in f32;
+//   * UP pairs waves: one streams 16 rows of w1, its partner the same rows of
+//     w3, both against the same token fragments; the partner hands its result
+//     over through LDS for the fused SiLU*mul epilogue (h in bf16).  DOWN
+//     fuses the gate-weighted scatter of each row back to its (token, slot)
+//     position in f32;
 //   * partial sums of the KS reduction shares are added in LDS in a fixed
 //     order, so results are bitwise reproducible.
 //
@@ -44,16 +47,22 @@ struct StreamParams {
     const int32_t* perm;     // DOWN
 };
 
-template <bool UP, int NS, int KS, int G, int KC>
+// SPLIT (UP only): waves ns < NS/2 stream w1 rows, waves ns >= NS/2 the same
+// rows of w3; u and v meet in LDS for the SiLU*mul epilogue.  Each wave then
+// carries one matrix, like DOWN, which halves its registers.
+template <bool UP, int NS, int KS, int G, int KC, bool SPLIT = false>
 struct StreamCfg {
     static constexpr int THREADS = 64 * NS * KS;
-    static constexpr int ROWS = 16 * NS;          // weight rows per workgroup
+    static constexpr int ROWS = SPLIT ? 16 * NS / 2 : 16 * NS;  // output rows per workgroup
     static constexpr int MT = 16 * G;             // token rows per pass (at most)
     static constexpr int LDK = KC + 8;            // padded LDS row (bf16 elements)
-    static constexpr int NMAT = UP ? 2 : 1;
+    static constexpr int NMAT = (UP && !SPLIT) ? 2 : 1;
     static constexpr int TILE_BYTES = 2 * KS * MT * LDK * 2;  // double-buffered
     static constexpr int RED_BYTES = (KS - 1) * NS * 64 * G * 4 * NMAT * 4;
-    static constexpr int LDS_BYTES = TILE_BYTES > RED_BYTES ? TILE_BYTES : RED_BYTES;
+    static constexpr int SPLIT_BYTES = SPLIT ? (NS / 2) * 64 * G * 4 * 4 : 0;
+    static constexpr int LDS_A = TILE_BYTES > RED_BYTES ? TILE_BYTES : RED_BYTES;
+    static constexpr int LDS_BYTES = LDS_A > SPLIT_BYTES ? LDS_A : SPLIT_BYTES;
+    static_assert(!SPLIT || (UP && KS == 1 && NS % 2 == 0), "SPLIT: UP, no K split, even NS");
 };
 
 // Registers of one reduction chunk: the staged token loads and the weight
@@ -74,11 +83,12 @@ struct PassCtx {
 // One pass over at most 16*GA token rows of expert e for this workgroup's
 // weight rows.  GA is the number of 16-row groups actually computed (a
 // compile-time count, so the MFMA sequence has no data-dependent branches).
-template <bool UP, int NS, int KS, int G, int KC, int GA>
+template <bool UP, int NS, int KS, int G, int KC, int GA, bool SPLIT>
 __device__ __forceinline__ void stream_pass(const StreamParams& p, unsigned char* smem,
                                             const PassCtx& x)
 {
-    using C = StreamCfg<UP, NS, KS, G, KC>;
+    using C = StreamCfg<UP, NS, KS, G, KC, SPLIT>;
+    constexpr bool TWO = UP && !SPLIT;  // two weight matrices per wave
     constexpr int KSTEPS = KC / 32;
     constexpr int GT = 64 * NS;  // threads that stage one token tile
     constexpr int TILE_LOADS = 16 * GA * KC / 8;
@@ -109,7 +119,7 @@ __device__ __forceinline__ void stream_pass(const StreamParams& p, unsigned char
         accB[g] = floatx4{0.f, 0.f, 0.f, 0.f};
     }
 
-    using R = ChunkRegs<TPT, KSTEPS, UP>;
+    using R = ChunkRegs<TPT, KSTEPS, TWO>;
     auto load = [&](R& r, int c) {
         const int ko = c * KC;
 #pragma unroll
@@ -118,7 +128,7 @@ __device__ __forceinline__ void stream_pass(const StreamParams& p, unsigned char
 #pragma unroll
         for (int kk = 0; kk < KSTEPS; ++kk) {
             r.a[kk] = as_bf16x8(ldg16(x.pa + ko + kk * 32));
-            if (UP) r.b[kk] = as_bf16x8(ldg16(x.pb + ko + kk * 32));
+            if (TWO) r.b[kk] = as_bf16x8(ldg16(x.pb + ko + kk * 32));
         }
     };
     // stage chunk c's tokens, start loading chunk c+1, multiply chunk c.  The
@@ -141,7 +151,7 @@ __device__ __forceinline__ void stream_pass(const StreamParams& p, unsigned char
                 const bf16x8 b = *reinterpret_cast<const bf16x8*>(
                     tile + (g * 16 + (lane & 15)) * C::LDK + kk * 32 + 8 * (lane >> 4));
                 accA[g] = mfma16x16x32(cur.a[kk], b, accA[g]);
-                if (UP) accB[g] = mfma16x16x32(cur.b[kk], b, accB[g]);
+                if (TWO) accB[g] = mfma16x16x32(cur.b[kk], b, accB[g]);
             }
         }
     };
@@ -186,7 +196,27 @@ __device__ __forceinline__ void stream_pass(const StreamParams& p, unsigned char
         }
     }
 
-    if (x.ks == 0) {
+    if constexpr (SPLIT) {
+        // the w3 waves hand v to the w1 waves of the same output rows
+        __syncthreads();
+        float* xv = reinterpret_cast<float*>(smem);
+        const int pair = x.ns % (NS / 2);
+        if (x.ns >= NS / 2) {
+#pragma unroll
+            for (int g = 0; g < GA; ++g)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) xv[((pair * G + g) * 4 + i) * 64 + lane] = accA[g][i];
+        }
+        __syncthreads();
+        if (x.ns < NS / 2) {
+#pragma unroll
+            for (int g = 0; g < GA; ++g)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) accB[g][i] = xv[((pair * G + g) * 4 + i) * 64 + lane];
+        }
+    }
+
+    if (x.ks == 0 && (!SPLIT || x.ns < NS / 2)) {
         const int n = x.n0 + 4 * (lane >> 4);
 #pragma unroll
         for (int g = 0; g < GA; ++g) {
@@ -219,10 +249,10 @@ __device__ __forceinline__ void stream_pass(const StreamParams& p, unsigned char
     __syncthreads();
 }
 
-template <bool UP, int NS, int KS, int G, int KC>
+template <bool UP, int NS, int KS, int G, int KC, bool SPLIT>
 __global__ __launch_bounds__(64 * NS * KS) void stream_kernel(StreamParams p)
 {
-    using C = StreamCfg<UP, NS, KS, G, KC>;
+    using C = StreamCfg<UP, NS, KS, G, KC, SPLIT>;
     __shared__ __attribute__((aligned(16))) unsigned char smem[C::LDS_BYTES];
 
     // one workgroup per (expert, weight slab), expert-major: the workgroups in
@@ -242,14 +272,19 @@ __global__ __launch_bounds__(64 * NS * KS) void stream_kernel(StreamParams p)
     x.ks = wave / NS;
     x.gt = tid % (64 * NS);
     x.e = e;
-    x.n0 = nb * C::ROWS + x.ns * 16;
+    x.n0 = nb * C::ROWS + (SPLIT ? x.ns % (NS / 2) : x.ns) * 16;
     x.row0 = row0;
     const int kper = p.K / KS;
     x.kbeg = x.ks * kper;
     x.nchunks = kper / KC;
     const int64_t wrow = (int64_t)e * p.N + x.n0 + (x.lane & 15);
-    x.pa = p.wa + wrow * p.K + x.kbeg + 8 * (x.lane >> 4);
-    x.pb = UP ? p.wb + wrow * p.K + x.kbeg + 8 * (x.lane >> 4) : nullptr;
+    if (SPLIT) {
+        x.pa = (x.ns < NS / 2 ? p.wa : p.wb) + wrow * p.K + x.kbeg + 8 * (x.lane >> 4);
+        x.pb = nullptr;
+    } else {
+        x.pa = p.wa + wrow * p.K + x.kbeg + 8 * (x.lane >> 4);
+        x.pb = UP ? p.wb + wrow * p.K + x.kbeg + 8 * (x.lane >> 4) : nullptr;
+    }
 
     // rows beyond 16*G are taken in further passes over the same slab (the
     // slab is re-read; one workgroup per slab measured faster than spreading
@@ -259,25 +294,25 @@ __global__ __launch_bounds__(64 * NS * KS) void stream_kernel(StreamParams p)
         x.Mp = min(M - m0, C::MT);
         const int gact = (x.Mp + 15) >> 4;
         if (gact <= 1) {
-            stream_pass<UP, NS, KS, G, KC, 1>(p, smem, x);
+            stream_pass<UP, NS, KS, G, KC, 1, SPLIT>(p, smem, x);
         } else if (gact <= 2) {
-            if constexpr (G >= 2) stream_pass<UP, NS, KS, G, KC, 2>(p, smem, x);
+            if constexpr (G >= 2) stream_pass<UP, NS, KS, G, KC, 2, SPLIT>(p, smem, x);
         } else if (gact <= 4) {
-            if constexpr (G >= 4) stream_pass<UP, NS, KS, G, KC, 4>(p, smem, x);
+            if constexpr (G >= 4) stream_pass<UP, NS, KS, G, KC, 4, SPLIT>(p, smem, x);
         } else if (gact <= 8) {
-            if constexpr (G >= 8) stream_pass<UP, NS, KS, G, KC, 8>(p, smem, x);
+            if constexpr (G >= 8) stream_pass<UP, NS, KS, G, KC, 8, SPLIT>(p, smem, x);
         } else {
-            if constexpr (G >= 16) stream_pass<UP, NS, KS, G, KC, 16>(p, smem, x);
+            if constexpr (G >= 16) stream_pass<UP, NS, KS, G, KC, 16, SPLIT>(p, smem, x);
         }
     }
 }
 
-template <bool UP, int NS, int KS, int G, int KC>
+template <bool UP, int NS, int KS, int G, int KC, bool SPLIT = false>
 hipError_t run(const StreamParams& p, hipStream_t stream)
 {
-    using C = StreamCfg<UP, NS, KS, G, KC>;
+    using C = StreamCfg<UP, NS, KS, G, KC, SPLIT>;
     const unsigned grid = static_cast<unsigned>(p.E * (p.N / C::ROWS));
-    stream_kernel<UP, NS, KS, G, KC><<<grid, C::THREADS, 0, stream>>>(p);
+    stream_kernel<UP, NS, KS, G, KC, SPLIT><<<grid, C::THREADS, 0, stream>>>(p);
     return hipGetLastError();
 }
 
@@ -305,17 +340,18 @@ hipError_t launch_stream_up(const UpArgs& a, int64_t, hipStream_t stream)
     p.K = a.d;
     p.E = a.E;
     p.h_out = a.h;
+    // 8 waves: 4 stream w1 rows, 4 the same w3 rows (SPLIT)
     const int G = stream_groups(a.A, a.E);
     if (G == 2) {
-        if (a.d % 256 == 0) return run<true, 4, 1, 2, 256>(p, stream);
-        if (a.d % 128 == 0) return run<true, 4, 1, 2, 128>(p, stream);
-        return run<true, 4, 1, 2, 64>(p, stream);
+        if (a.d % 256 == 0) return run<true, 8, 1, 2, 256, true>(p, stream);
+        if (a.d % 128 == 0) return run<true, 8, 1, 2, 128, true>(p, stream);
+        return run<true, 8, 1, 2, 64, true>(p, stream);
     }
     if (G == 4) {
-        if (a.d % 128 == 0) return run<true, 4, 1, 4, 128>(p, stream);
-        return run<true, 4, 1, 4, 64>(p, stream);
+        if (a.d % 128 == 0) return run<true, 8, 1, 4, 128, true>(p, stream);
+        return run<true, 8, 1, 4, 64, true>(p, stream);
     }
-    return run<true, 4, 1, 8, 64>(p, stream);
+    return run<true, 8, 1, 8, 64, true>(p, stream);
 }
 
 hipError_t launch_stream_down(const DownArgs& a, int64_t, hipStream_t stream)
