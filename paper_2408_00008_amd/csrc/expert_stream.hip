@@ -318,13 +318,14 @@ hipError_t run(const StreamParams& p, hipStream_t stream)
 
 }  // namespace
 
-// Tile shape by the mean rows per expert (A/E), from a sweep on MI355X at the
-// Mixtral shapes: 16*G rows per pass keeps about 2x headroom over the mean,
-// and the chunk length KC trades bytes in flight against registers.
+// Tile shape by the mean rows per expert (A/E), from sweeps on MI355X at the
+// Mixtral shapes: 16*G rows per pass keeps about 2x headroom over the mean
+// (4x for the largest tile, which also covers a skewed hot expert in one
+// pass), and the chunk length KC trades bytes in flight against registers.
 int stream_groups(int64_t A, int E)
 {
     const int64_t mean = (A + E - 1) / E;
-    return mean <= 24 ? 2 : (mean <= 48 ? 4 : 8);
+    return mean <= 24 ? 2 : (mean <= 48 ? 4 : 16);
 }
 
 hipError_t launch_stream_up(const UpArgs& a, int64_t, hipStream_t stream)
@@ -351,7 +352,7 @@ hipError_t launch_stream_up(const UpArgs& a, int64_t, hipStream_t stream)
         if (a.d % 128 == 0) return run<true, 8, 1, 4, 128, true>(p, stream);
         return run<true, 8, 1, 4, 64, true>(p, stream);
     }
-    return run<true, 8, 1, 8, 64, true>(p, stream);
+    return run<true, 8, 1, 16, 64, true>(p, stream);
 }
 
 hipError_t launch_stream_down(const DownArgs& a, int64_t, hipStream_t stream)
@@ -375,7 +376,8 @@ hipError_t launch_stream_down(const DownArgs& a, int64_t, hipStream_t stream)
         if (a.ffn % 128 == 0) return run<false, 4, 1, 4, 128>(p, stream);
         return run<false, 4, 1, 4, 64>(p, stream);
     }
-    return run<false, 4, 1, 8, 64>(p, stream);
+    if (a.d % 128 == 0) return run<false, 8, 1, 16, 64>(p, stream);
+    return run<false, 4, 1, 16, 64>(p, stream);
 }
 
 }  // namespace moe
