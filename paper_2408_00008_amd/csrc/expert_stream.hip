@@ -24,7 +24,8 @@
 //
 // Per-expert row counts come from the device-side offsets; experts with no
 // rows exit at once and no host synchronisation is needed.  An expert with
-// more than 16*G rows is processed in several passes over its slab.
+// more than 16*G rows is cut into several passes over its slab, which run as
+// separate workgroups placed to share the slab's weights through L2.
 #include "common.hpp"
 #include "launch.hpp"
 
@@ -45,6 +46,7 @@ struct StreamParams {
     float* y_out;            // DOWN [A, N]
     const float* topk_w;     // DOWN, null = unweighted row order
     const int32_t* perm;     // DOWN
+    int passes;              // workgroups per slab (each takes every passes-th pass)
 };
 
 // SPLIT (UP only): waves ns < NS/2 stream w1 rows, waves ns >= NS/2 the same
@@ -256,14 +258,51 @@ __global__ __launch_bounds__(64 * NS * KS) void stream_kernel(StreamParams p)
     using C = StreamCfg<UP, NS, KS, G, KC, SPLIT>;
     __shared__ __attribute__((aligned(16))) unsigned char smem[C::LDS_BYTES];
 
-    // one workgroup per (expert, weight slab), expert-major: the workgroups in
-    // flight stream neighbouring slabs of the same expert
+    // Workgroup -> (expert e, slab nb, pass slot q).  An expert's rows are
+    // cut into P_e = ceil(M_e/MT) balanced passes and it gets Q_e =
+    // min(P_e, passes) pass slots per slab; slot q takes passes q, q + Q_e, ...
+    // The items are numbered densely, expert-major, so the workgroups past
+    // the last item (the grid is sized for the worst case) come last and exit
+    // at once.  Within an expert the order is (group of 8 slabs, pass slot,
+    // slab % 8): dispatch places consecutive workgroups on consecutive XCDs,
+    // so all pass slots of a slab land on the same XCD one after another and
+    // the passes that re-read the slab's weights find them in that XCD's L2.
+    __shared__ int s_first[65];  // first item of expert e
     const int nbn = p.N / C::ROWS;
-    const int e = blockIdx.x / nbn;
-    const int nb = blockIdx.x - e * nbn;
+    const int nbn8 = (nbn + 7) & ~7;
+    if (threadIdx.x < 64) {
+        const int t = threadIdx.x;
+        int items = 0;
+        if (t < p.E) {
+            const int Mt = p.offsets[t + 1] - p.offsets[t];
+            const int P = (Mt + C::MT - 1) / C::MT;
+            items = nbn8 * (P < p.passes ? P : p.passes);
+        }
+        // inclusive scan over the wave
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+            const int v = __shfl_up(items, o, 64);
+            if (t >= o) items += v;
+        }
+        if (t < p.E) s_first[t + 1] = items;
+        if (t == 0) s_first[0] = 0;
+    }
+    __syncthreads();
+    const int b = blockIdx.x;
+    if (b >= s_first[p.E]) return;
+    int e = 0;
+    while (s_first[e + 1] <= b) ++e;
     const int row0 = p.offsets[e];
     const int M = p.offsets[e + 1] - row0;
-    if (M <= 0) return;
+    const int npass = (M + C::MT - 1) / C::MT;
+    const int nslot = npass < p.passes ? npass : p.passes;
+    const int local = b - s_first[e];
+    const int grp = local / (8 * nslot);
+    const int rem = local - grp * 8 * nslot;
+    const int q = rem >> 3;
+    const int nb = grp * 8 + (rem & 7);
+    if (nb >= nbn) return;
+    const int rp = (M + npass - 1) / npass;  // rows per pass, balanced
 
     PassCtx x;
     const int tid = threadIdx.x;
@@ -278,13 +317,14 @@ __global__ __launch_bounds__(64 * NS * KS) void stream_kernel(StreamParams p)
     const int kper = p.K / KS;
     x.kbeg = x.ks * kper;
     x.nchunks = kper / KC;
-    // Each workgroup walks its chunks starting at a rotated position, so the
+    // Each slab walks its chunks starting at a rotated position, so the
     // workgroups in flight read different columns of their rows at any one
-    // time (measured: all starting at column 0 costs about 10% of the read
-    // bandwidth).  Consecutive dispatch groups of 8 (one workgroup per XCD)
-    // share a rotation.  The reduction order changes with it; results stay
-    // deterministic for a given launch.
-    x.rot = static_cast<int>((static_cast<unsigned>(blockIdx.x >> 3) * 5u) % static_cast<unsigned>(x.nchunks));
+    // time (all starting at column 0 measured about 10% slower).  Slabs of one
+    // group of 8 (one per XCD) share a rotation, and so do the passes of a
+    // slab, which then read the same chunks at about the same time.  The
+    // reduction order changes with it; results stay deterministic.
+    x.rot = static_cast<int>((static_cast<unsigned>(e * (nbn8 >> 3) + grp) * 5u) %
+                             static_cast<unsigned>(x.nchunks));
     const int64_t wrow = (int64_t)e * p.N + x.n0 + (x.lane & 15);
     if (SPLIT) {
         x.pa = (x.ns < NS / 2 ? p.wa : p.wb) + wrow * p.K + x.kbeg + 8 * (x.lane >> 4);
@@ -294,12 +334,9 @@ __global__ __launch_bounds__(64 * NS * KS) void stream_kernel(StreamParams p)
         x.pb = UP ? p.wb + wrow * p.K + x.kbeg + 8 * (x.lane >> 4) : nullptr;
     }
 
-    // rows beyond 16*G are taken in further passes over the same slab (the
-    // slab is re-read; one workgroup per slab measured faster than spreading
-    // an expert's rows over several workgroups)
-    for (int m0 = 0; m0 < M; m0 += C::MT) {
-        x.m0 = m0;
-        x.Mp = min(M - m0, C::MT);
+    for (int pass = q; pass < npass; pass += nslot) {
+        x.m0 = pass * rp;
+        x.Mp = min(M - x.m0, rp);
         const int gact = (x.Mp + 15) >> 4;
         if (gact <= 1) {
             stream_pass<UP, NS, KS, G, KC, 1, SPLIT>(p, smem, x);
@@ -316,10 +353,16 @@ __global__ __launch_bounds__(64 * NS * KS) void stream_kernel(StreamParams p)
 }
 
 template <bool UP, int NS, int KS, int G, int KC, bool SPLIT = false>
-hipError_t run(const StreamParams& p, hipStream_t stream)
+hipError_t run(StreamParams p, int64_t rows_max, hipStream_t stream)
 {
+    // pass slots per slab: enough for an expert that takes rows_max rows
+    // (every token at most once), at most 8
+    constexpr int MT = StreamCfg<UP, NS, KS, G, KC, SPLIT>::MT;
+    const int64_t need = (rows_max + MT - 1) / MT;
+    p.passes = static_cast<int>(need < 1 ? 1 : (need > 8 ? 8 : need));
     using C = StreamCfg<UP, NS, KS, G, KC, SPLIT>;
-    const unsigned grid = static_cast<unsigned>(p.E * (p.N / C::ROWS));
+    const int nbn8 = (p.N / C::ROWS + 7) & ~7;
+    const unsigned grid = static_cast<unsigned>(p.E * nbn8 * p.passes);
     stream_kernel<UP, NS, KS, G, KC, SPLIT><<<grid, C::THREADS, 0, stream>>>(p);
     return hipGetLastError();
 }
@@ -327,16 +370,17 @@ hipError_t run(const StreamParams& p, hipStream_t stream)
 }  // namespace
 
 // Tile shape by the mean rows per expert (A/E), from sweeps on MI355X at the
-// Mixtral shapes: 16*G rows per pass keeps about 2x headroom over the mean
-// (4x for the largest tile, which also covers a skewed hot expert in one
-// pass), and the chunk length KC trades bytes in flight against registers.
+// Mixtral shapes: 32-row passes while the mean is small, 64-row passes above;
+// an expert with more rows than one pass holds is cut into several passes,
+// which run as separate workgroups.  The chunk length KC trades bytes in
+// flight against registers.
 int stream_groups(int64_t A, int E)
 {
     const int64_t mean = (A + E - 1) / E;
-    return mean <= 24 ? 2 : (mean <= 48 ? 4 : 16);
+    return mean <= 24 ? 2 : 4;
 }
 
-hipError_t launch_stream_up(const UpArgs& a, int64_t, hipStream_t stream)
+hipError_t launch_stream_up(const UpArgs& a, int64_t rows_max, hipStream_t stream)
 {
     StreamParams p{};
     p.act = a.x;
@@ -350,20 +394,16 @@ hipError_t launch_stream_up(const UpArgs& a, int64_t, hipStream_t stream)
     p.E = a.E;
     p.h_out = a.h;
     // 8 waves: 4 stream w1 rows, 4 the same w3 rows (SPLIT)
-    const int G = stream_groups(a.A, a.E);
-    if (G == 2) {
-        if (a.d % 256 == 0) return run<true, 8, 1, 2, 256, true>(p, stream);
-        if (a.d % 128 == 0) return run<true, 8, 1, 2, 128, true>(p, stream);
-        return run<true, 8, 1, 2, 64, true>(p, stream);
+    if (stream_groups(a.A, a.E) == 2) {
+        if (a.d % 256 == 0) return run<true, 8, 1, 2, 256, true>(p, rows_max, stream);
+        if (a.d % 128 == 0) return run<true, 8, 1, 2, 128, true>(p, rows_max, stream);
+        return run<true, 8, 1, 2, 64, true>(p, rows_max, stream);
     }
-    if (G == 4) {
-        if (a.d % 128 == 0) return run<true, 8, 1, 4, 128, true>(p, stream);
-        return run<true, 8, 1, 4, 64, true>(p, stream);
-    }
-    return run<true, 8, 1, 16, 64, true>(p, stream);
+    if (a.d % 128 == 0) return run<true, 8, 1, 4, 128, true>(p, rows_max, stream);
+    return run<true, 8, 1, 4, 64, true>(p, rows_max, stream);
 }
 
-hipError_t launch_stream_down(const DownArgs& a, int64_t, hipStream_t stream)
+hipError_t launch_stream_down(const DownArgs& a, int64_t rows_max, hipStream_t stream)
 {
     StreamParams p{};
     p.act = a.h;
@@ -375,17 +415,12 @@ hipError_t launch_stream_down(const DownArgs& a, int64_t, hipStream_t stream)
     p.y_out = a.y;
     p.topk_w = a.topk_w;
     p.perm = a.perm;
-    const int G = stream_groups(a.A, a.E);
-    if (G == 2) {
-        if (a.d % 128 == 0 && a.ffn % 128 == 0) return run<false, 8, 1, 2, 128>(p, stream);
-        return run<false, 4, 1, 2, 64>(p, stream);
+    if (stream_groups(a.A, a.E) == 2) {
+        if (a.d % 128 == 0 && a.ffn % 128 == 0) return run<false, 8, 1, 2, 128>(p, rows_max, stream);
+        return run<false, 4, 1, 2, 64>(p, rows_max, stream);
     }
-    if (G == 4) {
-        if (a.ffn % 128 == 0) return run<false, 4, 1, 4, 128>(p, stream);
-        return run<false, 4, 1, 4, 64>(p, stream);
-    }
-    if (a.d % 128 == 0) return run<false, 8, 1, 16, 64>(p, stream);
-    return run<false, 4, 1, 16, 64>(p, stream);
+    if (a.ffn % 128 == 0) return run<false, 4, 1, 4, 128>(p, rows_max, stream);
+    return run<false, 4, 1, 4, 64>(p, rows_max, stream);
 }
 
 }  // namespace moe

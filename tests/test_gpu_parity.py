@@ -193,6 +193,19 @@ def test_forward_empty_experts():
     _forward_check(c)
 
 
+@pytest.mark.parametrize("variant", [1, 2])
+def test_forward_heavy_expert(variant):
+    """A bias that sends every token to expert 0 (and one other): expert 0
+    takes all T rows, more passes than a slab has pass slots, so slots loop."""
+    say(f"[forward] heavy expert variant {variant}")
+    bias = [60.0, 0.0, 0.0, 0.0]
+    c = small_case(700, 256, 256, 4, 2, seed=21, bias=bias)
+    ids, _, offs, _, _ = gpu_route(c)
+    o = offs.cpu().numpy()
+    assert o[1] - o[0] == c.T
+    _forward_check(c, variant=variant)
+
+
 def test_forward_t0():
     c = small_case(3, 64, 64, 4, 2)
     out = torch.zeros(0, 64, dtype=torch.bfloat16, device=DEV)
