@@ -4,17 +4,12 @@
 // intensity ~ rows per expert flop/byte, above the MI355X ridge of ~310), so
 // the kernels reuse both operands from LDS:
 //
-//   * a workgroup computes a BN x BM tile of the output (BN weight rows x BM
-//     token rows) with 32x32x16 bf16 MFMAs, f32 accumulation; its 8 waves are
-//     arranged WAVES_N x WAVES_M, each owning NT x MT tiles of 32x32;
-//   * both operand tiles of a 64-wide reduction step are staged through LDS
-//     (rows padded by 16 bytes so the 16-byte fragment reads of 16 lanes hit
-//     all 64 banks once), double-buffered: the global loads of step k+1 are in
-//     flight while step k is multiplied, one barrier per step;
-//   * UP pairs, in each wave, 32 rows of w1 with the same 32 rows of w3, so the
-//     two accumulators of an output element sit in the same lane and the
+//   * a workgroup computes a 256 x 256 tile of the output (256 weight rows x
+//     256 token rows) with 32x32x16 bf16 MFMAs, f32 accumulation;
+//   * UP stages 128 rows of w1 and the same 128 rows of w3, and each wave
+//     holds both accumulators of an output element in the same lane, so the
 //     SiLU*mul epilogue needs no data movement; token rows are gathered
-//     through the dispatch permutation while staging (no separate permute);
+//     through the dispatch permutation while loading (no separate permute);
 //   * DOWN scales each output row by its gate weight and scatters it to the
 //     row's (token, slot) position;
 //   * workgroups are persistent: one per CU, each walking a contiguous share
@@ -44,71 +39,116 @@ struct TiledParams {
     const int32_t* perm;     // DOWN
 };
 
-template <bool UP, int WAVES_N, int WAVES_M, int NT, int MT>
-struct TiledCfg {
-    static constexpr int THREADS = 64 * WAVES_N * WAVES_M;
-    static constexpr int BN = WAVES_N * NT * 32;  // weight rows staged per workgroup
-    static constexpr int BM = WAVES_M * MT * 32;  // token rows per workgroup
-    static constexpr int NOUT = UP ? BN / 2 : BN; // output columns per workgroup
+int cu_count();
+
+// ---- four-wave schedule ------------------------------------------------------
+//
+// The same 256 x 256 output tile per workgroup, computed by 4 waves, one per
+// SIMD, each owning a 128 x 128 quarter (16 accumulator tiles of 32 x 32,
+// 256 accumulator registers per lane).  Measured on MI355X: a wave that
+// interleaves about one 1 KB global->LDS load with four 32x32x16 MFMAs keeps
+// the MFMA pipe ~85% busy and sustains the 256 x 256 tile's load rate, while
+// loads issued by a second wave on a SIMD whose MFMAs run back to back are
+// throttled to about one per 32 cycles per CU.  So every wave carries its
+// own loads, fragment reads and MFMAs in one interleaved stream.
+//
+//   * operands go from global memory straight into LDS (16-byte loads that
+//     write LDS at base + 16 * lane, no registers); a step holds BK = 64
+//     reduction elements, so one load covers 8 rows x 128 bytes (whole cache
+//     lines; half-line rows measured 1.7x slower to issue);
+//   * the weight tile A (256 rows) lives in a ring of 3 slots, the token tile
+//     B (256 rows) in a ring of 2: 96 + 64 KB, all of the LDS.  During step j
+//     every wave issues its share of B(j+1) while it multiplies k-steps 0-1
+//     and of A(j+2) during k-steps 2-3; both slots were last read in step
+//     j-1.  At the end of step j it waits until only A(j+2) is outstanding
+//     (loads retire in order), then one barrier publishes step j+1;
+//   * fragments of k-step ks+1 are read while k-step ks multiplies;
+//   * LDS rows are 128 bytes, unpadded; the eight 16-byte chunks of row r are
+//     stored at slot chunk ^ ((r >> 1) & 7), so every fragment read (16
+//     consecutive rows, one chunk) hits 16 distinct bank groups;
+//   * loads past the last step re-load the last step into the free slot, so
+//     the wait counts are the same every step.
+template <bool UP>
+struct QCfg {
+    static constexpr int THREADS = 256;
+    static constexpr int BN = 256;                 // weight rows staged (UP: 128 w1 + 128 w3)
+    static constexpr int BM = 256;                 // token rows
+    static constexpr int NOUT = UP ? BN / 2 : BN;  // output columns per tile
     static constexpr int BK = 64;
-    static constexpr int LDK = BK + 8;            // padded LDS row, bf16 elements
-    static constexpr int A_ELEMS = BN * LDK;
-    static constexpr int STAGE_ELEMS = (BN + BM) * LDK;
-    static constexpr int LDS_BYTES = 2 * STAGE_ELEMS * 2;
-    static constexpr int A_LOADS = BN * BK / 8 / THREADS;
-    static constexpr int B_LOADS = BM * BK / 8 / THREADS;
-    static_assert(BN * BK / 8 % THREADS == 0 && BM * BK / 8 % THREADS == 0, "tile/threads");
-    static_assert(!UP || (A_LOADS % 2 == 0 && (A_LOADS / 2) * (THREADS / 8) == BN / 2),
-                  "UP: the first half of the A loads covers the w1 rows");
-    static_assert(!UP || NT % 2 == 0, "UP pairs each w1 tile with a w3 tile per wave");
+    static constexpr int ROWB = BK * 2;            // bytes per LDS row
+    static constexpr int SLOT = 256 * ROWB;        // 32 KB, one operand of one step
+    static constexpr int B_OFF = 3 * SLOT;
+    static constexpr int LDS_BYTES = 5 * SLOT;
+    static constexpr int NT = 4, MT = 4;           // 32x32 tiles per wave: 128 weight rows x 128 tokens
+    static constexpr int LOADS = 8;                // 8-row loads per wave per operand per step
 };
 
-template <bool UP, int WAVES_N, int WAVES_M, int NT, int MT>
-__global__ __launch_bounds__(64 * WAVES_N * WAVES_M) void tiled_kernel(TiledParams p)
-{
-    using C = TiledCfg<UP, WAVES_N, WAVES_M, NT, MT>;
-    extern __shared__ __attribute__((aligned(16))) bf16_t lds[];
-    __shared__ int s_items[65];  // items before expert e: nbn * (tiles of experts < e)
-    __shared__ int s_tiles[65];
+__device__ __forceinline__ int q_swz(int r) { return (r >> 1) & 7; }
 
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int wn = wave % WAVES_N, wm = wave / WAVES_N;
+// s_waitcnt with only the vector-memory count constrained (expcnt/lgkmcnt at max)
+template <int N>
+__device__ __forceinline__ void wait_vmem()
+{
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((N & 15) | 0x70 | 0xF00 | (((N >> 4) & 3) << 14));
+}
+
+// s_waitcnt lgkmcnt(0) with vmcnt/expcnt at max
+__device__ __forceinline__ void wait_lds() { __builtin_amdgcn_s_waitcnt(0xC07F); }
+
+template <bool UP>
+__global__ __launch_bounds__(256) void q_kernel(TiledParams p)
+{
+    using C = QCfg<UP>;
+    constexpr int NT = C::NT, MT = C::MT, L = C::LOADS;
+    extern __shared__ __attribute__((aligned(16))) unsigned char ring[];
+
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wr = wave & 1;   // weight half of this wave
+    const int wm = wave >> 1;  // token half of this wave
     const int nbn = p.N / C::NOUT;
 
-    if (tid < p.E) {
-        const int M = p.offsets[tid + 1] - p.offsets[tid];
-        s_tiles[tid + 1] = (M + C::BM - 1) / C::BM;
+    // per-expert token tiles and their prefix, one expert per lane:
+    // items before expert e = nbn * (token tiles of experts < e)
+    const int my_tiles = lane < p.E ? (p.offsets[lane + 1] - p.offsets[lane] + C::BM - 1) / C::BM : 0;
+    int in_tiles = my_tiles;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const int v = __shfl_up(in_tiles, o, 64);
+        if (lane >= o) in_tiles += v;
     }
-    __syncthreads();
-    if (tid == 0) {
-        int tiles = 0;
-        for (int e = 0; e < p.E; ++e) {
-            s_items[e] = nbn * tiles;
-            const int mt = s_tiles[e + 1];
-            s_tiles[e] = tiles;
-            tiles += mt;
-        }
-        s_items[p.E] = nbn * tiles;
-        s_tiles[p.E] = tiles;
-    }
-    __syncthreads();
-    const int total = s_items[p.E];
-
-    // this XCD's contiguous share of the items (workgroups are handed to the
-    // 8 XCDs round-robin; the grid is a multiple of 8)
+    const int ex_items = nbn * (in_tiles - my_tiles);
+    const int total = nbn * __shfl(in_tiles, p.E - 1, 64);
     const int xcd = blockIdx.x & 7;
     const int per_xcd = gridDim.x >> 3;
     const int local = blockIdx.x >> 3;
     const int beg = (int)((int64_t)total * xcd / 8);
     const int end = (int)((int64_t)total * (xcd + 1) / 8);
-
     const int nk = p.K / C::BK;
 
+    // a load covers 8 rows starting at a multiple of 8: lane l takes row l / 8
+    // and the global chunk stored at slot l % 8 (odd loads start at 8 mod 16)
+    const int lrow = lane >> 3;
+    const int lchunk[2] = {(lane & 7) ^ ((lrow >> 1) & 7), (lane & 7) ^ (((8 + lrow) >> 1) & 7)};
+    // fragment reads: row (tile base + lane % 32), chunk 2 ks + lane / 32; the
+    // tile bases are multiples of 32, so the swizzle depends on the lane only
+    int xk[4];
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks)
+        xk[ks] = (lane & 31) * C::ROWB + (((2 * ks + (lane >> 5)) ^ (((lane & 31) >> 1) & 7)) << 4);
+    // byte offset of this wave's nt-th 32-row weight tile in an A slot (UP:
+    // nt < 2 are w1 rows, nt + 2 the same rows of w3), and of its token tiles
+    const int a_wave = (UP ? wr * 64 : wr * 128) * C::ROWB;
+    const int b_wave = wm * 128 * C::ROWB;
+    auto atile = [](int nt) { return (UP ? (nt >> 1) * (C::BN / 2) + (nt & 1) * 32 : nt * 32) * C::ROWB; };
+
     for (int w = beg + local; w < end; w += per_xcd) {
-        int e = 0;
-        while (s_items[e + 1] <= w) ++e;
-        const int mt_e = s_tiles[e + 1] - s_tiles[e];
-        const int r = w - s_items[e];
+        // the expert of item w: the last one (with tiles) whose first item is <= w
+        const uint64_t le = __ballot(lane < p.E && my_tiles > 0 && ex_items <= w);
+        const int e = 63 - __builtin_clzll(le);
+        const int mt_e = __shfl(my_tiles, e, 64);
+        const int r = w - __shfl(ex_items, e, 64);
         const int nb = r / mt_e;
         const int mtile = r - nb * mt_e;
         const int row0 = p.offsets[e];
@@ -116,35 +156,43 @@ __global__ __launch_bounds__(64 * WAVES_N * WAVES_M) void tiled_kernel(TiledPara
         const int m0 = mtile * C::BM;
         const int Mp = min(C::BM, M - m0);
 
-        // global sources of this thread's 16-byte staging loads: load `it`
-        // covers tile row it * (THREADS/8) + tid/8, 16-byte column tid % 8
-        constexpr int RSTEP = C::THREADS / 8;
-        const int trow = tid >> 3, c8 = tid & 7;
-        const bf16_t* abase1;
-        const bf16_t* abase3 = nullptr;
-        if (UP) {
-            abase1 = p.wa + ((int64_t)e * p.N + nb * C::NOUT + trow) * p.K + c8 * 8;
-            abase3 = p.wb + ((int64_t)e * p.N + nb * C::NOUT + trow) * p.K + c8 * 8;
-        } else {
-            abase1 = p.wa + ((int64_t)e * p.N + nb * C::NOUT + trow) * p.K + c8 * 8;
-        }
-        int bsrc[C::B_LOADS];  // source token row of each B load
-#pragma unroll
-        for (int it = 0; it < C::B_LOADS; ++it) {
-            const int mm = it * RSTEP + trow;
-            const int rowm = row0 + m0 + (mm < Mp ? mm : Mp - 1);
-            bsrc[it] = (UP && p.gather) ? p.gather[rowm] / p.kslots : rowm;
-        }
-        auto a_ptr = [&](int it) -> const bf16_t* {
-            if (UP) {
-                constexpr int HALF = C::A_LOADS / 2;  // loads of w1 rows, then of w3 rows
-                return it < HALF ? abase1 + (int64_t)it * RSTEP * p.K
-                                 : abase3 + (int64_t)(it - HALF) * RSTEP * p.K;
+        // wave w loads A rows [64w, 64w + 64) and B rows [64w, 64w + 64); the
+        // 64 A rows are 64 consecutive rows of w1, w3 or w2
+        const bf16_t* abase;
+        {
+            const bf16_t* base = p.wa;
+            int wrow = nb * C::NOUT + 64 * wave;
+            if (UP && 64 * wave >= C::BN / 2) {
+                base = p.wb;
+                wrow -= C::BN / 2;
             }
-            return abase1 + (int64_t)it * RSTEP * p.K;
+            abase = base + ((int64_t)e * p.N + wrow) * p.K;
+        }
+        const bf16_t* aptr[2] = {abase + (int64_t)lrow * p.K + lchunk[0] * 8,
+                                 abase + (int64_t)lrow * p.K + lchunk[1] * 8};
+        const bf16_t* bptr[L];
+#pragma unroll
+        for (int i = 0; i < L; ++i) {
+            const int tr = 64 * wave + 8 * i + lrow;
+            const int rowm = row0 + m0 + (tr < Mp ? tr : Mp - 1);
+            const int64_t src = (UP && p.gather) ? p.gather[rowm] / p.kslots : rowm;
+            bptr[i] = p.act + src * p.K + lchunk[i & 1] * 8;
+        }
+        const int64_t astep = (int64_t)8 * p.K;  // elements between a wave's consecutive A loads
+        auto load_a = [&](int s, int i) {
+            unsigned char* st = ring + (s % 3) * C::SLOT;
+            int64_t ko = (int64_t)(s < nk ? s : nk - 1) * C::BK + i * astep;
+            __builtin_amdgcn_global_load_lds(
+                (const void __attribute__((address_space(1)))*)(aptr[i & 1] + ko),
+                (void __attribute__((address_space(3)))*)(st + (64 * wave + 8 * i) * C::ROWB), 16, 0, 0);
         };
-        auto a_off = [&](int it) { return (it * RSTEP + trow) * C::LDK + c8 * 8; };
-        auto b_off = [&](int it) { return C::A_ELEMS + (it * RSTEP + trow) * C::LDK + c8 * 8; };
+        auto load_b = [&](int s, int i) {
+            unsigned char* st = ring + C::B_OFF + (s & 1) * C::SLOT;
+            const int ko = (s < nk ? s : nk - 1) * C::BK;
+            __builtin_amdgcn_global_load_lds(
+                (const void __attribute__((address_space(1)))*)(bptr[i] + ko),
+                (void __attribute__((address_space(3)))*)(st + (64 * wave + 8 * i) * C::ROWB), 16, 0, 0);
+        };
 
         floatx16 acc[NT][MT];
 #pragma unroll
@@ -154,106 +202,94 @@ __global__ __launch_bounds__(64 * WAVES_N * WAVES_M) void tiled_kernel(TiledPara
 #pragma unroll
                 for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.0f;
 
-        uint4 ra[C::A_LOADS], rb[C::B_LOADS];
-        auto gload = [&](int kt) {
-            const int ko = kt * C::BK;
-#pragma unroll
-            for (int it = 0; it < C::A_LOADS; ++it) ra[it] = ldg16(a_ptr(it) + ko);
-#pragma unroll
-            for (int it = 0; it < C::B_LOADS; ++it)
-                rb[it] = ldg16(p.act + (int64_t)bsrc[it] * p.K + c8 * 8 + ko);
-        };
-        auto lstore = [&](int buf) {
-            bf16_t* s = lds + buf * C::STAGE_ELEMS;
-#pragma unroll
-            for (int it = 0; it < C::A_LOADS; ++it) *reinterpret_cast<uint4*>(s + a_off(it)) = ra[it];
-#pragma unroll
-            for (int it = 0; it < C::B_LOADS; ++it) *reinterpret_cast<uint4*>(s + b_off(it)) = rb[it];
-        };
-
-        // LDS row of this wave's nt-th 32-row weight tile.  UP: tiles nt < NT/2
-        // are w1 rows, tile nt + NT/2 holds the same rows of w3.
-        auto arow = [&](int nt) {
-            if (UP) {
-                constexpr int H = NT / 2;
-                return (nt < H ? 0 : C::BN / 2) + wn * H * 32 + (nt % H) * 32;
+        bf16x8 fa[2][NT], fb[2][MT];
+        // fragment f (0-3: weight tiles, 4-7: token tiles) of k-step ks of step s
+        auto fread1 = [&](int s, int ks, int slot, int f) {
+            if (f < NT) {
+                const unsigned char* sa = ring + (s % 3) * C::SLOT + a_wave + xk[ks];
+                fa[slot][f] = *reinterpret_cast<const bf16x8*>(sa + atile(f));
+            } else {
+                const unsigned char* sb = ring + C::B_OFF + (s & 1) * C::SLOT + b_wave + xk[ks];
+                fb[slot][f - NT] = *reinterpret_cast<const bf16x8*>(sb + (f - NT) * 32 * C::ROWB);
             }
-            return wn * NT * 32 + nt * 32;
         };
+        auto fence = [] { __builtin_amdgcn_sched_barrier(0); };
 
-        constexpr int KSUB = C::BK / 16;  // MFMA k-steps per LDS stage
-        bf16x8 fa[2][NT], fb[2][MT];      // fragments of two consecutive k-steps
-        auto fread = [&](const bf16_t* s, int ks, bf16x8* a, bf16x8* b) {
-            const int col = ks * 16 + 8 * (lane >> 5);
+        // prologue: A(0), B(0), A(1), as the steady state would have issued
+        // them; A(0) and B(0) complete everywhere
 #pragma unroll
-            for (int nt = 0; nt < NT; ++nt)
-                a[nt] = *reinterpret_cast<const bf16x8*>(s + (arow(nt) + (lane & 31)) * C::LDK + col);
+        for (int i = 0; i < L; ++i) load_a(0, i);
 #pragma unroll
-            for (int mt = 0; mt < MT; ++mt)
-                b[mt] = *reinterpret_cast<const bf16x8*>(
-                    s + C::A_ELEMS + (wm * MT * 32 + mt * 32 + (lane & 31)) * C::LDK + col);
-        };
+        for (int i = 0; i < L; ++i) load_b(0, i);
+#pragma unroll
+        for (int i = 0; i < L; ++i) load_a(1, i);
+        wait_vmem<L>();
+        fence();
+        __builtin_amdgcn_s_barrier();
+        fence();
+#pragma unroll
+        for (int f = 0; f < NT + MT; ++f) fread1(0, 0, 0, f);
 
-        gload(0);
-        lstore(0);
-        __syncthreads();
-        for (int kt = 0; kt < nk; ++kt) {
-            const int buf = kt & 1;
-            const bf16_t* s = lds + buf * C::STAGE_ELEMS;
-            fread(s, 0, fa[0], fb[0]);
-            gload(kt + 1 < nk ? kt + 1 : kt);  // unconditional: keeps the waits exact
+        // step j: k-step ks multiplies fragments slot ks & 1 while the other
+        // slot receives the next k-step's fragments (in k-step 3: k-step 0 of
+        // step j+1).  Loads: B(j+1) in k-step 0, A(j+2) in k-steps 1 and 2.
+        // After k-step 2 every wave waits for its reads of step j's last
+        // fragments and for its loads up to B(j+1), then one barrier makes
+        // A(j+1), B(j+1) complete and frees the slots of A(j), B(j).
+        for (int j = 0; j < nk; ++j) {
 #pragma unroll
-            for (int ks = 0; ks < KSUB; ++ks) {
+            for (int ks = 0; ks < 4; ++ks) {
                 const int cur = ks & 1;
-                // fragments of k-step ks+1 are read while k-step ks multiplies
-                if (ks + 1 < KSUB) fread(s, ks + 1, fa[cur ^ 1], fb[cur ^ 1]);
+                // (in the last step k-step 3 reads step nk's slots, which hold
+                // the redundant re-loads; the values are not used)
+                const int rs = ks < 3 ? j : j + 1, rk = ks < 3 ? ks + 1 : 0;
 #pragma unroll
-                for (int nt = 0; nt < NT; ++nt)
-#pragma unroll
-                    for (int mt = 0; mt < MT; ++mt)
-                        acc[nt][mt] = mfma32x32x16(fa[cur][nt], fb[cur][mt], acc[nt][mt]);
-            }
-            // issue order of this step: fragment reads of k-step 0, the global
-            // loads of step kt+1, then each k-step's MFMAs interleaved one to
-            // one with the next k-step's fragment reads, then the LDS stores
-            __builtin_amdgcn_sched_group_barrier(0x100, NT + MT, 0);
-            __builtin_amdgcn_sched_group_barrier(0x020, C::A_LOADS + C::B_LOADS, 0);
-#pragma unroll
-            for (int ks = 0; ks < KSUB - 1; ++ks) {
-#pragma unroll
-                for (int i = 0; i < NT + MT; ++i) {
-                    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-                    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+                for (int g = 0; g < NT; ++g) {
+                    acc[g][0] = mfma32x32x16(fa[cur][g], fb[cur][0], acc[g][0]);
+                    acc[g][1] = mfma32x32x16(fa[cur][g], fb[cur][1], acc[g][1]);
+                    fence();
+                    fread1(rs, rk, cur ^ 1, 2 * g);
+                    fread1(rs, rk, cur ^ 1, 2 * g + 1);
+                    if (ks == 0) {
+                        load_b(j + 1, 2 * g);
+                        load_b(j + 1, 2 * g + 1);
+                    } else if (ks < 3) {
+                        load_a(j + 2, (ks - 1) * 4 + g);
+                    }
+                    fence();
+                    acc[g][2] = mfma32x32x16(fa[cur][g], fb[cur][2], acc[g][2]);
+                    acc[g][3] = mfma32x32x16(fa[cur][g], fb[cur][3], acc[g][3]);
+                    fence();
                 }
-                __builtin_amdgcn_sched_group_barrier(0x008, NT * MT - (NT + MT), 0);
+                if (ks == 2) {
+                    wait_lds();
+                    wait_vmem<L>();
+                    fence();
+                    __builtin_amdgcn_s_barrier();
+                    fence();
+                }
             }
-            __builtin_amdgcn_sched_group_barrier(0x008, NT * MT, 0);
-            lstore(buf ^ 1);
-            __syncthreads();
         }
 
-        // epilogue: lane holds, per 32x32 tile, columns (tokens) lane%32 and
-        // rows (weight rows) 8q + 4*(lane/32) + i for q, i < 4
+        // epilogue: lane holds, per 32x32 tile, column (token) lane % 32 and
+        // rows (weight rows) 8q + 4 * (lane / 32) + i, q, i < 4
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) {
-            const int mloc = wm * MT * 32 + mt * 32 + (lane & 31);
+            const int mloc = wm * 128 + mt * 32 + (lane & 31);
             if (mloc >= Mp) continue;
             const int64_t rrow = row0 + m0 + mloc;
             if (UP) {
-                constexpr int H = NT / 2;
-                bf16_t* hrow = p.h_out + rrow * p.N + nb * C::NOUT + wn * H * 32 + 4 * (lane >> 5);
+                bf16_t* hrow = p.h_out + rrow * p.N + nb * C::NOUT + wr * 64 + 4 * (lane >> 5);
 #pragma unroll
-                for (int j = 0; j < H; ++j) {
-                    const floatx16& u = acc[j][mt];
-                    const floatx16& v = acc[j + H][mt];
+                for (int h = 0; h < 2; ++h) {
+                    const floatx16& u = acc[h][mt];
+                    const floatx16& v = acc[h + 2][mt];
 #pragma unroll
                     for (int q = 0; q < 4; ++q) {
                         uint2 pk;
-                        pk.x = pack_bf16x2(silu(u[4 * q + 0]) * v[4 * q + 0],
-                                           silu(u[4 * q + 1]) * v[4 * q + 1]);
-                        pk.y = pack_bf16x2(silu(u[4 * q + 2]) * v[4 * q + 2],
-                                           silu(u[4 * q + 3]) * v[4 * q + 3]);
-                        *reinterpret_cast<uint2*>(hrow + j * 32 + 8 * q) = pk;
+                        pk.x = pack_bf16x2(silu(u[4 * q + 0]) * v[4 * q + 0], silu(u[4 * q + 1]) * v[4 * q + 1]);
+                        pk.y = pack_bf16x2(silu(u[4 * q + 2]) * v[4 * q + 2], silu(u[4 * q + 3]) * v[4 * q + 3]);
+                        *reinterpret_cast<uint2*>(hrow + h * 32 + 8 * q) = pk;
                     }
                 }
             } else {
@@ -263,7 +299,7 @@ __global__ __launch_bounds__(64 * WAVES_N * WAVES_M) void tiled_kernel(TiledPara
                     orow = p.perm[rrow];
                     gw = p.topk_w[orow];
                 }
-                float* yrow = p.y_out + orow * p.N + nb * C::NOUT + wn * NT * 32 + 4 * (lane >> 5);
+                float* yrow = p.y_out + orow * p.N + nb * C::NOUT + wr * 128 + 4 * (lane >> 5);
 #pragma unroll
                 for (int nt = 0; nt < NT; ++nt) {
 #pragma unroll
@@ -278,7 +314,31 @@ __global__ __launch_bounds__(64 * WAVES_N * WAVES_M) void tiled_kernel(TiledPara
                 }
             }
         }
+        // the next tile's loads reuse the rings: redundant tail loads and this
+        // tile's stores must be done, and every wave past its last read
+        wait_vmem<0>();
+        __syncthreads();
     }
+}
+
+template <bool UP>
+hipError_t run_q(const TiledParams& p, int64_t A, hipStream_t stream)
+{
+    using C = QCfg<UP>;
+    static bool attr_set = false;
+    if (!attr_set) {
+        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&q_kernel<UP>),
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS_BYTES);
+        if (e != hipSuccess) return e;
+        attr_set = true;
+    }
+    const int64_t nbn = p.N / C::NOUT;
+    const int64_t items = nbn * (A / C::BM + p.E);
+    int64_t grid = cu_count();
+    if (grid > items) grid = items;
+    grid = ((grid + 7) / 8) * 8;
+    q_kernel<UP><<<static_cast<unsigned>(grid), C::THREADS, C::LDS_BYTES, stream>>>(p);
+    return hipGetLastError();
 }
 
 int cu_count()
@@ -295,41 +355,12 @@ int cu_count()
     return cached[dev];
 }
 
-template <bool UP, int WAVES_N, int WAVES_M, int NT, int MT>
-hipError_t run_tiled(const TiledParams& p, int64_t A, hipStream_t stream)
-{
-    using C = TiledCfg<UP, WAVES_N, WAVES_M, NT, MT>;
-    static bool attr_set = false;
-    if (!attr_set) {
-        hipError_t e = hipFuncSetAttribute(
-            reinterpret_cast<const void*>(&tiled_kernel<UP, WAVES_N, WAVES_M, NT, MT>),
-            hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS_BYTES);
-        if (e != hipSuccess) return e;
-        attr_set = true;
-    }
-    // items are at most nbn * (A/BM + E); never more workgroups than items
-    const int64_t nbn = p.N / C::NOUT;
-    const int64_t items = nbn * (A / C::BM + p.E);
-    int64_t grid = cu_count();
-    if (grid > items) grid = items;
-    grid = ((grid + 7) / 8) * 8;
-    tiled_kernel<UP, WAVES_N, WAVES_M, NT, MT>
-        <<<static_cast<unsigned>(grid), C::THREADS, C::LDS_BYTES, stream>>>(p);
-    return hipGetLastError();
-}
-
-#define MOE_TILED_UP_CFG 4, 2, 2, 4
-#define MOE_TILED_DOWN_CFG 4, 2, 2, 4
-// UP: 8 waves as 4 (weight rows) x 2 (tokens); 128 w1 + 128 w3 rows x 256 tokens
-using UpTile = TiledCfg<true, MOE_TILED_UP_CFG>;
-// DOWN: 8 waves as 4 x 2; 256 w2 rows x 256 tokens
-using DownTile = TiledCfg<false, MOE_TILED_DOWN_CFG>;
-
 }  // namespace
 
 bool tiled_supported(int d, int ffn)
 {
-    return ffn % UpTile::NOUT == 0 && d % DownTile::NOUT == 0 && d % 64 == 0 && ffn % 64 == 0;
+    return ffn % QCfg<true>::NOUT == 0 && d % QCfg<false>::NOUT == 0 && d % QCfg<true>::BK == 0 &&
+           ffn % QCfg<false>::BK == 0;
 }
 
 hipError_t launch_tiled_up(const UpArgs& a, hipStream_t stream)
@@ -345,7 +376,7 @@ hipError_t launch_tiled_up(const UpArgs& a, hipStream_t stream)
     p.K = a.d;
     p.E = a.E;
     p.h_out = a.h;
-    return run_tiled<true, MOE_TILED_UP_CFG>(p, a.A, stream);
+    return run_q<true>(p, a.A, stream);
 }
 
 hipError_t launch_tiled_down(const DownArgs& a, hipStream_t stream)
@@ -360,7 +391,7 @@ hipError_t launch_tiled_down(const DownArgs& a, hipStream_t stream)
     p.y_out = a.y;
     p.topk_w = a.topk_w;
     p.perm = a.perm;
-    return run_tiled<false, MOE_TILED_DOWN_CFG>(p, a.A, stream);
+    return run_q<false>(p, a.A, stream);
 }
 
 }  // namespace moe
