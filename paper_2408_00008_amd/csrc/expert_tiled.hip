@@ -43,26 +43,29 @@ int cu_count();
 
 // ---- four-wave schedule ------------------------------------------------------
 //
-// The same 256 x 256 output tile per workgroup, computed by 4 waves, one per
-// SIMD, each owning a 128 x 128 quarter (16 accumulator tiles of 32 x 32,
-// 256 accumulator registers per lane).  Measured on MI355X: a wave that
-// interleaves about one 1 KB global->LDS load with four 32x32x16 MFMAs keeps
-// the MFMA pipe ~85% busy and sustains the 256 x 256 tile's load rate, while
-// loads issued by a second wave on a SIMD whose MFMAs run back to back are
-// throttled to about one per 32 cycles per CU.  So every wave carries its
-// own loads, fragment reads and MFMAs in one interleaved stream.
+// Each tile is computed by 4 waves, one per SIMD, each owning a 128 x 128
+// quarter (16 accumulator tiles of 32 x 32, 256 accumulator registers per
+// lane).  Measured on MI355X: a wave that interleaves about one 1 KB
+// global->LDS load with four 32x32x16 MFMAs keeps the MFMA pipe ~85% busy
+// and sustains the 256 x 256 tile's load rate, while loads issued by a second
+// wave on a SIMD whose MFMAs run back to back are throttled to about one per
+// 32 cycles per CU.  So every wave carries its own loads, fragment reads and
+// MFMAs in one interleaved instruction stream (its order pinned with
+// scheduling barriers).
 //
 //   * operands go from global memory straight into LDS (16-byte loads that
 //     write LDS at base + 16 * lane, no registers); a step holds BK = 64
 //     reduction elements, so one load covers 8 rows x 128 bytes (whole cache
 //     lines; half-line rows measured 1.7x slower to issue);
 //   * the weight tile A (256 rows) lives in a ring of 3 slots, the token tile
-//     B (256 rows) in a ring of 2: 96 + 64 KB, all of the LDS.  During step j
-//     every wave issues its share of B(j+1) while it multiplies k-steps 0-1
-//     and of A(j+2) during k-steps 2-3; both slots were last read in step
-//     j-1.  At the end of step j it waits until only A(j+2) is outstanding
-//     (loads retire in order), then one barrier publishes step j+1;
-//   * fragments of k-step ks+1 are read while k-step ks multiplies;
+//     B (256 rows) in a ring of 2: 96 + 64 KB, all of the LDS;
+//   * step j multiplies its 4 k-steps of 16; while k-step ks multiplies, the
+//     fragments of k-step ks+1 are read (in k-step 3: k-step 0 of step j+1),
+//     and the wave issues its share of B(j+1) in k-step 0 and of A(j+2) in
+//     k-steps 1-2.  After k-step 2 every wave waits for its fragment reads of
+//     step j and for its loads up to B(j+1) (loads retire in order), then one
+//     barrier makes A(j+1) and B(j+1) complete for all waves and frees the
+//     slots of A(j) and B(j) for the next step's loads;
 //   * LDS rows are 128 bytes, unpadded; the eight 16-byte chunks of row r are
 //     stored at slot chunk ^ ((r >> 1) & 7), so every fragment read (16
 //     consecutive rows, one chunk) hits 16 distinct bank groups;
