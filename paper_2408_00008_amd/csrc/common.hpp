@@ -16,18 +16,20 @@ __device__ __forceinline__ float bf16_to_f32(bf16_t b)
     return __uint_as_float(static_cast<uint32_t>(b) << 16);
 }
 
-// float -> bfloat16 with round-to-nearest-even (NaN kept quiet).
+// float -> bfloat16, round to nearest even (gfx950's v_cvt_pk_bf16_f32; NaN
+// stays NaN).
 __device__ __forceinline__ bf16_t f32_to_bf16(float f)
 {
-    uint32_t u = __float_as_uint(f);
-    if ((u & 0x7fffffffu) > 0x7f800000u) return static_cast<bf16_t>((u >> 16) | 0x40u);
-    u += 0x7fffu + ((u >> 16) & 1u);
-    return static_cast<bf16_t>(u >> 16);
+    return __builtin_bit_cast(bf16_t, static_cast<__bf16>(f));
 }
 
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi)
 {
-    return static_cast<uint32_t>(f32_to_bf16(lo)) | (static_cast<uint32_t>(f32_to_bf16(hi)) << 16);
+    typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+    bf16x2_t v;
+    v[0] = static_cast<__bf16>(lo);
+    v[1] = static_cast<__bf16>(hi);
+    return __builtin_bit_cast(uint32_t, v);
 }
 
 // silu(z) = z / (1 + exp(-z)) with the hardware exp2 and reciprocal (a few

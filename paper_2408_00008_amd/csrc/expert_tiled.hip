@@ -275,16 +275,22 @@ __global__ __launch_bounds__(256) void q_kernel(TiledParams p)
         }
 
         // epilogue: lane holds, per 32x32 tile, column (token) lane % 32 and
-        // rows (weight rows) 8q + 4 * (lane / 32) + i, q, i < 4
+        // rows (weight rows) 8q + 4 * (lane / 32) + i, q, i < 4.  Straight-line
+        // code, one output tile at a time: any branch here makes the compiler
+        // copy all accumulators out of their registers at once.  Token columns
+        // past the expert's rows were loaded from its last row, so they hold
+        // exactly that row's results and store the same bits to the same place.
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) {
             const int mloc = wm * 128 + mt * 32 + (lane & 31);
-            if (mloc >= Mp) continue;
-            const int64_t rrow = row0 + m0 + mloc;
+            const int64_t rrow = row0 + m0 + (mloc < Mp ? mloc : Mp - 1);
             if (UP) {
                 bf16_t* hrow = p.h_out + rrow * p.N + nb * C::NOUT + wr * 64 + 4 * (lane >> 5);
 #pragma unroll
                 for (int h = 0; h < 2; ++h) {
+                    // the accumulators are redefined here (in their AGPRs), so
+                    // their copies into VGPRs cannot move above this point
+                    asm volatile("" : "+a"(acc[h][mt]), "+a"(acc[h + 2][mt]));
                     const floatx16& u = acc[h][mt];
                     const floatx16& v = acc[h + 2][mt];
 #pragma unroll
@@ -294,6 +300,7 @@ __global__ __launch_bounds__(256) void q_kernel(TiledParams p)
                         pk.y = pack_bf16x2(silu(u[4 * q + 2]) * v[4 * q + 2], silu(u[4 * q + 3]) * v[4 * q + 3]);
                         *reinterpret_cast<uint2*>(hrow + h * 32 + 8 * q) = pk;
                     }
+                    __builtin_amdgcn_sched_barrier(0);
                 }
             } else {
                 int64_t orow = rrow;
@@ -305,6 +312,7 @@ __global__ __launch_bounds__(256) void q_kernel(TiledParams p)
                 float* yrow = p.y_out + orow * p.N + nb * C::NOUT + wr * 128 + 4 * (lane >> 5);
 #pragma unroll
                 for (int nt = 0; nt < NT; ++nt) {
+                    asm volatile("" : "+a"(acc[nt][mt]));
 #pragma unroll
                     for (int q = 0; q < 4; ++q) {
                         float4 v;
@@ -314,6 +322,7 @@ __global__ __launch_bounds__(256) void q_kernel(TiledParams p)
                         v.w = gw * acc[nt][mt][4 * q + 3];
                         *reinterpret_cast<float4*>(yrow + nt * 32 + 8 * q) = v;
                     }
+                    __builtin_amdgcn_sched_barrier(0);
                 }
             }
         }
