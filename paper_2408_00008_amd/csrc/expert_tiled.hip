@@ -18,6 +18,8 @@
 //     work on the token tiles of a few weight blocks at a time and share both
 //     operands through that XCD's L2.  Per-expert tile counts are read from
 //     the device-side offsets: ragged row counts need no host synchronisation.
+#include <type_traits>
+
 #include "common.hpp"
 #include "launch.hpp"
 
@@ -197,135 +199,154 @@ __global__ __launch_bounds__(256) void q_kernel(TiledParams p)
                 (void __attribute__((address_space(3)))*)(st + (64 * wave + 8 * i) * C::ROWB), 16, 0, 0);
         };
 
-        floatx16 acc[NT][MT];
-#pragma unroll
-        for (int i = 0; i < NT; ++i)
-#pragma unroll
-            for (int j = 0; j < MT; ++j)
-#pragma unroll
-                for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.0f;
+        // The tile body for NMT multiplied 32-token column blocks per wave
+        // (4: full tile).  An expert's last token tile often holds only a few
+        // rows; with NMT = 1 or 2 (at most 32 or 64 rows, all in the first
+        // token half) it skips the MFMAs and fragment reads of the other
+        // column blocks, which hold no rows.  Only computed blocks are stored;
+        // columns past the rows hold copies of the last row (see epilogue).
+        auto tile = [&](auto nmt_tag) {
+            constexpr int NMT = decltype(nmt_tag)::value;
+            floatx16 acc[NT][NMT];
+    #pragma unroll
+            for (int i = 0; i < NT; ++i)
+    #pragma unroll
+                for (int j = 0; j < NMT; ++j)
+    #pragma unroll
+                    for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.0f;
 
-        bf16x8 fa[2][NT], fb[2][MT];
-        // fragment f (0-3: weight tiles, 4-7: token tiles) of k-step ks of step s
-        auto fread1 = [&](int s, int ks, int slot, int f) {
-            if (f < NT) {
-                const unsigned char* sa = ring + (s % 3) * C::SLOT + a_wave + xk[ks];
-                fa[slot][f] = *reinterpret_cast<const bf16x8*>(sa + atile(f));
-            } else {
-                const unsigned char* sb = ring + C::B_OFF + (s & 1) * C::SLOT + b_wave + xk[ks];
-                fb[slot][f - NT] = *reinterpret_cast<const bf16x8*>(sb + (f - NT) * 32 * C::ROWB);
+            bf16x8 fa[2][NT], fb[2][NMT];
+            // fragment f (0-3: weight tiles, 4-7: token tiles) of k-step ks of step s
+            auto fread1 = [&](int s, int ks, int slot, int f) {
+                if (f >= NT + NMT) return;  // token tile not multiplied in this variant
+                if (f < NT) {
+                    const unsigned char* sa = ring + (s % 3) * C::SLOT + a_wave + xk[ks];
+                    fa[slot][f] = *reinterpret_cast<const bf16x8*>(sa + atile(f));
+                } else {
+                    const unsigned char* sb = ring + C::B_OFF + (s & 1) * C::SLOT + b_wave + xk[ks];
+                    fb[slot][f - NT] = *reinterpret_cast<const bf16x8*>(sb + (f - NT) * 32 * C::ROWB);
+                }
+            };
+            auto fence = [] { __builtin_amdgcn_sched_barrier(0); };
+
+            // prologue: A(0), B(0), A(1), as the steady state would have issued
+            // them; A(0) and B(0) complete everywhere
+    #pragma unroll
+            for (int i = 0; i < L; ++i) load_a(0, i);
+    #pragma unroll
+            for (int i = 0; i < L; ++i) load_b(0, i);
+    #pragma unroll
+            for (int i = 0; i < L; ++i) load_a(1, i);
+            wait_vmem<L>();
+            fence();
+            __builtin_amdgcn_s_barrier();
+            fence();
+    #pragma unroll
+            for (int f = 0; f < NT + NMT; ++f) fread1(0, 0, 0, f);
+
+            // step j: k-step ks multiplies fragments slot ks & 1 while the other
+            // slot receives the next k-step's fragments (in k-step 3: k-step 0 of
+            // step j+1).  Loads: B(j+1) in k-step 0, A(j+2) in k-steps 1 and 2.
+            // After k-step 2 every wave waits for its reads of step j's last
+            // fragments and for its loads up to B(j+1), then one barrier makes
+            // A(j+1), B(j+1) complete and frees the slots of A(j), B(j).
+            for (int j = 0; j < nk; ++j) {
+    #pragma unroll
+                for (int ks = 0; ks < 4; ++ks) {
+                    const int cur = ks & 1;
+                    // (in the last step k-step 3 reads step nk's slots, which hold
+                    // the redundant re-loads; the values are not used)
+                    const int rs = ks < 3 ? j : j + 1, rk = ks < 3 ? ks + 1 : 0;
+    #pragma unroll
+                    for (int g = 0; g < NT; ++g) {
+                        acc[g][0] = mfma32x32x16(fa[cur][g], fb[cur][0], acc[g][0]);
+                        if constexpr (NMT > 1) acc[g][1] = mfma32x32x16(fa[cur][g], fb[cur][1], acc[g][1]);
+                        fence();
+                        fread1(rs, rk, cur ^ 1, 2 * g);
+                        fread1(rs, rk, cur ^ 1, 2 * g + 1);
+                        if (ks == 0) {
+                            load_b(j + 1, 2 * g);
+                            load_b(j + 1, 2 * g + 1);
+                        } else if (ks < 3) {
+                            load_a(j + 2, (ks - 1) * 4 + g);
+                        }
+                        fence();
+                        if constexpr (NMT > 2) {
+                            acc[g][2] = mfma32x32x16(fa[cur][g], fb[cur][2], acc[g][2]);
+                            acc[g][3] = mfma32x32x16(fa[cur][g], fb[cur][3], acc[g][3]);
+                        }
+                        fence();
+                    }
+                    if (ks == 2) {
+                        wait_lds();
+                        wait_vmem<L>();
+                        fence();
+                        __builtin_amdgcn_s_barrier();
+                        fence();
+                    }
+                }
+            }
+
+            // epilogue: lane holds, per 32x32 tile, column (token) lane % 32 and
+            // rows (weight rows) 8q + 4 * (lane / 32) + i, q, i < 4.  Straight-line
+            // code, one output tile at a time: any branch here makes the compiler
+            // copy all accumulators out of their registers at once.  Token columns
+            // past the expert's rows were loaded from its last row, so they hold
+            // exactly that row's results and store the same bits to the same place.
+    #pragma unroll
+            for (int mt = 0; mt < NMT; ++mt) {
+                const int mloc = wm * 128 + mt * 32 + (lane & 31);
+                const int64_t rrow = row0 + m0 + (mloc < Mp ? mloc : Mp - 1);
+                if (UP) {
+                    bf16_t* hrow = p.h_out + rrow * p.N + nb * C::NOUT + wr * 64 + 4 * (lane >> 5);
+    #pragma unroll
+                    for (int h = 0; h < 2; ++h) {
+                        // the accumulators are redefined here (in their AGPRs), so
+                        // their copies into VGPRs cannot move above this point
+                        asm volatile("" : "+a"(acc[h][mt]), "+a"(acc[h + 2][mt]));
+                        const floatx16& u = acc[h][mt];
+                        const floatx16& v = acc[h + 2][mt];
+    #pragma unroll
+                        for (int q = 0; q < 4; ++q) {
+                            uint2 pk;
+                            pk.x = pack_bf16x2(silu(u[4 * q + 0]) * v[4 * q + 0], silu(u[4 * q + 1]) * v[4 * q + 1]);
+                            pk.y = pack_bf16x2(silu(u[4 * q + 2]) * v[4 * q + 2], silu(u[4 * q + 3]) * v[4 * q + 3]);
+                            *reinterpret_cast<uint2*>(hrow + h * 32 + 8 * q) = pk;
+                        }
+                        __builtin_amdgcn_sched_barrier(0);
+                    }
+                } else {
+                    int64_t orow = rrow;
+                    float gw = 1.0f;
+                    if (p.topk_w && p.perm) {
+                        orow = p.perm[rrow];
+                        gw = p.topk_w[orow];
+                    }
+                    float* yrow = p.y_out + orow * p.N + nb * C::NOUT + wr * 128 + 4 * (lane >> 5);
+    #pragma unroll
+                    for (int nt = 0; nt < NT; ++nt) {
+                        asm volatile("" : "+a"(acc[nt][mt]));
+    #pragma unroll
+                        for (int q = 0; q < 4; ++q) {
+                            float4 v;
+                            v.x = gw * acc[nt][mt][4 * q + 0];
+                            v.y = gw * acc[nt][mt][4 * q + 1];
+                            v.z = gw * acc[nt][mt][4 * q + 2];
+                            v.w = gw * acc[nt][mt][4 * q + 3];
+                            *reinterpret_cast<float4*>(yrow + nt * 32 + 8 * q) = v;
+                        }
+                        __builtin_amdgcn_sched_barrier(0);
+                    }
+                }
             }
         };
-        auto fence = [] { __builtin_amdgcn_sched_barrier(0); };
+        if (Mp <= 32)
+            tile(std::integral_constant<int, 1>{});
+        else if (Mp <= 64)
+            tile(std::integral_constant<int, 2>{});
+        else
+            tile(std::integral_constant<int, MT>{});
 
-        // prologue: A(0), B(0), A(1), as the steady state would have issued
-        // them; A(0) and B(0) complete everywhere
-#pragma unroll
-        for (int i = 0; i < L; ++i) load_a(0, i);
-#pragma unroll
-        for (int i = 0; i < L; ++i) load_b(0, i);
-#pragma unroll
-        for (int i = 0; i < L; ++i) load_a(1, i);
-        wait_vmem<L>();
-        fence();
-        __builtin_amdgcn_s_barrier();
-        fence();
-#pragma unroll
-        for (int f = 0; f < NT + MT; ++f) fread1(0, 0, 0, f);
-
-        // step j: k-step ks multiplies fragments slot ks & 1 while the other
-        // slot receives the next k-step's fragments (in k-step 3: k-step 0 of
-        // step j+1).  Loads: B(j+1) in k-step 0, A(j+2) in k-steps 1 and 2.
-        // After k-step 2 every wave waits for its reads of step j's last
-        // fragments and for its loads up to B(j+1), then one barrier makes
-        // A(j+1), B(j+1) complete and frees the slots of A(j), B(j).
-        for (int j = 0; j < nk; ++j) {
-#pragma unroll
-            for (int ks = 0; ks < 4; ++ks) {
-                const int cur = ks & 1;
-                // (in the last step k-step 3 reads step nk's slots, which hold
-                // the redundant re-loads; the values are not used)
-                const int rs = ks < 3 ? j : j + 1, rk = ks < 3 ? ks + 1 : 0;
-#pragma unroll
-                for (int g = 0; g < NT; ++g) {
-                    acc[g][0] = mfma32x32x16(fa[cur][g], fb[cur][0], acc[g][0]);
-                    acc[g][1] = mfma32x32x16(fa[cur][g], fb[cur][1], acc[g][1]);
-                    fence();
-                    fread1(rs, rk, cur ^ 1, 2 * g);
-                    fread1(rs, rk, cur ^ 1, 2 * g + 1);
-                    if (ks == 0) {
-                        load_b(j + 1, 2 * g);
-                        load_b(j + 1, 2 * g + 1);
-                    } else if (ks < 3) {
-                        load_a(j + 2, (ks - 1) * 4 + g);
-                    }
-                    fence();
-                    acc[g][2] = mfma32x32x16(fa[cur][g], fb[cur][2], acc[g][2]);
-                    acc[g][3] = mfma32x32x16(fa[cur][g], fb[cur][3], acc[g][3]);
-                    fence();
-                }
-                if (ks == 2) {
-                    wait_lds();
-                    wait_vmem<L>();
-                    fence();
-                    __builtin_amdgcn_s_barrier();
-                    fence();
-                }
-            }
-        }
-
-        // epilogue: lane holds, per 32x32 tile, column (token) lane % 32 and
-        // rows (weight rows) 8q + 4 * (lane / 32) + i, q, i < 4.  Straight-line
-        // code, one output tile at a time: any branch here makes the compiler
-        // copy all accumulators out of their registers at once.  Token columns
-        // past the expert's rows were loaded from its last row, so they hold
-        // exactly that row's results and store the same bits to the same place.
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt) {
-            const int mloc = wm * 128 + mt * 32 + (lane & 31);
-            const int64_t rrow = row0 + m0 + (mloc < Mp ? mloc : Mp - 1);
-            if (UP) {
-                bf16_t* hrow = p.h_out + rrow * p.N + nb * C::NOUT + wr * 64 + 4 * (lane >> 5);
-#pragma unroll
-                for (int h = 0; h < 2; ++h) {
-                    // the accumulators are redefined here (in their AGPRs), so
-                    // their copies into VGPRs cannot move above this point
-                    asm volatile("" : "+a"(acc[h][mt]), "+a"(acc[h + 2][mt]));
-                    const floatx16& u = acc[h][mt];
-                    const floatx16& v = acc[h + 2][mt];
-#pragma unroll
-                    for (int q = 0; q < 4; ++q) {
-                        uint2 pk;
-                        pk.x = pack_bf16x2(silu(u[4 * q + 0]) * v[4 * q + 0], silu(u[4 * q + 1]) * v[4 * q + 1]);
-                        pk.y = pack_bf16x2(silu(u[4 * q + 2]) * v[4 * q + 2], silu(u[4 * q + 3]) * v[4 * q + 3]);
-                        *reinterpret_cast<uint2*>(hrow + h * 32 + 8 * q) = pk;
-                    }
-                    __builtin_amdgcn_sched_barrier(0);
-                }
-            } else {
-                int64_t orow = rrow;
-                float gw = 1.0f;
-                if (p.topk_w && p.perm) {
-                    orow = p.perm[rrow];
-                    gw = p.topk_w[orow];
-                }
-                float* yrow = p.y_out + orow * p.N + nb * C::NOUT + wr * 128 + 4 * (lane >> 5);
-#pragma unroll
-                for (int nt = 0; nt < NT; ++nt) {
-                    asm volatile("" : "+a"(acc[nt][mt]));
-#pragma unroll
-                    for (int q = 0; q < 4; ++q) {
-                        float4 v;
-                        v.x = gw * acc[nt][mt][4 * q + 0];
-                        v.y = gw * acc[nt][mt][4 * q + 1];
-                        v.z = gw * acc[nt][mt][4 * q + 2];
-                        v.w = gw * acc[nt][mt][4 * q + 3];
-                        *reinterpret_cast<float4*>(yrow + nt * 32 + 8 * q) = v;
-                    }
-                    __builtin_amdgcn_sched_barrier(0);
-                }
-            }
-        }
         // the next tile's loads reuse the rings: redundant tail loads and this
         // tile's stores must be done, and every wave past its last read
         wait_vmem<0>();

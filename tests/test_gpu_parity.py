@@ -174,6 +174,7 @@ def test_forward_sampled(name, variant):
     (700, 256, 256, 4, 2),    # several ragged 256-row token tiles per expert
     (1000, 512, 384, 8, 2),   # odd count of 128-column output blocks
     (96, 256, 128, 64, 8),    # E = 64 with 1..20 rows per expert
+    (200, 256, 256, 8, 2),    # 33..64 rows per expert (partial tiles of every width)
 ])
 @pytest.mark.parametrize("variant", [1, 2])
 def test_forward_shapes(shape, variant):
