@@ -370,14 +370,14 @@ hipError_t run(StreamParams p, int64_t rows_max, hipStream_t stream)
 }  // namespace
 
 // Tile shape by the mean rows per expert (A/E), from sweeps on MI355X at the
-// Mixtral shapes: 32-row passes while the mean is small, 64-row passes above;
-// an expert with more rows than one pass holds is cut into several passes,
-// which run as separate workgroups.  The chunk length KC trades bytes in
-// flight against registers.
+// Mixtral shapes: 32-row passes while the mean is small, 64-row passes above
+// (128-row passes for the up GEMM above a mean of 48); an expert with more
+// rows than one pass holds is cut into several passes, which run as separate
+// workgroups.  The chunk length KC trades bytes in flight against registers.
 int stream_groups(int64_t A, int E)
 {
     const int64_t mean = (A + E - 1) / E;
-    return mean <= 24 ? 2 : 4;
+    return mean <= 24 ? 2 : (mean <= 48 ? 4 : 8);
 }
 
 hipError_t launch_stream_up(const UpArgs& a, int64_t rows_max, hipStream_t stream)
@@ -399,6 +399,7 @@ hipError_t launch_stream_up(const UpArgs& a, int64_t rows_max, hipStream_t strea
         if (a.d % 128 == 0) return run<true, 8, 1, 2, 128, true>(p, rows_max, stream);
         return run<true, 8, 1, 2, 64, true>(p, rows_max, stream);
     }
+    if (stream_groups(a.A, a.E) == 8) return run<true, 8, 1, 8, 64, true>(p, rows_max, stream);
     if (a.d % 128 == 0) return run<true, 8, 1, 4, 128, true>(p, rows_max, stream);
     return run<true, 8, 1, 4, 64, true>(p, rows_max, stream);
 }
