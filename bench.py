@@ -132,17 +132,19 @@ def main():
 
     evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
            for _ in range(args.steps)]
-    t_start = torch.cuda.Event(enable_timing=True)
-    t_end = torch.cuda.Event(enable_timing=True)
+    # one event at every step boundary: the first and last bracket the timed
+    # region, the ones between give the per-step spread
+    bounds = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     torch.cuda.synchronize()
     wall0 = time.perf_counter()
-    t_start.record(stream)
+    bounds[0].record(stream)
     for i in range(args.steps):
         step(*evs[i])
-    t_end.record(stream)
+        bounds[i + 1].record(stream)
     torch.cuda.synchronize()
     wall1 = time.perf_counter()
-    ms_total = t_start.elapsed_time(t_end)
+    ms_total = bounds[0].elapsed_time(bounds[-1])
+    step_ms = np.array([bounds[i].elapsed_time(bounds[i + 1]) for i in range(args.steps)])
     ms_per_step = ms_total / args.steps
     up_ms = sorted(e0.elapsed_time(e1) for e0, e1 in evs)
     up_avg_ms = sum(up_ms) / len(up_ms)
@@ -185,6 +187,7 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": round(ms_per_step, 4),
+        "step_ms_p10_p50_p90": [round(float(np.percentile(step_ms, q)), 4) for q in (10, 50, 90)],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,

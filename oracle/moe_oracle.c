@@ -33,6 +33,15 @@
  * Weight layout (row-major, reduction index contiguous):
  *   x [T,d], Wr [E,d], W1 [E,ffn,d], W3 [E,ffn,d], W2 [E,d,ffn], b [E] float.
  *
+ * 8-bit expert weights.  The paper's engine section (Sec. 4.1, "Model
+ * Quantization") stores weights as 8-bit floats, and its parallelism
+ * experiment (Sec. 5) serves an 8-bit quantized Mixtral-8x7B.  The format read
+ * here is OCP FP8 E4M3 with one float scale per weight row (output channel):
+ *   W[e,n,i] = E4M3(q[e,n,i]) * s[e,n]
+ * where E4M3(b) has sign bit 7, exponent bits 6..3 (bias 7) and mantissa bits
+ * 2..0; exponent 0 is subnormal (m/8 * 2^-6); exponent 15 with mantissa 7 is
+ * NaN; there is no infinity (largest finite 448).  The router stays bf16.
+ *
  * Pins: tests compare this file against a pure-Python brute force on tiny
  * shapes (subset enumeration for top-k, dense all-expert evaluation), against
  * torch fp64 dense SwiGLU for E=1,k=1 and against a dense softmax mixture for
@@ -56,6 +65,52 @@ static double widen(uint16_t b)
     float f;
     memcpy(&f, &u, sizeof f);
     return (double)f;
+}
+
+/* OCP FP8 E4M3 byte -> double (exact); NaN for S.1111.111. */
+static double fp8_e4m3(uint8_t b)
+{
+    const int sign = b >> 7, e = (b >> 3) & 15, m = b & 7;
+    double v;
+    if (e == 15 && m == 7)
+        v = NAN;
+    else if (e == 0)
+        v = ldexp((double)m / 8.0, -6);
+    else
+        v = ldexp(1.0 + (double)m / 8.0, e - 7);
+    return sign ? -v : v;
+}
+
+/* An expert weight tensor [E, rows, cols]: bf16 bits, or E4M3 bytes with one
+ * float scale per row. */
+typedef struct {
+    const uint16_t* bf16;
+    const uint8_t* q;
+    const float* s;
+} wmat_t;
+
+/* Row r (counted over all experts) of a weight tensor, widened to double.
+ * Returns 0 if any value is not finite. */
+static int widen_row(wmat_t w, int64_t r, int64_t cols, double* out)
+{
+    int ok = 1;
+    if (w.bf16) {
+        for (int64_t i = 0; i < cols; ++i) out[i] = widen(w.bf16[r * cols + i]);
+    } else {
+        const double s = (double)w.s[r];
+        for (int64_t i = 0; i < cols; ++i) out[i] = fp8_e4m3(w.q[r * cols + i]) * s;
+    }
+    for (int64_t i = 0; i < cols; ++i)
+        if (!isfinite(out[i])) ok = 0;
+    return ok;
+}
+
+/* Decodes n E4M3 bytes (for the tests' pins of the format). */
+int oracle_fp8_e4m3(const uint8_t* q, int64_t n, double* out)
+{
+    if (n < 0) return ORACLE_BAD_ARG;
+    for (int64_t i = 0; i < n; ++i) out[i] = fp8_e4m3(q[i]);
+    return ORACLE_OK;
 }
 
 int oracle_threads(int n)
@@ -189,9 +244,8 @@ static double silu(double z) { return z / (1.0 + exp(-z)); }
  * ascending j.  Optional diagnostics (NULL to skip):
  *   h_slots [T*k, ffn]: silu(W1 x) * (W3 x) of assignment a = t*k+j
  *   y_slots [T*k, d]  : W2 h of assignment a (not gate-weighted) */
-int oracle_moe_apply(const uint16_t* x, const uint16_t* w1, const uint16_t* w3,
-                     const uint16_t* w2, const int32_t* ids, const double* gates,
-                     int64_t T, int64_t d, int64_t ffn, int E, int k,
+static int moe_apply(const uint16_t* x, wmat_t w1, wmat_t w3, wmat_t w2, const int32_t* ids,
+                     const double* gates, int64_t T, int64_t d, int64_t ffn, int E, int k,
                      double* out, double* h_slots, double* y_slots)
 {
     if (T < 0 || d <= 0 || ffn <= 0 || E <= 0 || k <= 0 || k > E) return ORACLE_BAD_ARG;
@@ -209,6 +263,7 @@ int oracle_moe_apply(const uint16_t* x, const uint16_t* w1, const uint16_t* w3,
         return ORACLE_NO_MEMORY;
     }
     for (int64_t i = 0; i < T * d; ++i) xd[i] = widen(x[i]);
+    int bad = 0;  /* a weight row used below holds a non-finite value */
 
     for (int e = 0; e < E; ++e) {
         /* the assignments routed to expert e, ascending */
@@ -216,9 +271,6 @@ int oracle_moe_apply(const uint16_t* x, const uint16_t* w1, const uint16_t* w3,
         for (int64_t a = 0; a < A; ++a)
             if (ids[a] == e) rows[n_rows++] = a;
         if (n_rows == 0) continue;
-        const uint16_t* W1 = w1 + (int64_t)e * ffn * d;
-        const uint16_t* W3 = w3 + (int64_t)e * ffn * d;
-        const uint16_t* W2 = w2 + (int64_t)e * d * ffn;
 
         /* h[a,n] = silu(sum_i W1[n,i] x[t,i]) * (sum_i W3[n,i] x[t,i]) */
 #pragma omp parallel
@@ -227,9 +279,10 @@ int oracle_moe_apply(const uint16_t* x, const uint16_t* w1, const uint16_t* w3,
             double* r3 = (double*)malloc(sizeof(double) * (size_t)d);
 #pragma omp for schedule(static)
             for (int64_t n = 0; n < ffn; ++n) {
-                for (int64_t i = 0; i < d; ++i) {
-                    r1[i] = widen(W1[n * d + i]);
-                    r3[i] = widen(W3[n * d + i]);
+                if (!widen_row(w1, (int64_t)e * ffn + n, d, r1) |
+                    !widen_row(w3, (int64_t)e * ffn + n, d, r3)) {
+#pragma omp atomic write
+                    bad = 1;
                 }
                 for (int64_t q = 0; q < n_rows; ++q) {
                     const double* xt = xd + (rows[q] / k) * d;
@@ -251,7 +304,10 @@ int oracle_moe_apply(const uint16_t* x, const uint16_t* w1, const uint16_t* w3,
             double* r2 = (double*)malloc(sizeof(double) * (size_t)ffn);
 #pragma omp for schedule(static)
             for (int64_t i = 0; i < d; ++i) {
-                for (int64_t n = 0; n < ffn; ++n) r2[n] = widen(W2[i * ffn + n]);
+                if (!widen_row(w2, (int64_t)e * d + i, ffn, r2)) {
+#pragma omp atomic write
+                    bad = 1;
+                }
                 for (int64_t q = 0; q < n_rows; ++q) {
                     const double* ha = h + rows[q] * ffn;
                     double s = 0.0;
@@ -261,6 +317,11 @@ int oracle_moe_apply(const uint16_t* x, const uint16_t* w1, const uint16_t* w3,
             }
             free(r2);
         }
+    }
+
+    if (bad) {
+        free(xd); free(h); free(y); free(rows);
+        return ORACLE_NONFINITE;
     }
 
     /* out[t,i] = sum_{j ascending} gates[t,j] * y[t*k+j, i] */
@@ -277,6 +338,27 @@ int oracle_moe_apply(const uint16_t* x, const uint16_t* w1, const uint16_t* w3,
     return ORACLE_OK;
 }
 
+int oracle_moe_apply(const uint16_t* x, const uint16_t* w1, const uint16_t* w3,
+                     const uint16_t* w2, const int32_t* ids, const double* gates,
+                     int64_t T, int64_t d, int64_t ffn, int E, int k,
+                     double* out, double* h_slots, double* y_slots)
+{
+    const wmat_t m1 = {w1, NULL, NULL}, m3 = {w3, NULL, NULL}, m2 = {w2, NULL, NULL};
+    return moe_apply(x, m1, m3, m2, ids, gates, T, d, ffn, E, k, out, h_slots, y_slots);
+}
+
+/* As oracle_moe_apply with E4M3 expert weights and per-row scales:
+ * w1q/w3q [E,ffn,d] bytes, w1s/w3s [E,ffn]; w2q [E,d,ffn], w2s [E,d]. */
+int oracle_moe_apply_fp8(const uint16_t* x, const uint8_t* w1q, const float* w1s,
+                         const uint8_t* w3q, const float* w3s, const uint8_t* w2q,
+                         const float* w2s, const int32_t* ids, const double* gates,
+                         int64_t T, int64_t d, int64_t ffn, int E, int k,
+                         double* out, double* h_slots, double* y_slots)
+{
+    const wmat_t m1 = {NULL, w1q, w1s}, m3 = {NULL, w3q, w3s}, m2 = {NULL, w2q, w2s};
+    return moe_apply(x, m1, m3, m2, ids, gates, T, d, ffn, E, k, out, h_slots, y_slots);
+}
+
 /* The whole layer: router GEMM, top-k gating, experts, combine.  ids, gates
  * and logits are outputs (logits [T,E], ids/gates [T,k]). */
 int oracle_moe_layer(const uint16_t* x, const uint16_t* wr, const float* bias,
@@ -289,6 +371,21 @@ int oracle_moe_layer(const uint16_t* x, const uint16_t* wr, const float* bias,
     rc = oracle_topk_gate(logits, T, E, k, ids, gates);
     if (rc) return rc;
     return oracle_moe_apply(x, w1, w3, w2, ids, gates, T, d, ffn, E, k, out, NULL, NULL);
+}
+
+/* The whole layer with E4M3 expert weights (router in bf16). */
+int oracle_moe_layer_fp8(const uint16_t* x, const uint16_t* wr, const float* bias,
+                         const uint8_t* w1q, const float* w1s, const uint8_t* w3q,
+                         const float* w3s, const uint8_t* w2q, const float* w2s,
+                         int64_t T, int64_t d, int64_t ffn, int E, int k,
+                         double* out, double* logits, int32_t* ids, double* gates)
+{
+    int rc = oracle_router_logits(x, wr, bias, T, d, E, logits);
+    if (rc) return rc;
+    rc = oracle_topk_gate(logits, T, E, k, ids, gates);
+    if (rc) return rc;
+    return oracle_moe_apply_fp8(x, w1q, w1s, w3q, w3s, w2q, w2s, ids, gates, T, d, ffn, E, k,
+                                out, NULL, NULL);
 }
 
 /* ---- RMSNorm for the residual stack -------------------------------------- */

@@ -57,8 +57,14 @@ class Oracle:
         L.oracle_moe_layer.argtypes = [_p, _p, _p, _p, _p, _p, _i64, _i64, _i64,
                                        ctypes.c_int, ctypes.c_int, _p, _p, _p, _p]
         L.oracle_rmsnorm.argtypes = [_p, _p, _i64, _i64, _f64, _p]
+        L.oracle_fp8_e4m3.argtypes = [_p, _i64, _p]
+        L.oracle_moe_apply_fp8.argtypes = [_p, _p, _p, _p, _p, _p, _p, _p, _p, _i64, _i64, _i64,
+                                           ctypes.c_int, ctypes.c_int, _p, _p, _p]
+        L.oracle_moe_layer_fp8.argtypes = [_p, _p, _p, _p, _p, _p, _p, _p, _p, _i64, _i64, _i64,
+                                           ctypes.c_int, ctypes.c_int, _p, _p, _p, _p]
         for f in ("oracle_router_logits", "oracle_topk_gate", "oracle_gates_for_ids", "oracle_dispatch",
-                  "oracle_moe_apply", "oracle_moe_layer", "oracle_rmsnorm"):
+                  "oracle_moe_apply", "oracle_moe_layer", "oracle_rmsnorm", "oracle_fp8_e4m3",
+                  "oracle_moe_apply_fp8", "oracle_moe_layer_fp8"):
             getattr(L, f).restype = ctypes.c_int
 
     # -- helpers -----------------------------------------------------------
@@ -158,6 +164,66 @@ class Oracle:
             self._ptr(x), self._ptr(wr), self._ptr(b), self._ptr(w1), self._ptr(w3),
             self._ptr(w2), T, d, ffn, E, k, self._ptr(out), self._ptr(logits), self._ptr(ids),
             self._ptr(gates)), "moe_layer")
+        return {"out": out, "logits": logits, "ids": ids, "gates": gates}
+
+    @staticmethod
+    def _u8(a, shape=None):
+        a = a.cpu().numpy() if hasattr(a, "cpu") else a
+        a = np.ascontiguousarray(a, dtype=np.uint8)
+        if shape is not None:
+            assert a.shape == tuple(shape), (a.shape, shape)
+        return a
+
+    @staticmethod
+    def _f32(a, shape=None):
+        a = a.cpu().numpy() if hasattr(a, "cpu") else a
+        a = np.ascontiguousarray(a, dtype=np.float32)
+        if shape is not None:
+            assert a.shape == tuple(shape), (a.shape, shape)
+        return a
+
+    def fp8_e4m3(self, q):
+        q = self._u8(q)
+        out = np.empty(q.shape, np.float64)
+        self._check(self.lib.oracle_fp8_e4m3(self._ptr(q), q.size, self._ptr(out)), "fp8_e4m3")
+        return out
+
+    def _fp8_weights(self, w1q, w1s, w3q, w3s, w2q, w2s, d):
+        E, ffn = w1s.shape
+        return (self._u8(w1q, (E, ffn, d)), self._f32(w1s, (E, ffn)), self._u8(w3q, (E, ffn, d)),
+                self._f32(w3s, (E, ffn)), self._u8(w2q, (E, d, ffn)), self._f32(w2s, (E, d)))
+
+    def moe_apply_fp8(self, x, w1q, w1s, w3q, w3s, w2q, w2s, ids, gates, want_slots=False):
+        T, d = x.shape
+        ws = self._fp8_weights(w1q, w1s, w3q, w3s, w2q, w2s, d)
+        E, ffn = ws[1].shape
+        ids = np.ascontiguousarray(ids, dtype=np.int32)
+        gates = np.ascontiguousarray(gates, dtype=np.float64)
+        k = ids.shape[1]
+        x = self._bits(x)
+        out = np.empty((T, d), np.float64)
+        h = np.empty((T * k, ffn), np.float64) if want_slots else None
+        y = np.empty((T * k, d), np.float64) if want_slots else None
+        self._check(self.lib.oracle_moe_apply_fp8(
+            self._ptr(x), *[self._ptr(a) for a in ws], self._ptr(ids), self._ptr(gates),
+            T, d, ffn, E, k, self._ptr(out), self._ptr(h), self._ptr(y)), "moe_apply_fp8")
+        return (out, h, y) if want_slots else out
+
+    def moe_layer_fp8(self, x, wr, w1q, w1s, w3q, w3s, w2q, w2s, k, bias=None):
+        """The layer with E4M3 expert weights; returns dict(out, logits, ids, gates)."""
+        T, d = x.shape
+        ws = self._fp8_weights(w1q, w1s, w3q, w3s, w2q, w2s, d)
+        E, ffn = ws[1].shape
+        x, wr = self._bits(x), self._bits(wr, (E, d))
+        b = None if bias is None else np.ascontiguousarray(bias, dtype=np.float32)
+        out = np.empty((T, d), np.float64)
+        logits = np.empty((T, E), np.float64)
+        ids = np.empty((T, k), np.int32)
+        gates = np.empty((T, k), np.float64)
+        self._check(self.lib.oracle_moe_layer_fp8(
+            self._ptr(x), self._ptr(wr), self._ptr(b), *[self._ptr(a) for a in ws],
+            T, d, ffn, E, k, self._ptr(out), self._ptr(logits), self._ptr(ids), self._ptr(gates)),
+            "moe_layer_fp8")
         return {"out": out, "logits": logits, "ids": ids, "gates": gates}
 
     def rmsnorm(self, h, gamma, eps):

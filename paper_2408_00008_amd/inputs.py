@@ -20,6 +20,10 @@ convention of Mixtral checkpoints:
 * ``w2``       [E, d, ffn]
 * ``router_bias`` float32 [E] or None
 
+8-bit variants (:func:`make_layer_fp8`) quantize the same float draws per
+weight row to OCP E4M3 bytes with a float32 scale per row; that rounding is
+input preparation, like the rounding to bfloat16 above.
+
 The workloads mirror the serving setting of the paper's experiments section
 (a Mixtral-8x7B endpoint at 64 concurrent requests): a 64-token decode step, a
 skewed-routing decode step, a 4096-token prefill chunk (8 requests x 512 prompt
@@ -57,6 +61,7 @@ class Workload:
     layers: int = 1  # >1: a stack of MoE layers, each preceded by RMSNorm + residual
     eps: float = 1e-5  # RMSNorm epsilon for stacks
     seed: int = 0
+    fp8: bool = False  # expert weights as E4M3 bytes with per-row scales
 
     def replace(self, **kw) -> "Workload":
         return dataclasses.replace(self, **kw)
@@ -82,6 +87,12 @@ WORKLOADS = {
     # prefill chunk of 8 x 512 prompt tokens; router logits ~ N(0,1)
     "prefill_t4096": Workload("prefill_t4096", 4096, MIXTRAL_D, MIXTRAL_FFN, MIXTRAL_E, MIXTRAL_K,
                               1.0, 1 / 64.0, 0.02, 0.02, 0.02),
+    # the decode step with 8-bit (E4M3, per-row scale) expert weights
+    "decode_t64_fp8": Workload("decode_t64_fp8", 64, MIXTRAL_D, MIXTRAL_FFN, MIXTRAL_E, MIXTRAL_K,
+                               1.0, 0.02, 0.02, 0.02, 0.02, fp8=True),
+    "decode_t256_skew_fp8": Workload("decode_t256_skew_fp8", 256, MIXTRAL_D, MIXTRAL_FFN,
+                                     MIXTRAL_E, MIXTRAL_K, 1.0, 0.02, 0.02, 0.02, 0.02,
+                                     bias0=2.0, fp8=True),
     # 32 stacked layers, RMSNorm + residual around each, one decode step of 64
     "stack32_t64": Workload("stack32_t64", 64, MIXTRAL_D, MIXTRAL_FFN, MIXTRAL_E, MIXTRAL_K,
                             1.0, 0.02, 0.02, 0.02, 0.02, layers=32),
@@ -117,6 +128,49 @@ def make_layer(w: Workload, layer: int = 0, device="cpu") -> dict:
         "w2": randn_bf16((E, d, f), w.std_w2, w.seed, layer, TID_W2, device),
         "router_bias": None,
     }
+    if w.has_bias:
+        b = torch.zeros(E, dtype=torch.float32, device=device)
+        b[0] = w.bias0
+        out["router_bias"] = b
+    return out
+
+
+FP8_MAX = 448.0  # largest finite OCP E4M3 value
+
+
+def quantize_rows_fp8(w: torch.Tensor):
+    """8-bit expert weights from float ones, one scale per row (output channel):
+    s = max|row| / 448, q = E4M3(row / s) rounded to nearest even (torch's
+    float8_e4m3fn cast).  Returns (q as uint8 bytes, s as float32 [..., rows]).
+    An all-zero row gets scale 1."""
+    w = w.float()
+    amax = w.abs().amax(dim=-1)
+    s = torch.where(amax > 0, amax / FP8_MAX, torch.ones_like(amax))
+    q = (w / s.unsqueeze(-1)).clamp(-FP8_MAX, FP8_MAX).to(torch.float8_e4m3fn)
+    return q.view(torch.uint8), s.contiguous()
+
+
+def randn_f32(shape, std: float, seed: int, layer: int, tid: int, device="cpu") -> torch.Tensor:
+    """float32 N(0, std^2) draws (the source the bf16 weights are rounded from)."""
+    g = _gen(seed, layer, tid, device)
+    t = torch.randn(*shape, generator=g, device=device, dtype=torch.float32)
+    return t.mul_(std)
+
+
+def make_layer_fp8(w: Workload, layer: int = 0, device="cpu") -> dict:
+    """One MoE layer with 8-bit expert weights: router_w (bf16) and router_bias
+    as in :func:`make_layer`; w1q, w3q [E, ffn, d] and w2q [E, d, ffn] as
+    E4M3 bytes (uint8) with per-row float32 scales w1s, w3s [E, ffn] and
+    w2s [E, d].  The float weights are the same draws the bf16 layer rounds."""
+    E, d, f = w.E, w.d, w.ffn
+    out = {
+        "router_w": randn_bf16((E, d), w.std_router, w.seed, layer, TID_ROUTER, device),
+        "router_bias": None,
+    }
+    for name, shape, std, tid in (("w1", (E, f, d), w.std_w1, TID_W1), ("w3", (E, f, d), w.std_w3, TID_W3),
+                                  ("w2", (E, d, f), w.std_w2, TID_W2)):
+        q, sc = quantize_rows_fp8(randn_f32(shape, std, w.seed, layer, tid, device))
+        out[name + "q"], out[name + "s"] = q, sc
     if w.has_bias:
         b = torch.zeros(E, dtype=torch.float32, device=device)
         b[0] = w.bias0

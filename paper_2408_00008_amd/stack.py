@@ -104,16 +104,19 @@ def bench_stack(args, w: inputs.Workload):
     for _ in range(args.warmup):
         st.replay()
     torch.cuda.synchronize()
-    e0 = torch.cuda.Event(enable_timing=True)
-    e1 = torch.cuda.Event(enable_timing=True)
+    bounds = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     t0 = time.perf_counter()
-    e0.record(stream)
-    for _ in range(args.steps):
+    bounds[0].record(stream)
+    for i in range(args.steps):
         st.replay()
-    e1.record(stream)
+        bounds[i + 1].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    ms = e0.elapsed_time(e1) / args.steps
+    ms = bounds[0].elapsed_time(bounds[-1]) / args.steps
+    step_ms = sorted(bounds[i].elapsed_time(bounds[i + 1]) for i in range(args.steps))
+    pct = [step_ms[min(len(step_ms) - 1, int(q * len(step_ms)))] for q in (0.1, 0.5, 0.9)]
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
     # the same step without the graph, for the launch-overhead comparison
     st.load_input(x)
     torch.cuda.synchronize()
@@ -134,6 +137,7 @@ def bench_stack(args, w: inputs.Workload):
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": round(ms, 4),
+        "step_ms_p10_p50_p90": [round(v, 4) for v in pct],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,

@@ -67,3 +67,17 @@ def rowwise_rel(got, ref) -> float:
     den = np.abs(ref).max(axis=-1)
     den = np.where(den == 0, 1.0, den)
     return float((num / den).max())
+
+
+def tiny_case_fp8(T, d, ffn, E, k, seed=0, std=0.5, bias=None):
+    """tiny_case with E4M3 expert weights (per-row scales), quantized from
+    float normals by the input generator's row quantizer."""
+    from paper_2408_00008_amd import inputs
+
+    c = tiny_case(T, d, ffn, E, k, seed=seed, std=std, bias=bias)
+    g = torch.Generator().manual_seed(seed * 7919 + 17)
+    for name, shape in (("w1", (E, ffn, d)), ("w3", (E, ffn, d)), ("w2", (E, d, ffn))):
+        w = torch.randn(*shape, generator=g, dtype=torch.float32) * std
+        q, s = inputs.quantize_rows_fp8(w)
+        c[name + "q"], c[name + "s"] = q.numpy(), s.numpy()
+    return c

@@ -12,7 +12,10 @@ the mutation test) and raises AssertionError if the oracle disagrees with:
   numbers are stored in ``tests/golden/hand_example.json``;
 * invariants of the layer: gate weights sum to one, token-permutation
   equivariance, a zeroed expert contributes nothing, relabelling experts
-  changes nothing, scaling W2 by a power of two scales the output exactly.
+  changes nothing, scaling W2 by a power of two scales the output exactly;
+* for 8-bit (OCP E4M3) expert weights: every byte against torch's
+  float8_e4m3fn conversion, the values the OCP specification tabulates, and
+  the brute force fed with weights dequantized by torch.
 """
 
 from __future__ import annotations
@@ -25,7 +28,7 @@ import numpy as np
 import torch
 
 import bruteforce as bf
-from helpers import bits_of, tiny_case, widen
+from helpers import bits_of, tiny_case, tiny_case_fp8, widen
 
 GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
 
@@ -324,6 +327,69 @@ def pin_empty(o):
     assert r["out"].shape == (0, 8) and r["ids"].shape == (0, 2)
 
 
+def _fp8_torch(q):
+    return torch.from_numpy(np.ascontiguousarray(q, np.uint8)).view(torch.float8_e4m3fn).to(torch.float64).numpy()
+
+
+def pin_fp8_decode_table(o):
+    """All 256 E4M3 bytes decode like torch's float8_e4m3fn (a library
+    implementation of the OCP format), signs of zeros included."""
+    codes = np.arange(256, dtype=np.uint8)
+    got = o.fp8_e4m3(codes)
+    ref = _fp8_torch(codes)
+    nan = np.isnan(ref)
+    assert np.array_equal(np.isnan(got), nan)
+    assert np.array_equal(got[~nan], ref[~nan])
+    assert np.array_equal(np.signbit(got[~nan]), np.signbit(ref[~nan]))
+
+
+def pin_fp8_spec_values(o):
+    """Values the OCP 8-bit floating point specification gives for E4M3: the
+    smallest subnormal and normal, one, the largest finite value, NaN."""
+    table = {0x00: 0.0, 0x01: 2.0 ** -9, 0x07: 7 * 2.0 ** -9, 0x08: 2.0 ** -6, 0x38: 1.0,
+             0x39: 1.125, 0x7E: 448.0, 0xFE: -448.0, 0xB8: -1.0}
+    codes = np.array(sorted(table), dtype=np.uint8)
+    got = o.fp8_e4m3(codes)
+    assert got.tolist() == [table[c] for c in sorted(table)]
+    nz = o.fp8_e4m3(np.array([0x80, 0x7F, 0xFF], dtype=np.uint8))
+    assert nz[0] == 0.0 and np.signbit(nz[0]) and np.isnan(nz[1]) and np.isnan(nz[2])
+
+
+def _run_fp8(o, c):
+    return o.moe_layer_fp8(c["x"], c["wr"], c["w1q"], c["w1s"], c["w3q"], c["w3s"], c["w2q"], c["w2s"],
+                           c["k"], c["bias"])
+
+
+def pin_fp8_layer_bruteforce(o):
+    """The 8-bit layer == the brute force on weights dequantized by torch
+    (decoded byte times the row's scale)."""
+    for i, (T, d, ffn, E, k) in enumerate(TINY_SHAPES[:5]):
+        c = tiny_case_fp8(T, d, ffn, E, k, seed=300 + i)
+        deq = {n: (_fp8_torch(c[n + "q"]) * c[n + "s"].astype(np.float64)[..., None]).tolist()
+               for n in ("w1", "w3", "w2")}
+        out, ids, gates, logits = bf.moe_layer(_nested(c["x"]), _nested(c["wr"]), deq["w1"], deq["w3"],
+                                               deq["w2"], k, None)
+        r = _run_fp8(o, c)
+        assert r["ids"].tolist() == ids
+        _close(r["gates"], gates)
+        _close(r["out"], out, rtol=1e-11, atol=1e-12)
+
+
+def pin_fp8_row_scale(o):
+    """Doubling the scale of W2 row i doubles output column i exactly and
+    leaves the other columns unchanged."""
+    c = tiny_case_fp8(6, 8, 12, 4, 2, seed=331)
+    r = _run_fp8(o, c)
+    c2 = dict(c)
+    s2 = c["w2s"].copy()
+    s2[:, 3] *= 2.0
+    c2["w2s"] = s2
+    r2 = _run_fp8(o, c2)
+    assert np.array_equal(r2["out"][:, 3], 2.0 * r["out"][:, 3])
+    keep = [i for i in range(8) if i != 3]
+    assert np.array_equal(r2["out"][:, keep], r["out"][:, keep])
+
+
 ALL_PINS = [
     pin_bruteforce_random,
     pin_bruteforce_ties,
@@ -340,4 +406,8 @@ ALL_PINS = [
     pin_rmsnorm,
     pin_gates_for_ids,
     pin_empty,
+    pin_fp8_decode_table,
+    pin_fp8_spec_values,
+    pin_fp8_layer_bruteforce,
+    pin_fp8_row_scale,
 ]

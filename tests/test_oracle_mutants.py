@@ -28,8 +28,13 @@ MUTANTS = {
                                  "gates[t * k + j] = exp(l[s[j]]) / denom;"),
     "bias_dropped": ("if (bias) s += (double)bias[e];", ";"),
     "router_transposed": ("widen(wr[e * d + i])", "widen(wr[i * E + e])"),
-    "w2_transposed": ("r2[n] = widen(W2[i * ffn + n]);", "r2[n] = widen(W2[n * d + i]);"),
-    "w1_transposed": ("r1[i] = widen(W1[n * d + i]);", "r1[i] = widen(W1[i * ffn + n]);"),
+    "w2_row_stride": ("widen_row(w2, (int64_t)e * d + i, ffn, r2)", "widen_row(w2, (int64_t)e * ffn + i, ffn, r2)"),
+    "w1_row_stride": ("widen_row(w1, (int64_t)e * ffn + n, d, r1)", "widen_row(w1, (int64_t)e * d + n, d, r1)"),
+    "weight_row_reversed": ("out[i] = widen(w.bf16[r * cols + i]);", "out[i] = widen(w.bf16[r * cols + (cols - 1 - i)]);"),
+    "fp8_bias_8": ("ldexp(1.0 + (double)m / 8.0, e - 7)", "ldexp(1.0 + (double)m / 8.0, e - 8)"),
+    "fp8_subnormal_as_normal": ("v = ldexp((double)m / 8.0, -6);", "v = ldexp(1.0 + (double)m / 8.0, -7);"),
+    "fp8_scale_dropped": ("out[i] = fp8_e4m3(w.q[r * cols + i]) * s;", "out[i] = fp8_e4m3(w.q[r * cols + i]);"),
+    "fp8_sign_dropped": ("return sign ? -v : v;", "return v;"),
     "token_index": ("xd + (rows[q] / k) * d", "xd + (rows[q] % k) * d"),
     "combine_first_gate_only": ("s += gates[t * k + j] * y", "s += gates[t * k] * y"),
     "combine_unweighted": ("s += gates[t * k + j] * y", "s += y"),
