@@ -103,9 +103,17 @@ def main():
         return stack.bench_stack(args, w)
     T, d, ffn, E, k = w.T, w.d, w.ffn, w.E, w.k
     A = T * k
-    lay = inputs.make_layer(w, 0, dev)
     x = inputs.make_x(w, dev)
-    rw, w1, w3, w2, bias = lay["router_w"], lay["w1"], lay["w3"], lay["w2"], lay["router_bias"]
+    if w.fp8:
+        # E4M3 expert weights with per-row f32 scales (always the streaming kernels)
+        lay = inputs.make_layer_fp8(w, 0, dev)
+        q = [lay[n] for n in ("w1q", "w1s", "w3q", "w3s", "w2q", "w2s")]
+        wbytes_per_elem = 1
+    else:
+        lay = inputs.make_layer(w, 0, dev)
+        w1, w3, w2 = lay["w1"], lay["w3"], lay["w2"]
+        wbytes_per_elem = 2
+    rw, bias = lay["router_w"], lay["router_bias"]
 
     ids = torch.empty(T, k, dtype=torch.int32, device=dev)
     gw = torch.empty(T, k, dtype=torch.float32, device=dev)
@@ -120,10 +128,17 @@ def main():
         B.moe_route(x, rw, k, ids, gw, offs, perm, router_bias=bias, stream=stream)
         if ev0 is not None:
             ev0.record(stream)
-        B.moe_swiglu_up(x, offs, w1, w3, T, k, h, perm=perm, stream=stream)
+        if w.fp8:
+            B.moe_swiglu_up_fp8(x, offs, q[0], q[1], q[2], q[3], T, k, h, perm=perm, stream=stream)
+        else:
+            B.moe_swiglu_up(x, offs, w1, w3, T, k, h, perm=perm, stream=stream)
         if ev1 is not None:
             ev1.record(stream)
-        B.moe_swiglu_down(h, offs, w2, T, k, y, topk_w=gw, perm=perm, stream=stream)
+        if w.fp8:
+            B.moe_swiglu_down_fp8(h, offs, q[4], q[5], T, k, y, topk_w=gw, perm=perm,
+                                  stream=stream)
+        else:
+            B.moe_swiglu_down(h, offs, w2, T, k, y, topk_w=gw, perm=perm, stream=stream)
         B.moe_combine(y, T, d, k, out=out, stream=stream)
 
     for _ in range(args.warmup):
@@ -151,10 +166,13 @@ def main():
 
     counts = np.diff(offs.cpu().numpy())
     active = int((counts > 0).sum())
-    variant = {1: "stream", 2: "tiled"}[B.moe_gemm_variant_for(T, d, ffn, E, k)]
-    # algorithmic work of the up kernel: each active expert's w1 and w3 once,
-    # the routed token rows read once, h written once; 4*d*ffn FLOP per row
-    up_bytes = active * 2 * ffn * d * 2 + A * d * 2 + A * ffn * 2
+    variant = "stream" if w.fp8 else {1: "stream", 2: "tiled"}[B.moe_gemm_variant_for(T, d, ffn, E, k)]
+    # algorithmic work of the up kernel: each active expert's w1 and w3 once
+    # (bf16, or E4M3 bytes plus one f32 scale per row), the routed token rows
+    # read once, h written once; 4*d*ffn FLOP per row
+    scale_bytes = 4 if w.fp8 else 0
+    up_bytes = (active * 2 * ffn * (d * wbytes_per_elem + scale_bytes) + A * d * 2
+                + A * ffn * 2)
     up_flops = 4.0 * A * d * ffn
     kernel = "expert_up_" + variant
     if variant == "stream":
@@ -172,7 +190,8 @@ def main():
     roof["algorithmic_flop_per_launch"] = up_flops
 
     layer_flops = 2.0 * T * d * E + 6.0 * A * d * ffn
-    layer_bytes = active * 3 * ffn * d * 2 + E * d * 2 + T * d * 2 * 2
+    layer_bytes = (active * (3 * ffn * d * wbytes_per_elem + (2 * ffn + d) * scale_bytes)
+                   + E * d * 2 + T * d * 2 * 2)
     tok_s = T * args.steps / (ms_total * 1e-3)
 
     cpu = None
@@ -191,9 +210,10 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16",
+        "dtype": "bf16",  # MFMA operands; E4M3 weights are widened exactly to bf16
         "data": "synthetic (seeded normals of the Mixtral-8x7B layer shapes; no dataset, random weights)",
         "config": {"workload": args.workload, "T": T, "d": d, "ffn": ffn, "E": E, "k": k,
+                   "expert_weights": "e4m3 + f32 row scale" if w.fp8 else "bf16",
                    "router_bias0": w.bias0, "seed": args.seed, "active_experts": active,
                    "rows_per_expert": counts.tolist()},
         "layer": {"tflops": round(layer_flops / (ms_per_step * 1e-3) / 1e12, 2),
@@ -221,20 +241,30 @@ def cpu_baseline(args, w, x, lay, T):
     cores = len(os.sched_getaffinity(0))
     cores = min(cores, int(os.environ.get("OMP_NUM_THREADS", cores)))
     o.threads(cores)
-    bits = {n: inputs.bf16_bits(lay[n]) for n in ("router_w", "w1", "w3", "w2")}
     xb = inputs.bf16_bits(x)
+    rwb = inputs.bf16_bits(lay["router_w"])
     bias = None if lay["router_bias"] is None else lay["router_bias"].cpu().numpy()
+    if w.fp8:
+        ws = [lay[n].cpu().numpy() for n in ("w1q", "w1s", "w3q", "w3s", "w2q", "w2s")]
+
+        def layer(n):
+            o.moe_layer_fp8(xb[:n], rwb, *ws, w.k, bias)
+    else:
+        ws = [inputs.bf16_bits(lay[n]) for n in ("w1", "w3", "w2")]
+
+        def layer(n):
+            o.moe_layer(xb[:n], rwb, *ws, w.k, bias)
     S = T
     # probe with a small slice, then size the sample
     t0 = time.perf_counter()
-    o.moe_layer(xb[:min(T, 8)], bits["router_w"], bits["w1"], bits["w3"], bits["w2"], w.k, bias)
+    layer(min(T, 8))
     probe = time.perf_counter() - t0
     if T > 8 and probe * T / 8 > 3 * args.cpu_seconds:
         S = max(8, int(8 * args.cpu_seconds / probe))
     tokens, el, reps = 0, 0.0, 0
     while el < args.cpu_seconds and reps < 1000:
         t0 = time.perf_counter()
-        o.moe_layer(xb[:S], bits["router_w"], bits["w1"], bits["w3"], bits["w2"], w.k, bias)
+        layer(S)
         el += time.perf_counter() - t0
         tokens += S
         reps += 1

@@ -167,6 +167,41 @@ moe_status_t moe_forward_ex(const moe_bf16_t* x, const moe_bf16_t* router_w,
                             size_t workspace_bytes, hipStream_t stream);
 
 /*
+ * 8-bit expert weights (Sec. 4.1, "Model Quantization": weights stored as
+ * 8-bit floats; Sec. 5 serves an 8-bit quantized Mixtral-8x7B).  Each expert
+ * matrix is held as OCP FP8 E4M3 bytes -- sign, 4 exponent bits with bias 7,
+ * 3 mantissa bits; exponent 0 is subnormal (m/8 * 2^-6); S.1111.111 is NaN;
+ * largest finite value 448 -- with one f32 scale per weight row:
+ *   w1[e,n,i] = e4m3(w1q[e,n,i]) * w1s[e,n]     w1q, w3q [E,ffn,d] u8, w1s, w3s [E,ffn] f32
+ *   w2[e,i,n] = e4m3(w2q[e,i,n]) * w2s[e,i]     w2q [E,d,ffn] u8,  w2s [E,d] f32
+ * The E4M3 values convert exactly to bf16 operands, products accumulate in
+ * f32 and each row's sum is multiplied by its scale; everything else (token
+ * rows, h, y, out, routing) is as in the bf16 calls of the same name, with
+ * the same limits and alignment rules (byte arrays and scales 16-byte
+ * aligned).  A NaN byte, or a non-finite scale, makes the rows it reaches
+ * NaN.  These calls always use the weight-streaming kernels.
+ */
+moe_status_t moe_swiglu_up_fp8(const moe_bf16_t* x, const int32_t* perm,
+                               const int32_t* expert_offsets, const uint8_t* w1q,
+                               const float* w1s, const uint8_t* w3q, const float* w3s, int64_t T,
+                               int32_t d, int32_t ffn, int32_t E, int32_t k, moe_bf16_t* h,
+                               hipStream_t stream);
+
+moe_status_t moe_swiglu_down_fp8(const moe_bf16_t* h, const int32_t* expert_offsets,
+                                 const uint8_t* w2q, const float* w2s, const float* topk_w,
+                                 const int32_t* perm, int64_t T, int32_t d, int32_t ffn, int32_t E,
+                                 int32_t k, float* y, hipStream_t stream);
+
+/* moe_forward_ex with the 8-bit expert weights above (the router stays bf16). */
+moe_status_t moe_forward_fp8_ex(const moe_bf16_t* x, const moe_bf16_t* router_w,
+                                const float* router_bias, const uint8_t* w1q, const float* w1s,
+                                const uint8_t* w3q, const float* w3s, const uint8_t* w2q,
+                                const float* w2s, int64_t T, int32_t d, int32_t ffn, int32_t E,
+                                int32_t k, const float* residual, moe_bf16_t* out,
+                                float* out_f32, void* workspace, size_t workspace_bytes,
+                                hipStream_t stream);
+
+/*
  * RMSNorm of the f32 residual stream, as in front of each MoE block of a
  * pre-norm residual stack (Mixtral's layer structure, Sec. 4.1 citation):
  *   a[t,i] = bf16( h[t,i] / sqrt(mean_i h[t,i]^2 + eps) * gamma[i] )
@@ -183,7 +218,7 @@ size_t moe_workspace_size(int64_t T, int32_t d, int32_t ffn, int32_t E, int32_t 
  *   0 = automatic (by rows per expert, T*k/E), 1 = weight-streaming (decode
  *   shapes), 2 = tiled (prefill shapes).  Process-wide; returns the previous
  *   value, or -1 for an unknown value (nothing changed).  For testing and
- *   measurement.
+ *   measurement.  The 8-bit weight calls ignore it.
  */
 int moe_set_gemm_variant(int variant);
 

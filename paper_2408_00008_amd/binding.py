@@ -24,6 +24,7 @@ VARIANT_AUTO, VARIANT_STREAM, VARIANT_TILED = 0, 1, 2
 EXPORTS = (
     "moe_route", "moe_permute", "moe_swiglu_up", "moe_swiglu_down", "moe_grouped_swiglu",
     "moe_combine", "moe_forward", "moe_forward_ex", "moe_rmsnorm", "moe_workspace_size",
+    "moe_swiglu_up_fp8", "moe_swiglu_down_fp8", "moe_forward_fp8_ex",
     "moe_set_gemm_variant", "moe_gemm_variant_for", "moe_status_string", "moe_last_error", "moe_version",
 )
 
@@ -61,6 +62,10 @@ def lib() -> ctypes.CDLL:
         "moe_forward": [p, p, p, p, p, i64, i32, i32, i32, i32, p, p],
         "moe_forward_ex": [p, p, p, p, p, p, i64, i32, i32, i32, i32, p, p, p, p, sz, p],
         "moe_rmsnorm": [p, p, i64, i32, f32, p, p],
+        "moe_swiglu_up_fp8": [p, p, p, p, p, p, p, i64, i32, i32, i32, i32, p, p],
+        "moe_swiglu_down_fp8": [p, p, p, p, p, p, i64, i32, i32, i32, i32, p, p],
+        "moe_forward_fp8_ex": [p, p, p, p, p, p, p, p, p, i64, i32, i32, i32, i32, p, p, p, p,
+                               sz, p],
     }
     for name, args in sig.items():
         fn = getattr(L, name)
@@ -107,7 +112,7 @@ def _stream(stream) -> Optional[int]:
     return int(stream)
 
 
-bf16, f32, i32 = torch.bfloat16, torch.float32, torch.int32
+bf16, f32, i32, u8 = torch.bfloat16, torch.float32, torch.int32, torch.uint8
 
 
 def moe_route(x, router_w, k, topk_ids, topk_w, expert_offsets, perm, router_bias=None,
@@ -179,6 +184,38 @@ def moe_forward_ex(x, router_w, w1, w3, w2, k, out=None, out_f32=None, router_bi
         _ptr(w1, bf16, "w1"), _ptr(w3, bf16, "w3"), _ptr(w2, bf16, "w2"), T, d, ffn, E, k,
         _ptr(residual, f32, "residual"), _ptr(out, bf16, "out"), _ptr(out_f32, f32, "out_f32"),
         _ptr(workspace, None, "workspace"), ws_bytes, _stream(stream)), "moe_forward_ex")
+
+
+def moe_swiglu_up_fp8(x, expert_offsets, w1q, w1s, w3q, w3s, T, k, h, perm=None, stream=None):
+    """8-bit weights: w1q/w3q [E,ffn,d] E4M3 bytes (uint8), w1s/w3s [E,ffn] f32 row scales."""
+    E, ffn, d = w1q.shape
+    _check(lib().moe_swiglu_up_fp8(
+        _ptr(x, bf16, "x"), _ptr(perm, i32, "perm"), _ptr(expert_offsets, i32, "offsets"),
+        _ptr(w1q, u8, "w1q"), _ptr(w1s, f32, "w1s"), _ptr(w3q, u8, "w3q"), _ptr(w3s, f32, "w3s"),
+        T, d, ffn, E, k, _ptr(h, bf16, "h"), _stream(stream)), "moe_swiglu_up_fp8")
+
+
+def moe_swiglu_down_fp8(h, expert_offsets, w2q, w2s, T, k, y, topk_w=None, perm=None,
+                        stream=None):
+    """8-bit weights: w2q [E,d,ffn] E4M3 bytes (uint8), w2s [E,d] f32 row scales."""
+    E, d, ffn = w2q.shape
+    _check(lib().moe_swiglu_down_fp8(
+        _ptr(h, bf16, "h"), _ptr(expert_offsets, i32, "offsets"), _ptr(w2q, u8, "w2q"),
+        _ptr(w2s, f32, "w2s"), _ptr(topk_w, f32, "topk_w"), _ptr(perm, i32, "perm"), T, d, ffn,
+        E, k, _ptr(y, f32, "y"), _stream(stream)), "moe_swiglu_down_fp8")
+
+
+def moe_forward_fp8_ex(x, router_w, w1q, w1s, w3q, w3s, w2q, w2s, k, out=None, out_f32=None,
+                       router_bias=None, residual=None, workspace=None, stream=None):
+    T, d = x.shape
+    E, ffn, _ = w1q.shape
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(lib().moe_forward_fp8_ex(
+        _ptr(x, bf16, "x"), _ptr(router_w, bf16, "router_w"), _ptr(router_bias, f32, "router_bias"),
+        _ptr(w1q, u8, "w1q"), _ptr(w1s, f32, "w1s"), _ptr(w3q, u8, "w3q"), _ptr(w3s, f32, "w3s"),
+        _ptr(w2q, u8, "w2q"), _ptr(w2s, f32, "w2s"), T, d, ffn, E, k,
+        _ptr(residual, f32, "residual"), _ptr(out, bf16, "out"), _ptr(out_f32, f32, "out_f32"),
+        _ptr(workspace, None, "workspace"), ws_bytes, _stream(stream)), "moe_forward_fp8_ex")
 
 
 def moe_rmsnorm(h, gamma, eps, a, stream=None):

@@ -10,6 +10,7 @@
 #include <cstdio>
 #include <cstring>
 #include <mutex>
+#include <vector>
 #include <string>
 #include <unordered_map>
 
@@ -193,8 +194,77 @@ moe_status_t library_workspace(size_t need_bytes, hipStream_t stream, void** out
 
 int64_t rows_bound(int64_t T, int32_t) { return T; }
 
+// Expert weights of one call: bf16 matrices, or E4M3 bytes with per-row f32
+// scales (q*, s* non-NULL).
+struct ExpertWeights {
+    const moe_bf16_t* w1 = nullptr;
+    const moe_bf16_t* w3 = nullptr;
+    const moe_bf16_t* w2 = nullptr;
+    const uint8_t* q1 = nullptr;
+    const float* s1 = nullptr;
+    const uint8_t* q3 = nullptr;
+    const float* s3 = nullptr;
+    const uint8_t* q2 = nullptr;
+    const float* s2 = nullptr;
+    bool f8 = false;
+    bool fp8() const { return f8; }
+};
+
+moe_status_t check_up_weights(const ExpertWeights& w)
+{
+    if (!w.fp8()) {
+        TRY(need(w.w1, "w1"));
+        return need(w.w3, "w3");
+    }
+    TRY(need(w.q1, "w1q"));
+    TRY(need(w.s1, "w1s"));
+    TRY(need(w.q3, "w3q"));
+    return need(w.s3, "w3s");
+}
+
+moe_status_t check_down_weights(const ExpertWeights& w)
+{
+    if (!w.fp8()) return need(w.w2, "w2");
+    TRY(need(w.q2, "w2q"));
+    return need(w.s2, "w2s");
+}
+
+// (name, range) of every weight buffer of an up or down call
+std::vector<std::pair<const char*, Range>> weight_ranges(const ExpertWeights& w, int32_t d,
+                                                         int32_t ffn, int32_t E, bool up, bool down)
+{
+    const size_t n = (size_t)E * ffn * d;
+    std::vector<std::pair<const char*, Range>> r;
+    if (!w.fp8()) {
+        if (up) r.push_back({"w1", {w.w1, n * 2}}), r.push_back({"w3", {w.w3, n * 2}});
+        if (down) r.push_back({"w2", {w.w2, n * 2}});
+    } else {
+        if (up) {
+            r.push_back({"w1q", {w.q1, n}});
+            r.push_back({"w1s", {w.s1, (size_t)E * ffn * 4}});
+            r.push_back({"w3q", {w.q3, n}});
+            r.push_back({"w3s", {w.s3, (size_t)E * ffn * 4}});
+        }
+        if (down) {
+            r.push_back({"w2q", {w.q2, n}});
+            r.push_back({"w2s", {w.s2, (size_t)E * d * 4}});
+        }
+    }
+    return r;
+}
+
+moe_status_t no_overlap_v(const char* oname, Range o, const std::vector<std::pair<const char*, Range>>& ins)
+{
+    for (const auto& in : ins)
+        if (overlap(o, in.second))
+            return fail(MOE_ERR_INVALID_ARG, "%s overlaps %s", oname, in.first);
+    return MOE_OK;
+}
+
 hipError_t run_up(const moe::UpArgs& a, int64_t T, hipStream_t stream)
 {
+    // 8-bit weights run the weight-streaming kernels at every size
+    if (a.q1) return moe::launch_stream_up(a, rows_bound(T, a.kslots), stream);
     const int v = moe::resolve_variant(g_variant.load(), a.A, a.E);
     if (v == moe::VARIANT_TILED && moe::tiled_supported(a.d, a.ffn))
         return moe::launch_tiled_up(a, stream);
@@ -203,6 +273,7 @@ hipError_t run_up(const moe::UpArgs& a, int64_t T, hipStream_t stream)
 
 hipError_t run_down(const moe::DownArgs& a, int64_t T, int32_t k, hipStream_t stream)
 {
+    if (a.q2) return moe::launch_stream_down(a, rows_bound(T, k), stream);
     const int v = moe::resolve_variant(g_variant.load(), a.A, a.E);
     if (v == moe::VARIANT_TILED && moe::tiled_supported(a.d, a.ffn))
         return moe::launch_tiled_down(a, stream);
@@ -220,6 +291,162 @@ int resolve_variant(int requested, int64_t A, int E)
     return (A <= 128LL * E) ? VARIANT_STREAM : VARIANT_TILED;
 }
 }  // namespace moe
+
+namespace {
+
+// ---- entry points shared by the bf16 and the 8-bit weight formats --------
+
+moe_status_t swiglu_up_impl(const moe_bf16_t* x_perm, const int32_t* perm,
+                            const int32_t* expert_offsets, const ExpertWeights& w, int64_t T,
+                            int32_t d, int32_t ffn, int32_t E, int32_t k, moe_bf16_t* h,
+                            hipStream_t stream)
+{
+    TRY(check_Ek(E, k));
+    TRY(check_T(T, k));
+    TRY(check_dim("d", d));
+    TRY(check_dim("ffn", ffn));
+    TRY(need_rows(x_perm, "x_perm", T));
+    TRY(need(expert_offsets, "expert_offsets"));
+    TRY(check_up_weights(w));
+    TRY(need_rows(h, "h", T));
+    TRY(maybe(perm, "perm"));
+    const size_t A = static_cast<size_t>(T) * k;
+    const size_t xrows = perm ? static_cast<size_t>(T) : A;
+    auto ins = weight_ranges(w, d, ffn, E, true, false);
+    ins.push_back({"x", {x_perm, xrows * d * 2}});
+    ins.push_back({"expert_offsets", {expert_offsets, (size_t)(E + 1) * 4}});
+    ins.push_back({"perm", {perm, A * 4}});
+    TRY(no_overlap_v("h", {h, A * ffn * 2}, ins));
+    if (T == 0) return ok();
+    moe::UpArgs a{x_perm, perm, k, expert_offsets, w.w1, w.w3, h, (int64_t)A, d, ffn, E};
+    a.q1 = w.q1, a.s1 = w.s1, a.q3 = w.q3, a.s3 = w.s3;
+    hipError_t e = run_up(a, T, stream);
+    return e == hipSuccess ? ok() : hip_fail(e, "expert up kernel launch");
+}
+
+moe_status_t swiglu_down_impl(const moe_bf16_t* h, const int32_t* expert_offsets,
+                              const ExpertWeights& w, const float* topk_w, const int32_t* perm,
+                              int64_t T, int32_t d, int32_t ffn, int32_t E, int32_t k, float* y,
+                              hipStream_t stream)
+{
+    TRY(check_Ek(E, k));
+    TRY(check_T(T, k));
+    TRY(check_dim("d", d));
+    TRY(check_dim("ffn", ffn));
+    TRY(need_rows(h, "h", T));
+    TRY(need(expert_offsets, "expert_offsets"));
+    TRY(check_down_weights(w));
+    TRY(maybe(topk_w, "topk_w"));
+    TRY(maybe(perm, "perm"));
+    TRY(need_rows(y, "y", T));
+    const size_t A = static_cast<size_t>(T) * k;
+    auto ins = weight_ranges(w, d, ffn, E, false, true);
+    ins.push_back({"h", {h, A * ffn * 2}});
+    ins.push_back({"topk_w", {topk_w, A * 4}});
+    ins.push_back({"perm", {perm, A * 4}});
+    ins.push_back({"expert_offsets", {expert_offsets, (size_t)(E + 1) * 4}});
+    TRY(no_overlap_v("y", {y, A * d * 4}, ins));
+    if (T == 0) return ok();
+    const bool scatter = topk_w && perm;
+    moe::DownArgs a{h, expert_offsets, w.w2, scatter ? topk_w : nullptr, scatter ? perm : nullptr,
+                    y, (int64_t)A, d, ffn, E};
+    a.q2 = w.q2, a.s2 = w.s2;
+    hipError_t e = run_down(a, T, k, stream);
+    return e == hipSuccess ? ok() : hip_fail(e, "expert down kernel launch");
+}
+
+moe_status_t forward_impl(const moe_bf16_t* x, const moe_bf16_t* router_w,
+                          const float* router_bias, const ExpertWeights& w, int64_t T, int32_t d,
+                          int32_t ffn, int32_t E, int32_t k, const float* residual,
+                          moe_bf16_t* out, float* out_f32, void* workspace,
+                          size_t workspace_bytes, hipStream_t stream)
+{
+    TRY(check_Ek(E, k));
+    TRY(check_T(T, k));
+    TRY(check_dim("d", d));
+    TRY(check_dim("ffn", ffn));
+    TRY(need_rows(x, "x", T));
+    TRY(need(router_w, "router_w"));
+    TRY(maybe(router_bias, "router_bias"));
+    TRY(check_up_weights(w));
+    TRY(check_down_weights(w));
+    TRY(maybe(residual, "residual"));
+    TRY(maybe(out, "out"));
+    TRY(maybe(out_f32, "out_f32"));
+    if (!out && !out_f32 && T > 0)
+        return fail(MOE_ERR_INVALID_ARG, "out and out_f32 are both NULL");
+    if (workspace && (reinterpret_cast<uintptr_t>(workspace) & 255u))
+        return fail(MOE_ERR_INVALID_ARG, "workspace is not 256-byte aligned");
+    const size_t td = static_cast<size_t>(T) * d;
+    auto ins = weight_ranges(w, d, ffn, E, true, true);
+    ins.push_back({"x", {x, td * 2}});
+    ins.push_back({"router_w", {router_w, (size_t)E * d * 2}});
+    ins.push_back({"router_bias", {router_bias, (size_t)E * 4}});
+    TRY(no_overlap_v("out", {out, td * 2}, ins));
+    TRY(no_overlap("out", {out, td * 2}, {{"residual", {residual, td * 4}}, {"out_f32", {out_f32, td * 4}}}));
+    TRY(no_overlap_v("out_f32", {out_f32, td * 4}, ins));
+    if (residual && out_f32 != residual)
+        TRY(no_overlap("out_f32", {out_f32, td * 4}, {{"residual", {residual, td * 4}}}));
+    const Layout L = layout(T, d, ffn, E, k);
+    if (workspace && workspace_bytes < L.total)
+        return fail(MOE_ERR_NO_MEMORY, "workspace of %zu bytes is smaller than the %zu needed",
+                    workspace_bytes, L.total);
+    if (workspace) {
+        const Range ws{workspace, L.total};
+        TRY(no_overlap_v("workspace", ws, ins));
+        TRY(no_overlap("workspace", ws, {{"out", {out, td * 2}}, {"out_f32", {out_f32, td * 4}},
+                       {"residual", {residual, td * 4}}}));
+    }
+    if (T == 0) return ok();
+
+    void* base = workspace;
+    if (!base) TRY(library_workspace(L.total, stream, &base));
+    char* b = static_cast<char*>(base);
+    int32_t* ids = reinterpret_cast<int32_t*>(b + L.ids);
+    float* gw = reinterpret_cast<float*>(b + L.w);
+    int32_t* offs = reinterpret_cast<int32_t*>(b + L.off);
+    int32_t* perm = reinterpret_cast<int32_t*>(b + L.perm);
+    moe::bf16_t* h = reinterpret_cast<moe::bf16_t*>(b + L.h);
+    float* y = reinterpret_cast<float*>(b + L.y);
+    const int64_t A = T * k;
+
+    hipError_t e = moe::launch_router_topk(x, router_w, router_bias, T, d, E, k, ids, gw, nullptr,
+                                           stream);
+    if (e != hipSuccess) return hip_fail(e, "router kernel launch");
+    e = moe::launch_dispatch(ids, A, E, offs, perm, stream);
+    if (e != hipSuccess) return hip_fail(e, "dispatch kernel launch");
+    moe::UpArgs ua{x, perm, k, offs, w.w1, w.w3, h, A, d, ffn, E};
+    ua.q1 = w.q1, ua.s1 = w.s1, ua.q3 = w.q3, ua.s3 = w.s3;
+    e = run_up(ua, T, stream);
+    if (e != hipSuccess) return hip_fail(e, "expert up kernel launch");
+    moe::DownArgs da{h, offs, w.w2, gw, perm, y, A, d, ffn, E};
+    da.q2 = w.q2, da.s2 = w.s2;
+    e = run_down(da, T, k, stream);
+    if (e != hipSuccess) return hip_fail(e, "expert down kernel launch");
+    e = moe::launch_combine(y, residual, T, d, k, out, out_f32, stream);
+    if (e != hipSuccess) return hip_fail(e, "combine kernel launch");
+    return ok();
+}
+
+ExpertWeights bf16_weights(const moe_bf16_t* w1, const moe_bf16_t* w3, const moe_bf16_t* w2)
+{
+    ExpertWeights w;
+    w.w1 = w1, w.w3 = w3, w.w2 = w2;
+    return w;
+}
+
+// the format is fixed by the entry point, not by which pointers are NULL, so
+// a NULL byte array is reported as such
+ExpertWeights fp8_weights(const uint8_t* q1, const float* s1, const uint8_t* q3, const float* s3,
+                          const uint8_t* q2, const float* s2)
+{
+    ExpertWeights w;
+    w.q1 = q1, w.s1 = s1, w.q3 = q3, w.s3 = s3, w.q2 = q2, w.s2 = s2;
+    w.f8 = true;
+    return w;
+}
+
+}  // namespace
 
 extern "C" {
 
@@ -275,26 +502,8 @@ moe_status_t moe_swiglu_up(const moe_bf16_t* x_perm, const int32_t* perm,
                            const moe_bf16_t* w3, int64_t T, int32_t d, int32_t ffn, int32_t E,
                            int32_t k, moe_bf16_t* h, hipStream_t stream)
 {
-    TRY(check_Ek(E, k));
-    TRY(check_T(T, k));
-    TRY(check_dim("d", d));
-    TRY(check_dim("ffn", ffn));
-    TRY(need_rows(x_perm, "x_perm", T));
-    TRY(need(expert_offsets, "expert_offsets"));
-    TRY(need(w1, "w1"));
-    TRY(need(w3, "w3"));
-    TRY(need_rows(h, "h", T));
-    TRY(maybe(perm, "perm"));
-    const size_t A = static_cast<size_t>(T) * k;
-    const size_t wbytes = (size_t)E * ffn * d * 2;
-    const size_t xrows = perm ? static_cast<size_t>(T) : A;
-    TRY(no_overlap("h", {h, A * ffn * 2}, {{"x", {x_perm, xrows * d * 2}}, {"w1", {w1, wbytes}},
-                   {"w3", {w3, wbytes}}, {"expert_offsets", {expert_offsets, (size_t)(E + 1) * 4}},
-                   {"perm", {perm, A * 4}}}));
-    if (T == 0) return ok();
-    moe::UpArgs a{x_perm, perm, k, expert_offsets, w1, w3, h, (int64_t)A, d, ffn, E};
-    hipError_t e = run_up(a, T, stream);
-    return e == hipSuccess ? ok() : hip_fail(e, "expert up kernel launch");
+    return swiglu_up_impl(x_perm, perm, expert_offsets, bf16_weights(w1, w3, nullptr), T, d, ffn,
+                          E, k, h, stream);
 }
 
 moe_status_t moe_swiglu_down(const moe_bf16_t* h, const int32_t* expert_offsets,
@@ -302,26 +511,29 @@ moe_status_t moe_swiglu_down(const moe_bf16_t* h, const int32_t* expert_offsets,
                              int64_t T, int32_t d, int32_t ffn, int32_t E, int32_t k, float* y,
                              hipStream_t stream)
 {
-    TRY(check_Ek(E, k));
-    TRY(check_T(T, k));
-    TRY(check_dim("d", d));
-    TRY(check_dim("ffn", ffn));
-    TRY(need_rows(h, "h", T));
-    TRY(need(expert_offsets, "expert_offsets"));
-    TRY(need(w2, "w2"));
-    TRY(maybe(topk_w, "topk_w"));
-    TRY(maybe(perm, "perm"));
-    TRY(need_rows(y, "y", T));
-    const size_t A = static_cast<size_t>(T) * k;
-    TRY(no_overlap("y", {y, A * d * 4}, {{"h", {h, A * ffn * 2}}, {"w2", {w2, (size_t)E * d * ffn * 2}},
-                   {"topk_w", {topk_w, A * 4}}, {"perm", {perm, A * 4}},
-                   {"expert_offsets", {expert_offsets, (size_t)(E + 1) * 4}}}));
-    if (T == 0) return ok();
-    const bool scatter = topk_w && perm;
-    moe::DownArgs a{h, expert_offsets, w2, scatter ? topk_w : nullptr, scatter ? perm : nullptr,
-                    y, (int64_t)A, d, ffn, E};
-    hipError_t e = run_down(a, T, k, stream);
-    return e == hipSuccess ? ok() : hip_fail(e, "expert down kernel launch");
+    return swiglu_down_impl(h, expert_offsets, bf16_weights(nullptr, nullptr, w2), topk_w, perm,
+                            T, d, ffn, E, k, y, stream);
+}
+
+moe_status_t moe_swiglu_up_fp8(const moe_bf16_t* x_perm, const int32_t* perm,
+                               const int32_t* expert_offsets, const uint8_t* w1q,
+                               const float* w1s, const uint8_t* w3q, const float* w3s, int64_t T,
+                               int32_t d, int32_t ffn, int32_t E, int32_t k, moe_bf16_t* h,
+                               hipStream_t stream)
+{
+    return swiglu_up_impl(x_perm, perm, expert_offsets,
+                          fp8_weights(w1q, w1s, w3q, w3s, nullptr, nullptr), T, d, ffn, E, k, h,
+                          stream);
+}
+
+moe_status_t moe_swiglu_down_fp8(const moe_bf16_t* h, const int32_t* expert_offsets,
+                                 const uint8_t* w2q, const float* w2s, const float* topk_w,
+                                 const int32_t* perm, int64_t T, int32_t d, int32_t ffn, int32_t E,
+                                 int32_t k, float* y, hipStream_t stream)
+{
+    return swiglu_down_impl(h, expert_offsets,
+                            fp8_weights(nullptr, nullptr, nullptr, nullptr, w2q, w2s), topk_w,
+                            perm, T, d, ffn, E, k, y, stream);
 }
 
 moe_status_t moe_grouped_swiglu(const moe_bf16_t* x_perm, const int32_t* expert_offsets,
@@ -387,71 +599,20 @@ moe_status_t moe_forward_ex(const moe_bf16_t* x, const moe_bf16_t* router_w,
                             moe_bf16_t* out, float* out_f32, void* workspace,
                             size_t workspace_bytes, hipStream_t stream)
 {
-    TRY(check_Ek(E, k));
-    TRY(check_T(T, k));
-    TRY(check_dim("d", d));
-    TRY(check_dim("ffn", ffn));
-    TRY(need_rows(x, "x", T));
-    TRY(need(router_w, "router_w"));
-    TRY(maybe(router_bias, "router_bias"));
-    TRY(need(w1, "w1"));
-    TRY(need(w3, "w3"));
-    TRY(need(w2, "w2"));
-    TRY(maybe(residual, "residual"));
-    TRY(maybe(out, "out"));
-    TRY(maybe(out_f32, "out_f32"));
-    if (!out && !out_f32 && T > 0)
-        return fail(MOE_ERR_INVALID_ARG, "out and out_f32 are both NULL");
-    if (workspace && (reinterpret_cast<uintptr_t>(workspace) & 255u))
-        return fail(MOE_ERR_INVALID_ARG, "workspace is not 256-byte aligned");
-    const size_t td = static_cast<size_t>(T) * d;
-    const size_t wbytes = (size_t)E * ffn * d * 2;
-    const std::initializer_list<std::pair<const char*, Range>> ins = {
-        {"x", {x, td * 2}}, {"router_w", {router_w, (size_t)E * d * 2}},
-        {"router_bias", {router_bias, (size_t)E * 4}}, {"w1", {w1, wbytes}},
-        {"w3", {w3, wbytes}}, {"w2", {w2, wbytes}}};
-    TRY(no_overlap("out", {out, td * 2}, ins));
-    TRY(no_overlap("out", {out, td * 2}, {{"residual", {residual, td * 4}}, {"out_f32", {out_f32, td * 4}}}));
-    TRY(no_overlap("out_f32", {out_f32, td * 4}, ins));
-    if (residual && out_f32 != residual)
-        TRY(no_overlap("out_f32", {out_f32, td * 4}, {{"residual", {residual, td * 4}}}));
-    const Layout L = layout(T, d, ffn, E, k);
-    if (workspace && workspace_bytes < L.total)
-        return fail(MOE_ERR_NO_MEMORY, "workspace of %zu bytes is smaller than the %zu needed",
-                    workspace_bytes, L.total);
-    if (workspace) {
-        const Range ws{workspace, L.total};
-        TRY(no_overlap("workspace", ws, ins));
-        TRY(no_overlap("workspace", ws, {{"out", {out, td * 2}}, {"out_f32", {out_f32, td * 4}},
-                       {"residual", {residual, td * 4}}}));
-    }
-    if (T == 0) return ok();
+    return forward_impl(x, router_w, router_bias, bf16_weights(w1, w3, w2), T, d, ffn, E, k,
+                        residual, out, out_f32, workspace, workspace_bytes, stream);
+}
 
-    void* base = workspace;
-    if (!base) TRY(library_workspace(L.total, stream, &base));
-    char* b = static_cast<char*>(base);
-    int32_t* ids = reinterpret_cast<int32_t*>(b + L.ids);
-    float* gw = reinterpret_cast<float*>(b + L.w);
-    int32_t* offs = reinterpret_cast<int32_t*>(b + L.off);
-    int32_t* perm = reinterpret_cast<int32_t*>(b + L.perm);
-    moe::bf16_t* h = reinterpret_cast<moe::bf16_t*>(b + L.h);
-    float* y = reinterpret_cast<float*>(b + L.y);
-    const int64_t A = T * k;
-
-    hipError_t e = moe::launch_router_topk(x, router_w, router_bias, T, d, E, k, ids, gw, nullptr,
-                                           stream);
-    if (e != hipSuccess) return hip_fail(e, "router kernel launch");
-    e = moe::launch_dispatch(ids, A, E, offs, perm, stream);
-    if (e != hipSuccess) return hip_fail(e, "dispatch kernel launch");
-    moe::UpArgs ua{x, perm, k, offs, w1, w3, h, A, d, ffn, E};
-    e = run_up(ua, T, stream);
-    if (e != hipSuccess) return hip_fail(e, "expert up kernel launch");
-    moe::DownArgs da{h, offs, w2, gw, perm, y, A, d, ffn, E};
-    e = run_down(da, T, k, stream);
-    if (e != hipSuccess) return hip_fail(e, "expert down kernel launch");
-    e = moe::launch_combine(y, residual, T, d, k, out, out_f32, stream);
-    if (e != hipSuccess) return hip_fail(e, "combine kernel launch");
-    return ok();
+moe_status_t moe_forward_fp8_ex(const moe_bf16_t* x, const moe_bf16_t* router_w,
+                                const float* router_bias, const uint8_t* w1q, const float* w1s,
+                                const uint8_t* w3q, const float* w3s, const uint8_t* w2q,
+                                const float* w2s, int64_t T, int32_t d, int32_t ffn, int32_t E,
+                                int32_t k, const float* residual, moe_bf16_t* out,
+                                float* out_f32, void* workspace, size_t workspace_bytes,
+                                hipStream_t stream)
+{
+    return forward_impl(x, router_w, router_bias, fp8_weights(w1q, w1s, w3q, w3s, w2q, w2s), T, d,
+                        ffn, E, k, residual, out, out_f32, workspace, workspace_bytes, stream);
 }
 
 moe_status_t moe_forward(const moe_bf16_t* x, const moe_bf16_t* router_w, const moe_bf16_t* w1,

@@ -63,6 +63,19 @@ __device__ __forceinline__ bf16x8 as_bf16x8(const uint4& v)
     return __builtin_bit_cast(bf16x8, v);
 }
 
+// Eight OCP FP8 E4M3 values (the bytes of lo, then of hi, in memory order) ->
+// bf16x8.  Exact: every E4M3 value is a bfloat16 value.  The packed
+// conversion results are taken as whole words.
+__device__ __forceinline__ bf16x8 e4m3x8_to_bf16(uint32_t lo, uint32_t hi)
+{
+    uint4 r;
+    r.x = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(lo, 1.0f, false));
+    r.y = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(lo, 1.0f, true));
+    r.z = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(hi, 1.0f, false));
+    r.w = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(hi, 1.0f, true));
+    return __builtin_bit_cast(bf16x8, r);
+}
+
 __device__ __forceinline__ uint4 ldg16(const void* p)
 {
     return *reinterpret_cast<const uint4*>(p);

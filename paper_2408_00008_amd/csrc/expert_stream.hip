@@ -40,6 +40,10 @@ struct StreamParams {
     const int32_t* offsets;  // [E+1]
     const bf16_t* wa;        // UP: w1, DOWN: w2   [E, N, K]
     const bf16_t* wb;        // UP: w3             [E, N, K]
+    const uint8_t* qa;       // 8-bit kernels: E4M3 bytes of wa / wb, [E, N, K]
+    const uint8_t* qb;
+    const float* sa;         // 8-bit kernels: per-row scales of qa / qb, [E, N]
+    const float* sb;
     int N, K;                // weight rows / reduction length per expert
     int E;
     bf16_t* h_out;           // UP   [A, N]
@@ -67,31 +71,43 @@ struct StreamCfg {
     static_assert(!SPLIT || (UP && KS == 1 && NS % 2 == 0), "SPLIT: UP, no K split, even NS");
 };
 
-// Registers of one reduction chunk: the staged token loads and the weight
-// fragments (A operands) of KC/32 MFMA k-steps.
-template <int TPT, int KSTEPS, bool UP>
+// Registers of one reduction chunk: the staged token loads and the raw
+// 16-byte weight loads (A operands): KC/32 MFMA k-steps, one load per k-step
+// in bf16, one per two k-steps in E4M3.
+template <int TPT, int NLOAD, bool TWO>
 struct ChunkRegs {
     uint4 t[TPT];
-    bf16x8 a[KSTEPS];
-    bf16x8 b[UP ? KSTEPS : 1];
+    uint4 a[NLOAD];
+    uint4 b[TWO ? NLOAD : 1];
 };
 
 struct PassCtx {
     int e, n0, row0, m0, Mp, ks, ns, gt, lane, kbeg, nchunks, rot;
     const bf16_t* pa;
     const bf16_t* pb;
+    const uint8_t* qa;  // 8-bit kernels: this lane's weight bytes
+    const uint8_t* qb;
+    const float* sa;    // 8-bit kernels: scales of this wave's weight rows
+    const float* sb;
 };
 
 // One pass over at most 16*GA token rows of expert e for this workgroup's
 // weight rows.  GA is the number of 16-row groups actually computed (a
 // compile-time count, so the MFMA sequence has no data-dependent branches).
-template <bool UP, int NS, int KS, int G, int KC, int GA, bool SPLIT>
+// F8: the weights are E4M3 bytes with per-row scales.  A 16-byte load then
+// holds 16 consecutive reduction elements of a row, which feed two k-steps;
+// the reduction order is permuted accordingly (lane l, k-step 2j + h takes
+// elements 64j + 16 (l / 16) + 8h .. +7) and the token fragments are read in
+// the same order.  The row scales multiply the accumulators.
+template <bool UP, int NS, int KS, int G, int KC, int GA, bool SPLIT, bool F8>
 __device__ __forceinline__ void stream_pass(const StreamParams& p, unsigned char* smem,
                                             const PassCtx& x)
 {
     using C = StreamCfg<UP, NS, KS, G, KC, SPLIT>;
     constexpr bool TWO = UP && !SPLIT;  // two weight matrices per wave
     constexpr int KSTEPS = KC / 32;
+    constexpr int NLOAD = F8 ? KSTEPS / 2 : KSTEPS;
+    static_assert(!F8 || KC % 64 == 0, "E4M3 chunks hold whole 64-element row segments");
     constexpr int GT = 64 * NS;  // threads that stage one token tile
     constexpr int TILE_LOADS = 16 * GA * KC / 8;
     constexpr int TPT = (TILE_LOADS + GT - 1) / GT;
@@ -121,7 +137,7 @@ __device__ __forceinline__ void stream_pass(const StreamParams& p, unsigned char
         accB[g] = floatx4{0.f, 0.f, 0.f, 0.f};
     }
 
-    using R = ChunkRegs<TPT, KSTEPS, TWO>;
+    using R = ChunkRegs<TPT, NLOAD, TWO>;
     auto load = [&](R& r, int c) {
         const int cr = c + x.rot;
         const int ko = (cr < x.nchunks ? cr : cr - x.nchunks) * KC;
@@ -129,9 +145,23 @@ __device__ __forceinline__ void stream_pass(const StreamParams& p, unsigned char
         for (int it = 0; it < TPT; ++it)
             if (ldsoff[it] >= 0) r.t[it] = ldg16(src[it] + ko);
 #pragma unroll
-        for (int kk = 0; kk < KSTEPS; ++kk) {
-            r.a[kk] = as_bf16x8(ldg16(x.pa + ko + kk * 32));
-            if (TWO) r.b[kk] = as_bf16x8(ldg16(x.pb + ko + kk * 32));
+        for (int j = 0; j < NLOAD; ++j) {
+            if constexpr (F8) {
+                r.a[j] = ldg16(x.qa + ko + j * 64);
+                if (TWO) r.b[j] = ldg16(x.qb + ko + j * 64);
+            } else {
+                r.a[j] = ldg16(x.pa + ko + j * 32);
+                if (TWO) r.b[j] = ldg16(x.pb + ko + j * 32);
+            }
+        }
+    };
+    // the A operand of k-step kk
+    auto opnd = [](const uint4* w, int kk) -> bf16x8 {
+        if constexpr (F8) {
+            const uint4 v = w[kk >> 1];
+            return (kk & 1) ? e4m3x8_to_bf16(v.z, v.w) : e4m3x8_to_bf16(v.x, v.y);
+        } else {
+            return as_bf16x8(w[kk]);
         }
     };
     // stage chunk c's tokens, start loading chunk c+1, multiply chunk c.  The
@@ -149,12 +179,16 @@ __device__ __forceinline__ void stream_pass(const StreamParams& p, unsigned char
         __syncthreads();
 #pragma unroll
         for (int kk = 0; kk < KSTEPS; ++kk) {
+            const bf16x8 a = opnd(cur.a, kk);
+            const bf16x8 a2 = TWO ? opnd(cur.b, kk) : a;
+            const int kcol = F8 ? (kk >> 1) * 64 + 16 * (lane >> 4) + 8 * (kk & 1)
+                                : kk * 32 + 8 * (lane >> 4);
 #pragma unroll
             for (int g = 0; g < GA; ++g) {
                 const bf16x8 b = *reinterpret_cast<const bf16x8*>(
-                    tile + (g * 16 + (lane & 15)) * C::LDK + kk * 32 + 8 * (lane >> 4));
-                accA[g] = mfma16x16x32(cur.a[kk], b, accA[g]);
-                if (TWO) accB[g] = mfma16x16x32(cur.b[kk], b, accB[g]);
+                    tile + (g * 16 + (lane & 15)) * C::LDK + kcol);
+                accA[g] = mfma16x16x32(a, b, accA[g]);
+                if (TWO) accB[g] = mfma16x16x32(a2, b, accB[g]);
             }
         }
     };
@@ -195,6 +229,20 @@ __device__ __forceinline__ void stream_pass(const StreamParams& p, unsigned char
                         if (UP) accB[g][i] += sr[((g * 4 + i) * C::NMAT + 1) * 64 + lane];
                     }
                 }
+            }
+        }
+    }
+
+    if constexpr (F8) {
+        // row scales: lane holds output rows n0 + 4 (lane / 16) + i
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const float s1 = x.sa[4 * (lane >> 4) + i];
+            const float s2 = TWO ? x.sb[4 * (lane >> 4) + i] : 0.0f;
+#pragma unroll
+            for (int g = 0; g < GA; ++g) {
+                accA[g][i] *= s1;
+                if (TWO) accB[g][i] *= s2;
             }
         }
     }
@@ -252,7 +300,7 @@ __device__ __forceinline__ void stream_pass(const StreamParams& p, unsigned char
     __syncthreads();
 }
 
-template <bool UP, int NS, int KS, int G, int KC, bool SPLIT>
+template <bool UP, int NS, int KS, int G, int KC, bool SPLIT, bool F8>
 __global__ __launch_bounds__(64 * NS * KS) void stream_kernel(StreamParams p)
 {
     using C = StreamCfg<UP, NS, KS, G, KC, SPLIT>;
@@ -326,7 +374,15 @@ __global__ __launch_bounds__(64 * NS * KS) void stream_kernel(StreamParams p)
     x.rot = static_cast<int>((static_cast<unsigned>(e * (nbn8 >> 3) + grp) * 5u) %
                              static_cast<unsigned>(x.nchunks));
     const int64_t wrow = (int64_t)e * p.N + x.n0 + (x.lane & 15);
-    if (SPLIT) {
+    const int64_t srow = (int64_t)e * p.N + x.n0;  // first row of this wave's 16
+    if constexpr (F8) {
+        const bool w3 = SPLIT && x.ns >= NS / 2;
+        x.qa = (w3 ? p.qb : p.qa) + wrow * p.K + x.kbeg + 16 * (x.lane >> 4);
+        x.qb = (UP && !SPLIT) ? p.qb + wrow * p.K + x.kbeg + 16 * (x.lane >> 4) : nullptr;
+        x.sa = (w3 ? p.sb : p.sa) + srow;
+        x.sb = (UP && !SPLIT) ? p.sb + srow : nullptr;
+        x.pa = x.pb = nullptr;
+    } else if (SPLIT) {
         x.pa = (x.ns < NS / 2 ? p.wa : p.wb) + wrow * p.K + x.kbeg + 8 * (x.lane >> 4);
         x.pb = nullptr;
     } else {
@@ -339,20 +395,20 @@ __global__ __launch_bounds__(64 * NS * KS) void stream_kernel(StreamParams p)
         x.Mp = min(M - x.m0, rp);
         const int gact = (x.Mp + 15) >> 4;
         if (gact <= 1) {
-            stream_pass<UP, NS, KS, G, KC, 1, SPLIT>(p, smem, x);
+            stream_pass<UP, NS, KS, G, KC, 1, SPLIT, F8>(p, smem, x);
         } else if (gact <= 2) {
-            if constexpr (G >= 2) stream_pass<UP, NS, KS, G, KC, 2, SPLIT>(p, smem, x);
+            if constexpr (G >= 2) stream_pass<UP, NS, KS, G, KC, 2, SPLIT, F8>(p, smem, x);
         } else if (gact <= 4) {
-            if constexpr (G >= 4) stream_pass<UP, NS, KS, G, KC, 4, SPLIT>(p, smem, x);
+            if constexpr (G >= 4) stream_pass<UP, NS, KS, G, KC, 4, SPLIT, F8>(p, smem, x);
         } else if (gact <= 8) {
-            if constexpr (G >= 8) stream_pass<UP, NS, KS, G, KC, 8, SPLIT>(p, smem, x);
+            if constexpr (G >= 8) stream_pass<UP, NS, KS, G, KC, 8, SPLIT, F8>(p, smem, x);
         } else {
-            if constexpr (G >= 16) stream_pass<UP, NS, KS, G, KC, 16, SPLIT>(p, smem, x);
+            if constexpr (G >= 16) stream_pass<UP, NS, KS, G, KC, 16, SPLIT, F8>(p, smem, x);
         }
     }
 }
 
-template <bool UP, int NS, int KS, int G, int KC, bool SPLIT = false>
+template <bool UP, int NS, int KS, int G, int KC, bool SPLIT = false, bool F8 = false>
 hipError_t run(StreamParams p, int64_t rows_max, hipStream_t stream)
 {
     // pass slots per slab: enough for an expert that takes rows_max rows
@@ -363,7 +419,7 @@ hipError_t run(StreamParams p, int64_t rows_max, hipStream_t stream)
     using C = StreamCfg<UP, NS, KS, G, KC, SPLIT>;
     const int nbn8 = (p.N / C::ROWS + 7) & ~7;
     const unsigned grid = static_cast<unsigned>(p.E * nbn8 * p.passes);
-    stream_kernel<UP, NS, KS, G, KC, SPLIT><<<grid, C::THREADS, 0, stream>>>(p);
+    stream_kernel<UP, NS, KS, G, KC, SPLIT, F8><<<grid, C::THREADS, 0, stream>>>(p);
     return hipGetLastError();
 }
 
@@ -389,17 +445,39 @@ hipError_t launch_stream_up(const UpArgs& a, int64_t rows_max, hipStream_t strea
     p.offsets = a.offsets;
     p.wa = a.w1;
     p.wb = a.w3;
+    p.qa = a.q1;
+    p.qb = a.q3;
+    p.sa = a.s1;
+    p.sb = a.s3;
     p.N = a.ffn;
     p.K = a.d;
     p.E = a.E;
     p.h_out = a.h;
+    const int G = stream_groups(a.A, a.E);
     // 8 waves: 4 stream w1 rows, 4 the same w3 rows (SPLIT)
-    if (stream_groups(a.A, a.E) == 2) {
+    if (a.q1) {
+        // E4M3 rows are half as many bytes: chunks twice as long hold the
+        // same bytes in flight with the same registers
+        if (G == 2) {
+            if (a.d % 512 == 0) return run<true, 8, 1, 2, 512, true, true>(p, rows_max, stream);
+            if (a.d % 256 == 0) return run<true, 8, 1, 2, 256, true, true>(p, rows_max, stream);
+            if (a.d % 128 == 0) return run<true, 8, 1, 2, 128, true, true>(p, rows_max, stream);
+            return run<true, 8, 1, 2, 64, true, true>(p, rows_max, stream);
+        }
+        if (G == 8) {
+            if (a.d % 128 == 0) return run<true, 8, 1, 8, 128, true, true>(p, rows_max, stream);
+            return run<true, 8, 1, 8, 64, true, true>(p, rows_max, stream);
+        }
+        if (a.d % 256 == 0) return run<true, 8, 1, 4, 256, true, true>(p, rows_max, stream);
+        if (a.d % 128 == 0) return run<true, 8, 1, 4, 128, true, true>(p, rows_max, stream);
+        return run<true, 8, 1, 4, 64, true, true>(p, rows_max, stream);
+    }
+    if (G == 2) {
         if (a.d % 256 == 0) return run<true, 8, 1, 2, 256, true>(p, rows_max, stream);
         if (a.d % 128 == 0) return run<true, 8, 1, 2, 128, true>(p, rows_max, stream);
         return run<true, 8, 1, 2, 64, true>(p, rows_max, stream);
     }
-    if (stream_groups(a.A, a.E) == 8) return run<true, 8, 1, 8, 64, true>(p, rows_max, stream);
+    if (G == 8) return run<true, 8, 1, 8, 64, true>(p, rows_max, stream);
     if (a.d % 128 == 0) return run<true, 8, 1, 4, 128, true>(p, rows_max, stream);
     return run<true, 8, 1, 4, 64, true>(p, rows_max, stream);
 }
@@ -410,13 +488,28 @@ hipError_t launch_stream_down(const DownArgs& a, int64_t rows_max, hipStream_t s
     p.act = a.h;
     p.offsets = a.offsets;
     p.wa = a.w2;
+    p.qa = a.q2;
+    p.sa = a.s2;
     p.N = a.d;
     p.K = a.ffn;
     p.E = a.E;
     p.y_out = a.y;
     p.topk_w = a.topk_w;
     p.perm = a.perm;
-    if (stream_groups(a.A, a.E) == 2) {
+    const int G = stream_groups(a.A, a.E);
+    if (a.q2) {
+        if (G == 2) {
+            if (a.d % 128 == 0 && a.ffn % 256 == 0)
+                return run<false, 8, 1, 2, 256, false, true>(p, rows_max, stream);
+            if (a.d % 128 == 0 && a.ffn % 128 == 0)
+                return run<false, 8, 1, 2, 128, false, true>(p, rows_max, stream);
+            return run<false, 4, 1, 2, 64, false, true>(p, rows_max, stream);
+        }
+        if (a.ffn % 256 == 0) return run<false, 4, 1, 4, 256, false, true>(p, rows_max, stream);
+        if (a.ffn % 128 == 0) return run<false, 4, 1, 4, 128, false, true>(p, rows_max, stream);
+        return run<false, 4, 1, 4, 64, false, true>(p, rows_max, stream);
+    }
+    if (G == 2) {
         if (a.d % 128 == 0 && a.ffn % 128 == 0) return run<false, 8, 1, 2, 128>(p, rows_max, stream);
         return run<false, 4, 1, 2, 64>(p, rows_max, stream);
     }

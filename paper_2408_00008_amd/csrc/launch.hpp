@@ -42,6 +42,12 @@ struct UpArgs {
     bf16_t* h;               // [A,ffn]
     int64_t A;
     int d, ffn, E;
+    // 8-bit weights (then w1/w3 are unused): E4M3 bytes [E,ffn,d] and per-row
+    // scales [E,ffn]
+    const uint8_t* q1 = nullptr;
+    const float* s1 = nullptr;
+    const uint8_t* q3 = nullptr;
+    const float* s3 = nullptr;
 };
 
 struct DownArgs {
@@ -53,6 +59,9 @@ struct DownArgs {
     float* y;                // [A,d]
     int64_t A;
     int d, ffn, E;
+    // 8-bit weights (then w2 is unused): E4M3 bytes [E,d,ffn], scales [E,d]
+    const uint8_t* q2 = nullptr;
+    const float* s2 = nullptr;
 };
 
 enum GemmVariant { VARIANT_AUTO = 0, VARIANT_STREAM = 1, VARIANT_TILED = 2 };

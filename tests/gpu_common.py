@@ -131,3 +131,69 @@ def oracle_out(c: Case, rows, gpu_ids_rows=None):
         gates = o.gates_for_ids(logits, ids)
     out = o.moe_apply(x, c.bits("w1"), c.bits("w3"), c.bits("w2"), ids, gates)
     return out, logits, ids, gates
+
+
+# ---- 8-bit expert weights ----------------------------------------------------
+
+class Fp8Case:
+    """A layer with E4M3 expert weights (per-row f32 scales) on the GPU."""
+
+    def __init__(self, w: "inputs.Workload", name):
+        lay = inputs.make_layer_fp8(w, 0, DEV)
+        self.T, self.d, self.ffn, self.E, self.k = w.T, w.d, w.ffn, w.E, w.k
+        self.name = name
+        self.x = inputs.make_x(w, DEV)
+        self.router_w, self.router_bias = lay["router_w"], lay["router_bias"]
+        for n in ("w1q", "w1s", "w3q", "w3s", "w2q", "w2s"):
+            setattr(self, n, lay[n])
+        self._host = {}
+
+    def host(self, name):
+        """Host copy: bf16 tensors as uint16 bits, the rest as numpy arrays."""
+        if name not in self._host:
+            t = getattr(self, name)
+            self._host[name] = inputs.bf16_bits(t) if t.dtype == torch.bfloat16 else t.cpu().numpy()
+        return self._host[name]
+
+    @property
+    def bias_np(self):
+        return None if self.router_bias is None else self.router_bias.cpu().numpy()
+
+    def weights(self):
+        return [self.host(n) for n in ("w1q", "w1s", "w3q", "w3s", "w2q", "w2s")]
+
+
+def fp8_workload_case(name, seed=0) -> Fp8Case:
+    return Fp8Case(inputs.WORKLOADS[name].replace(seed=seed), name)
+
+
+def fp8_small_case(T, d, ffn, E, k, seed=0, bias=None) -> Fp8Case:
+    std_w = 1.0 / np.sqrt(d)
+    w = inputs.Workload("small", T, d, ffn, E, k, 1.0, std_w, std_w, std_w, 1.0 / np.sqrt(ffn),
+                        seed=seed, fp8=True)
+    c = Fp8Case(w, f"fp8small{T}x{d}x{ffn}x{E}k{k}")
+    if bias is not None:
+        c.router_bias = torch.tensor(bias, dtype=torch.float32, device=DEV)
+    return c
+
+
+def gpu_forward_fp8(c: Fp8Case, out_f32=False):
+    out = torch.empty(c.T, c.d, dtype=torch.bfloat16, device=DEV)
+    of = torch.empty(c.T, c.d, dtype=torch.float32, device=DEV) if out_f32 else None
+    B.moe_forward_fp8_ex(c.x, c.router_w, c.w1q, c.w1s, c.w3q, c.w3s, c.w2q, c.w2s, c.k, out=out,
+                         out_f32=of, router_bias=c.router_bias)
+    torch.cuda.synchronize()
+    return (out, of) if out_f32 else out
+
+
+def oracle_out_fp8(c: Fp8Case, rows, gpu_ids_rows=None):
+    """As oracle_out, for the 8-bit weights."""
+    o = orc()
+    x = c.host("x")[rows]
+    logits = o.router_logits(x, c.host("router_w"), c.bias_np)
+    ids, gates = o.topk_gate(logits, c.k)
+    if gpu_ids_rows is not None:
+        ids = np.ascontiguousarray(gpu_ids_rows, dtype=np.int32)
+        gates = o.gates_for_ids(logits, ids)
+    out = o.moe_apply_fp8(x, *c.weights(), ids, gates)
+    return out, logits, ids, gates

@@ -142,3 +142,34 @@ def test_variant_switch(L):
     assert L.moe_set_gemm_variant(2) == 1
     assert L.moe_set_gemm_variant(7) == -1
     assert L.moe_set_gemm_variant(prev) == 2
+
+
+def test_fp8_entry_points_reject(L):
+    """8-bit weight calls: byte arrays and scales are required and 16-byte
+    aligned, outputs may not overlap them, T = 0 is a no-op."""
+    big = 1 << 40
+    q1, s1, q3, s3, q2, s2 = (big * (i + 1) for i in range(6))
+    out = 7 * big
+
+    def fwd8(**kw):
+        a = dict(x=X, rw=RW, q1=q1, s1=s1, q3=q3, s3=s3, q2=q2, s2=s2, T=4, out=out)
+        a.update(kw)
+        return L.moe_forward_fp8_ex(a["x"], a["rw"], None, a["q1"], a["s1"], a["q3"], a["s3"],
+                                    a["q2"], a["s2"], a["T"], 128, 256, 8, 2, None, a["out"],
+                                    None, None, 0, None)
+
+    assert fwd8(s1=0) == B.MOE_ERR_INVALID_ARG and b"w1s is NULL" in L.moe_last_error()
+    assert fwd8(q2=0) == B.MOE_ERR_INVALID_ARG and b"w2q is NULL" in L.moe_last_error()
+    assert fwd8(q3=q3 + 8) == B.MOE_ERR_INVALID_ARG and b"w3q" in L.moe_last_error()
+    assert fwd8(s2=s2 + 4) == B.MOE_ERR_INVALID_ARG and b"w2s" in L.moe_last_error()
+    assert fwd8(out=s3 + 64) == B.MOE_ERR_INVALID_ARG and b"overlaps w3s" in L.moe_last_error()
+    assert fwd8(T=0) == B.MOE_OK
+    # up: h overlapping a scale array; down: y overlapping the byte array
+    st = L.moe_swiglu_up_fp8(X, None, 0x700000, q1, s1, q3, s3, 4, 128, 256, 8, 2, s1 + 16, None)
+    assert st == B.MOE_ERR_INVALID_ARG and b"overlaps w1s" in L.moe_last_error()
+    st = L.moe_swiglu_down_fp8(X, 0x700000, q2, s2, None, None, 4, 128, 256, 8, 2, q2 + 256, None)
+    assert st == B.MOE_ERR_INVALID_ARG and b"overlaps w2q" in L.moe_last_error()
+    st = L.moe_swiglu_down_fp8(X, 0x700000, None, s2, None, None, 4, 128, 256, 8, 2, out, None)
+    assert st == B.MOE_ERR_INVALID_ARG and b"w2q is NULL" in L.moe_last_error()
+    assert L.moe_swiglu_up_fp8(None, None, 0x700000, q1, s1, q3, s3, 0, 128, 256, 8, 2, None,
+                               None) == B.MOE_OK

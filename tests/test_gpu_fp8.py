@@ -1,0 +1,138 @@
+"""GPU parity of the 8-bit expert weight path (E4M3 bytes, one f32 scale per
+weight row; Sec. 4.1 "Model Quantization", Sec. 5's 8-bit Mixtral) against
+the fp64 oracle on the same bytes and scales.
+
+The kernels convert each E4M3 byte exactly to a bf16 operand and scale each
+row's f32 sum, so the error budget is that of the bf16 path: the same
+row-wise relative tolerance and routing rule apply."""
+
+import numpy as np
+import pytest
+import torch
+
+from gpu_common import (DEV, bf16_to_f64, fp8_small_case, fp8_workload_case, gpu_forward_fp8,
+                        gpu_route, orc, oracle_out_fp8, say)
+from parity import OUT_TOL, check_routing, rowwise_rel
+from paper_2408_00008_amd import binding as B
+
+pytestmark = pytest.mark.gpu
+
+
+def _forward_check(c, rows=None):
+    out = gpu_forward_fp8(c)
+    ids, *_ = gpu_route(c)
+    rows = np.arange(c.T) if rows is None else np.asarray(rows)
+    g_ids = ids.cpu().numpy()
+    ref, logits, *_ = oracle_out_fp8(c, rows, g_ids[rows])
+    check_routing(g_ids[rows], logits, c.k)
+    err = rowwise_rel(bf16_to_f64(out)[rows], ref)
+    say(f"  {c.name} T={c.T}: rowwise rel {err:.3e} over {len(rows)} tokens")
+    assert err < OUT_TOL
+    return out
+
+
+@pytest.mark.parametrize("shape", [(16, 256, 512, 8, 2), "decode_t64_fp8"])
+def test_fp8_stages_teacher_forced(shape):
+    """up/down fed the oracle's routing; h and y compared slot by slot, with
+    and without the fused gather and the fused gate-weighted scatter."""
+    c = fp8_workload_case(shape) if isinstance(shape, str) else fp8_small_case(*shape, seed=3)
+    say(f"[fp8 stages] {c.name}")
+    o = orc()
+    x = c.host("x")
+    logits = o.router_logits(x, c.host("router_w"), c.bias_np)
+    ids, gates = o.topk_gate(logits, c.k)
+    _, offs, perm = o.dispatch(ids, c.E)
+    _, h_ref, y_ref = o.moe_apply_fp8(x, *c.weights(), ids, gates, want_slots=True)
+    A = c.T * c.k
+    d_offs = torch.from_numpy(offs).to(DEV)
+    d_perm = torch.from_numpy(perm).to(DEV)
+    d_gw = torch.from_numpy(gates.astype(np.float32).reshape(-1)).to(DEV)
+    h = torch.empty(A, c.ffn, dtype=torch.bfloat16, device=DEV)
+    B.moe_swiglu_up_fp8(c.x, d_offs, c.w1q, c.w1s, c.w3q, c.w3s, c.T, c.k, h, perm=d_perm)
+    xp = torch.empty(A, c.d, dtype=torch.bfloat16, device=DEV)
+    B.moe_permute(c.x, d_perm, c.k, xp)
+    h_np = torch.empty_like(h)
+    B.moe_swiglu_up_fp8(xp, d_offs, c.w1q, c.w1s, c.w3q, c.w3s, c.T, c.k, h_np)
+    y = torch.empty(A, c.d, dtype=torch.float32, device=DEV)
+    B.moe_swiglu_down_fp8(h, d_offs, c.w2q, c.w2s, c.T, c.k, y, topk_w=d_gw, perm=d_perm)
+    y_plain = torch.empty_like(y)
+    B.moe_swiglu_down_fp8(h, d_offs, c.w2q, c.w2s, c.T, c.k, y_plain)
+    torch.cuda.synchronize()
+    # the gathered and the pre-permuted token rows are the same bits
+    assert torch.equal(h, h_np)
+    e_h = rowwise_rel(bf16_to_f64(h), h_ref[perm])
+    e_y = rowwise_rel(y.cpu().numpy(), y_ref * gates.reshape(-1, 1))
+    e_yp = rowwise_rel(y_plain.cpu().numpy(), y_ref[perm])
+    say(f"  rowwise rel: h {e_h:.2e} y {e_y:.2e} y_plain {e_yp:.2e}")
+    assert e_h < OUT_TOL and e_y < OUT_TOL and e_yp < OUT_TOL
+
+
+def test_fp8_forward_full():
+    say("[fp8 forward] decode_t64_fp8 (every token)")
+    _forward_check(fp8_workload_case("decode_t64_fp8"))
+
+
+def test_fp8_forward_skew_sampled():
+    say("[fp8 forward] decode_t256_skew_fp8 (sampled tokens)")
+    c = fp8_workload_case("decode_t256_skew_fp8")
+    rng = np.random.default_rng(12)
+    rows = np.unique(np.concatenate([[0, c.T - 1], rng.choice(c.T, 30, replace=False)]))
+    _forward_check(c, rows)
+
+
+@pytest.mark.parametrize("shape", [
+    (1, 64, 64, 1, 1),        # single token, single expert
+    (37, 192, 320, 8, 2),     # ragged T, d/ffn not multiples of 128
+    (5, 128, 128, 4, 4),      # k = E
+    (300, 128, 192, 64, 8),   # E = 64, k = 8 limits
+    (513, 256, 512, 8, 2),    # rows per expert > 64
+    (200, 256, 256, 8, 2),    # 33..64 rows per expert
+    (96, 1024, 512, 8, 2),    # d a multiple of 512 (the longest up chunks)
+])
+def test_fp8_forward_shapes(shape):
+    say(f"[fp8 forward] shape {shape}")
+    _forward_check(fp8_small_case(*shape, seed=13))
+
+
+def test_fp8_forward_heavy_expert():
+    """Every token on expert 0: more passes than a slab has pass slots."""
+    say("[fp8 forward] heavy expert")
+    c = fp8_small_case(700, 256, 256, 4, 2, seed=21, bias=[60.0, 0.0, 0.0, 0.0])
+    _, _, offs, _, _ = gpu_route(c)
+    o = offs.cpu().numpy()
+    assert o[1] - o[0] == c.T
+    _forward_check(c)
+
+
+def test_fp8_deterministic():
+    c = fp8_small_case(64, 512, 512, 8, 2, seed=5)
+    a = gpu_forward_fp8(c)
+    b = gpu_forward_fp8(c)
+    assert torch.equal(a, b)
+
+
+def test_fp8_nan_byte_reaches_only_its_expert():
+    """An E4M3 NaN byte in one w1 row of expert e turns exactly the tokens
+    routed to e into NaN; every other token still matches the oracle."""
+    say("[fp8] NaN byte")
+    c = fp8_small_case(48, 128, 256, 8, 2, seed=9)
+    ids, *_ = gpu_route(c)
+    g_ids = ids.cpu().numpy()
+    e = int(np.bincount(g_ids.reshape(-1), minlength=c.E).argmax())
+    c.w1q[e, 7, 33] = 0x7F
+    c._host.pop("w1q", None)
+    out = gpu_forward_fp8(c).float().cpu().numpy()
+    hit = (g_ids == e).any(axis=1)
+    assert hit.any() and (~hit).any()
+    assert np.isnan(out[hit]).all()
+    rows = np.nonzero(~hit)[0]
+    assert np.isfinite(out[rows]).all()
+    ref, *_ = oracle_out_fp8(c, rows, g_ids[rows])
+    assert rowwise_rel(out[rows].astype(np.float64), ref) < OUT_TOL
+
+
+def test_fp8_t0():
+    c = fp8_small_case(3, 64, 64, 4, 2)
+    out = torch.zeros(0, 64, dtype=torch.bfloat16, device=DEV)
+    B.moe_forward_fp8_ex(c.x[:0], c.router_w, c.w1q, c.w1s, c.w3q, c.w3s, c.w2q, c.w2s, 2, out=out)
+    torch.cuda.synchronize()
