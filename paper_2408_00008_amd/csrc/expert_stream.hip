@@ -71,12 +71,11 @@ struct StreamCfg {
     static_assert(!SPLIT || (UP && KS == 1 && NS % 2 == 0), "SPLIT: UP, no K split, even NS");
 };
 
-// Registers of one reduction chunk: the staged token loads and the raw
-// 16-byte weight loads (A operands): KC/32 MFMA k-steps, one load per k-step
-// in bf16, one per two k-steps in E4M3.
-template <int TPT, int NLOAD, bool TWO>
+// Weight registers of one reduction chunk: the raw 16-byte loads that are
+// the A operands of KC/32 MFMA k-steps, one load per k-step in bf16, one per
+// two k-steps in E4M3.
+template <int NLOAD, bool TWO>
 struct ChunkRegs {
-    uint4 t[TPT];
     uint4 a[NLOAD];
     uint4 b[TWO ? NLOAD : 1];
 };
@@ -99,7 +98,9 @@ struct PassCtx {
 // the reduction order is permuted accordingly (lane l, k-step 2j + h takes
 // elements 64j + 16 (l / 16) + 8h .. +7) and the token fragments are read in
 // the same order.  The row scales multiply the accumulators.
-template <bool UP, int NS, int KS, int G, int KC, int GA, bool SPLIT, bool F8>
+// ST weight register sets: chunk c is multiplied while the weights of chunks
+// c+1 .. c+ST-1 are in flight (the token tile is always one chunk ahead).
+template <bool UP, int NS, int KS, int G, int KC, int GA, bool SPLIT, bool F8, int ST>
 __device__ __forceinline__ void stream_pass(const StreamParams& p, unsigned char* smem,
                                             const PassCtx& x)
 {
@@ -108,6 +109,7 @@ __device__ __forceinline__ void stream_pass(const StreamParams& p, unsigned char
     constexpr int KSTEPS = KC / 32;
     constexpr int NLOAD = F8 ? KSTEPS / 2 : KSTEPS;
     static_assert(!F8 || KC % 64 == 0, "E4M3 chunks hold whole 64-element row segments");
+    static_assert(ST == 2 || ST == 3, "two or three weight register sets");
     constexpr int GT = 64 * NS;  // threads that stage one token tile
     constexpr int TILE_LOADS = 16 * GA * KC / 8;
     constexpr int TPT = (TILE_LOADS + GT - 1) / GT;
@@ -137,13 +139,23 @@ __device__ __forceinline__ void stream_pass(const StreamParams& p, unsigned char
         accB[g] = floatx4{0.f, 0.f, 0.f, 0.f};
     }
 
-    using R = ChunkRegs<TPT, NLOAD, TWO>;
-    auto load = [&](R& r, int c) {
+    using R = ChunkRegs<NLOAD, TWO>;
+    uint4 tok[TPT];
+    // chunk c starts at column (c + rot) mod nchunks of the slab; c is clamped
+    // to the last chunk, whose loads then repeat (see step)
+    auto kofs = [&](int c) {
+        c = c < x.nchunks ? c : x.nchunks - 1;
         const int cr = c + x.rot;
-        const int ko = (cr < x.nchunks ? cr : cr - x.nchunks) * KC;
+        return (cr < x.nchunks ? cr : cr - x.nchunks) * KC;
+    };
+    auto load_t = [&](int c) {
+        const int ko = kofs(c);
 #pragma unroll
         for (int it = 0; it < TPT; ++it)
-            if (ldsoff[it] >= 0) r.t[it] = ldg16(src[it] + ko);
+            if (ldsoff[it] >= 0) tok[it] = ldg16(src[it] + ko);
+    };
+    auto load_w = [&](R& r, int c) {
+        const int ko = kofs(c);
 #pragma unroll
         for (int j = 0; j < NLOAD; ++j) {
             if constexpr (F8) {
@@ -164,18 +176,24 @@ __device__ __forceinline__ void stream_pass(const StreamParams& p, unsigned char
             return as_bf16x8(w[kk]);
         }
     };
-    // stage chunk c's tokens, start loading chunk c+1, multiply chunk c.  The
-    // load is unconditional (the last chunk re-reads itself) so that the
-    // compiler's memory-counter waits stay exact and the loads of chunk c+1
-    // remain in flight while chunk c is multiplied.  Chunk c's tile is the
-    // one chunk c-2 read; every wave finished those reads before it reached
-    // chunk c-1's barrier, so one barrier per chunk suffices.
-    auto step = [&](int c, R& cur, R& nxt) {
+    // Stage chunk c's tokens, load chunk c+1's tokens and chunk c+ST-1's
+    // weights (into the set chunk c-1 used), multiply chunk c.  The loads are
+    // unconditional (past the last chunk they repeat it) so that the
+    // compiler's memory-counter waits stay exact; they retire in issue order,
+    // so waiting for chunk c's tokens (issued after chunk c's weights and
+    // before chunk c+1's) leaves chunks c+1 .. c+ST-1 in flight.  Chunk c's
+    // tile is the one chunk c-2 read; every wave finished those reads before
+    // it reached chunk c-1's barrier, so one barrier per chunk suffices.
+    auto step = [&](int c, R& cur, R& ahead) {
         bf16_t* tile = tiles + (c & 1) * C::MT * C::LDK;
 #pragma unroll
         for (int it = 0; it < TPT; ++it)
-            if (ldsoff[it] >= 0) *reinterpret_cast<uint4*>(tile + ldsoff[it]) = cur.t[it];
-        load(nxt, c + 1 < x.nchunks ? c + 1 : c);
+            if (ldsoff[it] >= 0) *reinterpret_cast<uint4*>(tile + ldsoff[it]) = tok[it];
+        load_t(c + 1);
+        load_w(ahead, c + ST - 1);
+        // E4M3: keep the first conversion (which waits for this chunk's
+        // weights) below the new loads, or fewer chunks would be in flight
+        if constexpr (F8) __builtin_amdgcn_sched_barrier(0);
         __syncthreads();
 #pragma unroll
         for (int kk = 0; kk < KSTEPS; ++kk) {
@@ -193,12 +211,22 @@ __device__ __forceinline__ void stream_pass(const StreamParams& p, unsigned char
         }
     };
 
-    R r0, r1;
-    load(r0, 0);
+    R r0, r1, r2;
+    load_t(0);
+    load_w(r0, 0);
+    if constexpr (ST == 3) load_w(r1, 1);
     __syncthreads();  // the previous pass (or reduction) is done with the LDS
-    for (int c = 0; c < x.nchunks; c += 2) {
-        step(c, r0, r1);
-        if (c + 1 < x.nchunks) step(c + 1, r1, r0);
+    if constexpr (ST == 2) {
+        for (int c = 0; c < x.nchunks; c += 2) {
+            step(c, r0, r1);
+            if (c + 1 < x.nchunks) step(c + 1, r1, r0);
+        }
+    } else {
+        for (int c = 0; c < x.nchunks; c += 3) {
+            step(c, r0, r2);
+            if (c + 1 < x.nchunks) step(c + 1, r1, r0);
+            if (c + 2 < x.nchunks) step(c + 2, r2, r1);
+        }
     }
 
     if (KS > 1) {
@@ -300,7 +328,7 @@ __device__ __forceinline__ void stream_pass(const StreamParams& p, unsigned char
     __syncthreads();
 }
 
-template <bool UP, int NS, int KS, int G, int KC, bool SPLIT, bool F8>
+template <bool UP, int NS, int KS, int G, int KC, bool SPLIT, bool F8, int ST>
 __global__ __launch_bounds__(64 * NS * KS) void stream_kernel(StreamParams p)
 {
     using C = StreamCfg<UP, NS, KS, G, KC, SPLIT>;
@@ -395,20 +423,20 @@ __global__ __launch_bounds__(64 * NS * KS) void stream_kernel(StreamParams p)
         x.Mp = min(M - x.m0, rp);
         const int gact = (x.Mp + 15) >> 4;
         if (gact <= 1) {
-            stream_pass<UP, NS, KS, G, KC, 1, SPLIT, F8>(p, smem, x);
+            stream_pass<UP, NS, KS, G, KC, 1, SPLIT, F8, ST>(p, smem, x);
         } else if (gact <= 2) {
-            if constexpr (G >= 2) stream_pass<UP, NS, KS, G, KC, 2, SPLIT, F8>(p, smem, x);
+            if constexpr (G >= 2) stream_pass<UP, NS, KS, G, KC, 2, SPLIT, F8, ST>(p, smem, x);
         } else if (gact <= 4) {
-            if constexpr (G >= 4) stream_pass<UP, NS, KS, G, KC, 4, SPLIT, F8>(p, smem, x);
+            if constexpr (G >= 4) stream_pass<UP, NS, KS, G, KC, 4, SPLIT, F8, ST>(p, smem, x);
         } else if (gact <= 8) {
-            if constexpr (G >= 8) stream_pass<UP, NS, KS, G, KC, 8, SPLIT, F8>(p, smem, x);
+            if constexpr (G >= 8) stream_pass<UP, NS, KS, G, KC, 8, SPLIT, F8, ST>(p, smem, x);
         } else {
-            if constexpr (G >= 16) stream_pass<UP, NS, KS, G, KC, 16, SPLIT, F8>(p, smem, x);
+            if constexpr (G >= 16) stream_pass<UP, NS, KS, G, KC, 16, SPLIT, F8, ST>(p, smem, x);
         }
     }
 }
 
-template <bool UP, int NS, int KS, int G, int KC, bool SPLIT = false, bool F8 = false>
+template <bool UP, int NS, int KS, int G, int KC, bool SPLIT = false, bool F8 = false, int ST = 2>
 hipError_t run(StreamParams p, int64_t rows_max, hipStream_t stream)
 {
     // pass slots per slab: enough for an expert that takes rows_max rows
@@ -419,7 +447,7 @@ hipError_t run(StreamParams p, int64_t rows_max, hipStream_t stream)
     using C = StreamCfg<UP, NS, KS, G, KC, SPLIT>;
     const int nbn8 = (p.N / C::ROWS + 7) & ~7;
     const unsigned grid = static_cast<unsigned>(p.E * nbn8 * p.passes);
-    stream_kernel<UP, NS, KS, G, KC, SPLIT, F8><<<grid, C::THREADS, 0, stream>>>(p);
+    stream_kernel<UP, NS, KS, G, KC, SPLIT, F8, ST><<<grid, C::THREADS, 0, stream>>>(p);
     return hipGetLastError();
 }
 
@@ -456,10 +484,10 @@ hipError_t launch_stream_up(const UpArgs& a, int64_t rows_max, hipStream_t strea
     const int G = stream_groups(a.A, a.E);
     // 8 waves: 4 stream w1 rows, 4 the same w3 rows (SPLIT)
     if (a.q1) {
-        // E4M3 rows are half as many bytes: chunks twice as long hold the
-        // same bytes in flight with the same registers
+        // E4M3 (sweeps on MI355X): 256-element chunks for up to 32 rows per
+        // pass; 512 would hold the bf16 kernel's bytes in flight but needs
+        // 154 VGPRs, one workgroup per CU, and measured 13% slower
         if (G == 2) {
-            if (a.d % 512 == 0) return run<true, 8, 1, 2, 512, true, true>(p, rows_max, stream);
             if (a.d % 256 == 0) return run<true, 8, 1, 2, 256, true, true>(p, rows_max, stream);
             if (a.d % 128 == 0) return run<true, 8, 1, 2, 128, true, true>(p, rows_max, stream);
             return run<true, 8, 1, 2, 64, true, true>(p, rows_max, stream);
@@ -468,7 +496,6 @@ hipError_t launch_stream_up(const UpArgs& a, int64_t rows_max, hipStream_t strea
             if (a.d % 128 == 0) return run<true, 8, 1, 8, 128, true, true>(p, rows_max, stream);
             return run<true, 8, 1, 8, 64, true, true>(p, rows_max, stream);
         }
-        if (a.d % 256 == 0) return run<true, 8, 1, 4, 256, true, true>(p, rows_max, stream);
         if (a.d % 128 == 0) return run<true, 8, 1, 4, 128, true, true>(p, rows_max, stream);
         return run<true, 8, 1, 4, 64, true, true>(p, rows_max, stream);
     }
@@ -505,7 +532,6 @@ hipError_t launch_stream_down(const DownArgs& a, int64_t rows_max, hipStream_t s
                 return run<false, 8, 1, 2, 128, false, true>(p, rows_max, stream);
             return run<false, 4, 1, 2, 64, false, true>(p, rows_max, stream);
         }
-        if (a.ffn % 256 == 0) return run<false, 4, 1, 4, 256, false, true>(p, rows_max, stream);
         if (a.ffn % 128 == 0) return run<false, 4, 1, 4, 128, false, true>(p, rows_max, stream);
         return run<false, 4, 1, 4, 64, false, true>(p, rows_max, stream);
     }

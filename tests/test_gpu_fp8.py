@@ -87,7 +87,7 @@ def test_fp8_forward_skew_sampled():
     (300, 128, 192, 64, 8),   # E = 64, k = 8 limits
     (513, 256, 512, 8, 2),    # rows per expert > 64
     (200, 256, 256, 8, 2),    # 33..64 rows per expert
-    (96, 1024, 512, 8, 2),    # d a multiple of 512 (the longest up chunks)
+    (96, 1024, 512, 8, 2),    # several 256-element chunks per row (rotated starts)
 ])
 def test_fp8_forward_shapes(shape):
     say(f"[fp8 forward] shape {shape}")
