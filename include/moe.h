@@ -89,6 +89,12 @@ moe_status_t moe_permute(const moe_bf16_t* x, const int32_t* perm, int64_t T, in
                          int32_t k, moe_bf16_t* x_perm, hipStream_t stream);
 
 /*
+ * Expert stages (moe_swiglu_up/down, their _fp8 forms, moe_grouped_swiglu):
+ * E is the number of experts whose weights are passed.  It may be a shard of
+ * the routed experts (expert parallelism: pass the shard's weights and its
+ * slice of the offsets, whose row numbers stay absolute), so k may exceed it
+ * here; 1 <= k <= 8 still holds.
+ *
  * First half of the per-expert SwiGLU FFN (Sec. 4.1, Mixtral experts):
  * for every expert e and row r in [expert_offsets[e], expert_offsets[e+1]):
  *   h[r,n] = bf16( silu(sum_i w1[e,n,i] xr[i]) * sum_i w3[e,n,i] xr[i] )

@@ -85,6 +85,17 @@ moe_status_t check_Ek(int32_t E, int32_t k)
     return MOE_OK;
 }
 
+// the expert-GEMM stages: E counts the experts whose weights are passed, which
+// may be a shard of the routed experts, so k is not bounded by it
+moe_status_t check_Ek_stage(int32_t E, int32_t k)
+{
+    if (E < 1) return fail(MOE_ERR_INVALID_ARG, "E=%d must be >= 1", E);
+    if (E > kMaxE) return fail(MOE_ERR_UNSUPPORTED, "E=%d exceeds %d", E, kMaxE);
+    if (k < 1) return fail(MOE_ERR_INVALID_ARG, "k=%d must be >= 1", k);
+    if (k > kMaxK) return fail(MOE_ERR_UNSUPPORTED, "k=%d exceeds %d", k, kMaxK);
+    return MOE_OK;
+}
+
 moe_status_t check_dim(const char* name, int32_t v)
 {
     if (v < 1) return fail(MOE_ERR_INVALID_ARG, "%s=%d must be >= 1", name, v);
@@ -301,7 +312,7 @@ moe_status_t swiglu_up_impl(const moe_bf16_t* x_perm, const int32_t* perm,
                             int32_t d, int32_t ffn, int32_t E, int32_t k, moe_bf16_t* h,
                             hipStream_t stream)
 {
-    TRY(check_Ek(E, k));
+    TRY(check_Ek_stage(E, k));
     TRY(check_T(T, k));
     TRY(check_dim("d", d));
     TRY(check_dim("ffn", ffn));
@@ -329,7 +340,7 @@ moe_status_t swiglu_down_impl(const moe_bf16_t* h, const int32_t* expert_offsets
                               int64_t T, int32_t d, int32_t ffn, int32_t E, int32_t k, float* y,
                               hipStream_t stream)
 {
-    TRY(check_Ek(E, k));
+    TRY(check_Ek_stage(E, k));
     TRY(check_T(T, k));
     TRY(check_dim("d", d));
     TRY(check_dim("ffn", ffn));
@@ -542,7 +553,7 @@ moe_status_t moe_grouped_swiglu(const moe_bf16_t* x_perm, const int32_t* expert_
                                 int64_t T, int32_t d, int32_t ffn, int32_t E, int32_t k,
                                 moe_bf16_t* h_ws, float* y, hipStream_t stream)
 {
-    TRY(check_Ek(E, k));
+    TRY(check_Ek_stage(E, k));
     TRY(check_T(T, k));
     TRY(check_dim("d", d));
     TRY(check_dim("ffn", ffn));

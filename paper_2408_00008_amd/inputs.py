@@ -93,6 +93,15 @@ WORKLOADS = {
     "decode_t256_skew_fp8": Workload("decode_t256_skew_fp8", 256, MIXTRAL_D, MIXTRAL_FFN,
                                      MIXTRAL_E, MIXTRAL_K, 1.0, 0.02, 0.02, 0.02, 0.02,
                                      bias0=2.0, fp8=True),
+    # one GPU's share of the decode step under 8-way tensor parallelism: every
+    # expert with ffn / 8 hidden units (the partial outputs are then summed
+    # across GPUs)
+    "decode_t64_tp8": Workload("decode_t64_tp8", 64, MIXTRAL_D, MIXTRAL_FFN // 8, MIXTRAL_E,
+                               MIXTRAL_K, 1.0, 0.02, 0.02, 0.02, 0.02),
+    # a continuous-batching step mixing 64 decode tokens with a 512-token
+    # prefill chunk in one call
+    "mixed_t576": Workload("mixed_t576", 576, MIXTRAL_D, MIXTRAL_FFN, MIXTRAL_E, MIXTRAL_K,
+                           1.0, 0.02, 0.02, 0.02, 0.02),
     # 32 stacked layers, RMSNorm + residual around each, one decode step of 64
     "stack32_t64": Workload("stack32_t64", 64, MIXTRAL_D, MIXTRAL_FFN, MIXTRAL_E, MIXTRAL_K,
                             1.0, 0.02, 0.02, 0.02, 0.02, layers=32),

@@ -153,7 +153,7 @@ def test_forward_full(name):
     _forward_check(wl(name))
 
 
-@pytest.mark.parametrize("name", ["decode_t256_skew", "prefill_t4096"])
+@pytest.mark.parametrize("name", ["decode_t256_skew", "prefill_t4096", "mixed_t576", "decode_t64_tp8"])
 @pytest.mark.parametrize("variant", [0, 1])
 def test_forward_sampled(name, variant):
     say(f"[forward] {name} variant {variant} (sampled tokens)")
