@@ -145,7 +145,6 @@ __global__ __launch_bounds__(256) void q_kernel(TiledParams p)
     // byte offset of this wave's nt-th 32-row weight tile in an A slot (UP:
     // nt < 2 are w1 rows, nt + 2 the same rows of w3), and of its token tiles
     const int a_wave = (UP ? wr * 64 : wr * 128) * C::ROWB;
-    const int b_wave = wm * 128 * C::ROWB;
     auto atile = [](int nt) { return (UP ? (nt >> 1) * (C::BN / 2) + (nt & 1) * 32 : nt * 32) * C::ROWB; };
 
     for (int w = beg + local; w < end; w += per_xcd) {
@@ -200,13 +199,21 @@ __global__ __launch_bounds__(256) void q_kernel(TiledParams p)
         };
 
         // The tile body for NMT multiplied 32-token column blocks per wave
-        // (4: full tile).  An expert's last token tile often holds only a few
-        // rows; with NMT = 1 or 2 (at most 32 or 64 rows, all in the first
-        // token half) it skips the MFMAs and fragment reads of the other
-        // column blocks, which hold no rows.  Only computed blocks are stored;
-        // columns past the rows hold copies of the last row (see epilogue).
+        // (4: full tile).  The tile's blocks that hold rows are split evenly
+        // between the two token waves: wave wm multiplies blocks
+        // [wm NMT, wm NMT + NMT), NMT = ceil(blocks / 2), so a tile of an
+        // expert's last few rows (or of an expert with 65-192 rows) skips the
+        // MFMAs and fragment reads of empty blocks and both waves finish
+        // together.  Only computed blocks are stored; columns past the rows
+        // hold copies of the last row (see epilogue).
         auto tile = [&](auto nmt_tag) {
             constexpr int NMT = decltype(nmt_tag)::value;
+            const int b_wave = wm * NMT * 32 * C::ROWB;
+            // token rows [0, 64 NMT) are multiplied: wave w loads rows
+            // [64w, 64w + 64), so waves w >= NMT skip their token loads.  Their
+            // memory-counter waits stay exact: the A loads they still issue
+            // are the ones each wait leaves in flight.
+            const bool bload = wave < NMT;
             floatx16 acc[NT][NMT];
     #pragma unroll
             for (int i = 0; i < NT; ++i)
@@ -233,8 +240,10 @@ __global__ __launch_bounds__(256) void q_kernel(TiledParams p)
             // them; A(0) and B(0) complete everywhere
     #pragma unroll
             for (int i = 0; i < L; ++i) load_a(0, i);
+            if (bload) {
     #pragma unroll
-            for (int i = 0; i < L; ++i) load_b(0, i);
+                for (int i = 0; i < L; ++i) load_b(0, i);
+            }
     #pragma unroll
             for (int i = 0; i < L; ++i) load_a(1, i);
             wait_vmem<L>();
@@ -265,16 +274,16 @@ __global__ __launch_bounds__(256) void q_kernel(TiledParams p)
                         fread1(rs, rk, cur ^ 1, 2 * g);
                         fread1(rs, rk, cur ^ 1, 2 * g + 1);
                         if (ks == 0) {
-                            load_b(j + 1, 2 * g);
-                            load_b(j + 1, 2 * g + 1);
+                            if (bload) {
+                                load_b(j + 1, 2 * g);
+                                load_b(j + 1, 2 * g + 1);
+                            }
                         } else if (ks < 3) {
                             load_a(j + 2, (ks - 1) * 4 + g);
                         }
                         fence();
-                        if constexpr (NMT > 2) {
-                            acc[g][2] = mfma32x32x16(fa[cur][g], fb[cur][2], acc[g][2]);
-                            acc[g][3] = mfma32x32x16(fa[cur][g], fb[cur][3], acc[g][3]);
-                        }
+                        if constexpr (NMT > 2) acc[g][2] = mfma32x32x16(fa[cur][g], fb[cur][2], acc[g][2]);
+                        if constexpr (NMT > 3) acc[g][3] = mfma32x32x16(fa[cur][g], fb[cur][3], acc[g][3]);
                         fence();
                     }
                     if (ks == 2) {
@@ -295,7 +304,7 @@ __global__ __launch_bounds__(256) void q_kernel(TiledParams p)
             // exactly that row's results and store the same bits to the same place.
     #pragma unroll
             for (int mt = 0; mt < NMT; ++mt) {
-                const int mloc = wm * 128 + mt * 32 + (lane & 31);
+                const int mloc = (wm * NMT + mt) * 32 + (lane & 31);
                 const int64_t rrow = row0 + m0 + (mloc < Mp ? mloc : Mp - 1);
                 if (UP) {
                     bf16_t* hrow = p.h_out + rrow * p.N + nb * C::NOUT + wr * 64 + 4 * (lane >> 5);
@@ -340,12 +349,15 @@ __global__ __launch_bounds__(256) void q_kernel(TiledParams p)
                 }
             }
         };
-        if (Mp <= 32)
+        static_assert(MT == 4, "the tile variants cover 1 to 4 blocks per wave");
+        if (Mp <= 64)
             tile(std::integral_constant<int, 1>{});
-        else if (Mp <= 64)
+        else if (Mp <= 128)
             tile(std::integral_constant<int, 2>{});
+        else if (Mp <= 192)
+            tile(std::integral_constant<int, 3>{});
         else
-            tile(std::integral_constant<int, MT>{});
+            tile(std::integral_constant<int, 4>{});
 
         // the next tile's loads reuse the rings: redundant tail loads and this
         // tile's stores must be done, and every wave past its last read
