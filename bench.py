@@ -30,7 +30,8 @@ HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, published
 BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 MFMA, published
 
 KERNEL_SOURCES = {"stream": "paper_2408_00008_amd/csrc/expert_stream.hip",
-                  "tiled": "paper_2408_00008_amd/csrc/expert_tiled.hip"}
+                  "tiled": "paper_2408_00008_amd/csrc/expert_tiled.hip",
+                  "split": "paper_2408_00008_amd/csrc/expert_stream.hip"}
 
 
 def parse():
@@ -166,7 +167,9 @@ def main():
 
     counts = np.diff(offs.cpu().numpy())
     active = int((counts > 0).sum())
-    variant = "stream" if w.fp8 else {1: "stream", 2: "tiled"}[B.moe_gemm_variant_for(T, d, ffn, E, k)]
+    variant = {1: "stream", 2: "tiled", 3: "split"}[B.moe_gemm_variant_for(T, d, ffn, E, k)]
+    if w.fp8 and variant == "tiled":
+        variant = "stream"  # 8-bit weights always stream
     # algorithmic work of the up kernel: each active expert's w1 and w3 once
     # (bf16, or E4M3 bytes plus one f32 scale per row), the routed token rows
     # read once, h written once; 4*d*ffn FLOP per row
@@ -175,7 +178,9 @@ def main():
                 + A * ffn * 2)
     up_flops = 4.0 * A * d * ffn
     kernel = "expert_up_" + variant
-    if variant == "stream":
+    if variant in ("stream", "split"):
+        # split: experts of up to 64 rows stream, heavier ones take a second
+        # launch; both sit between the same two events
         achieved = up_bytes / (up_avg_ms * 1e-3) / 1e9
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                 "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4)}

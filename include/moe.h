@@ -221,16 +221,22 @@ size_t moe_workspace_size(int64_t T, int32_t d, int32_t ffn, int32_t E, int32_t 
 
 /*
  * Expert-GEMM kernel family used by moe_swiglu_up/down and the forward calls:
- *   0 = automatic (by rows per expert, T*k/E), 1 = weight-streaming (decode
- *   shapes), 2 = tiled (prefill shapes).  Process-wide; returns the previous
- *   value, or -1 for an unknown value (nothing changed).  For testing and
- *   measurement.  The 8-bit weight calls ignore it.
+ *   0 = automatic, 1 = weight-streaming (decode shapes), 2 = tiled (prefill
+ *   shapes).  Automatic: streaming while T*k/E <= 64, tiled above; in the
+ *   streaming regime with T > 64 (so an expert may hold more than 64 rows)
+ *   each expert GEMM is two launches that split the experts on the device by
+ *   their row count (<= 64: streaming; more: tiled for the bf16 up GEMM,
+ *   streaming with 128-row passes otherwise).  Process-wide; returns the
+ *   previous value, or -1 for an unknown value (nothing changed).  For
+ *   testing and measurement.  The 8-bit weight calls never take the tiled
+ *   kernel.
  */
 int moe_set_gemm_variant(int variant);
 
-/* The kernel family (1 = weight-streaming, 2 = tiled) the expert GEMMs use
- * for these sizes under the current moe_set_gemm_variant setting; 0 for
- * invalid sizes.  Host-only, enqueues nothing. */
+/* The kernel family the bf16 expert GEMMs use for these sizes under the
+ * current moe_set_gemm_variant setting: 1 = weight-streaming, 2 = tiled,
+ * 3 = split by rows per expert (see moe_set_gemm_variant); 0 for invalid
+ * sizes.  Host-only, enqueues nothing. */
 int moe_gemm_variant_for(int64_t T, int32_t d, int32_t ffn, int32_t E, int32_t k);
 
 /* Static text of a status code. */

@@ -51,6 +51,7 @@ struct StreamParams {
     const float* topk_w;     // DOWN, null = unweighted row order
     const int32_t* perm;     // DOWN
     int passes;              // workgroups per slab (each takes every passes-th pass)
+    int mlo, mhi;            // experts with mlo <= rows <= mhi only
 };
 
 // SPLIT (UP only): waves ns < NS/2 stream w1 rows, waves ns >= NS/2 the same
@@ -358,7 +359,7 @@ __global__ __launch_bounds__(64 * NS * KS) void stream_kernel(StreamParams p)
         if (t < p.E) {
             const int Mt = p.offsets[t + 1] - p.offsets[t];
             const int P = (Mt + C::MT - 1) / C::MT;
-            items = nbn8 * (P < p.passes ? P : p.passes);
+            if (Mt >= p.mlo && Mt <= p.mhi) items = nbn8 * (P < p.passes ? P : p.passes);
         }
         // inclusive scan over the wave
 #pragma unroll
@@ -472,10 +473,12 @@ hipError_t run(StreamParams p, int64_t rows_max, hipStream_t stream)
 // (128-row passes for the up GEMM above a mean of 48); an expert with more
 // rows than one pass holds is cut into several passes, which run as separate
 // workgroups.  The chunk length KC trades bytes in flight against registers.
-int stream_groups(int64_t A, int E)
+int stream_groups(int64_t A, int E, int64_t rows_max)
 {
     const int64_t mean = (A + E - 1) / E;
-    return mean <= 24 ? 2 : (mean <= 48 ? 4 : 8);
+    const int g = mean <= 24 ? 2 : (mean <= 48 ? 4 : 8);
+    // no expert has more than rows_max rows: 64-row passes hold any of them
+    return (g > 4 && rows_max <= 64) ? 4 : g;
 }
 
 hipError_t launch_stream_up(const UpArgs& a, int64_t rows_max, hipStream_t stream)
@@ -495,7 +498,9 @@ hipError_t launch_stream_up(const UpArgs& a, int64_t rows_max, hipStream_t strea
     p.K = a.d;
     p.E = a.E;
     p.h_out = a.h;
-    const int G = stream_groups(a.A, a.E);
+    p.mlo = a.mlo;
+    p.mhi = a.mhi;
+    const int G = a.groups ? a.groups : stream_groups(a.A, a.E, rows_max);
     // 8 waves: 4 stream w1 rows, 4 the same w3 rows (SPLIT)
     if (a.q1) {
         // E4M3 (sweeps on MI355X): 256-element chunks for up to 32 rows per
@@ -537,7 +542,9 @@ hipError_t launch_stream_down(const DownArgs& a, int64_t rows_max, hipStream_t s
     p.y_out = a.y;
     p.topk_w = a.topk_w;
     p.perm = a.perm;
-    const int G = stream_groups(a.A, a.E);
+    p.mlo = a.mlo;
+    p.mhi = a.mhi;
+    const int G = a.groups ? a.groups : stream_groups(a.A, a.E, rows_max);
     if (a.q2) {
         if (G == 2) {
             if (a.d % 128 == 0 && a.ffn % 256 == 0)
@@ -546,6 +553,8 @@ hipError_t launch_stream_down(const DownArgs& a, int64_t rows_max, hipStream_t s
                 return run<false, 8, 1, 2, 128, false, true>(p, rows_max, stream);
             return run<false, 4, 1, 2, 64, false, true>(p, rows_max, stream);
         }
+        if (G == 4 && a.d % 128 == 0 && a.ffn % 128 == 0)
+            return run<false, 8, 1, 4, 128, false, true, 3>(p, rows_max, stream);
         if (a.ffn % 128 == 0) return run<false, 4, 1, 4, 128, false, true>(p, rows_max, stream);
         return run<false, 4, 1, 4, 64, false, true>(p, rows_max, stream);
     }
@@ -553,6 +562,11 @@ hipError_t launch_stream_down(const DownArgs& a, int64_t rows_max, hipStream_t s
         if (a.d % 128 == 0 && a.ffn % 128 == 0) return run<false, 8, 1, 2, 128>(p, rows_max, stream);
         return run<false, 4, 1, 2, 64>(p, rows_max, stream);
     }
+    // up to 64 rows per pass: 8 waves (128 output rows) share each staged
+    // token tile and three weight sets are in flight; above, 4 waves, so a
+    // heavy expert's passes spread over twice as many workgroups
+    if (G == 4 && a.d % 128 == 0 && a.ffn % 128 == 0)
+        return run<false, 8, 1, 4, 128, false, false, 3>(p, rows_max, stream);
     if (a.ffn % 128 == 0) return run<false, 4, 1, 4, 128>(p, rows_max, stream);
     return run<false, 4, 1, 4, 64>(p, rows_max, stream);
 }

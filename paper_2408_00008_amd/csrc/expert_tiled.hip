@@ -39,6 +39,7 @@ struct TiledParams {
     float* y_out;            // DOWN [A, N]
     const float* topk_w;     // DOWN, null = unweighted row order
     const int32_t* perm;     // DOWN
+    int mlo, mhi;            // experts with mlo <= rows <= mhi only
 };
 
 int cu_count();
@@ -116,7 +117,8 @@ __global__ __launch_bounds__(256) void q_kernel(TiledParams p)
 
     // per-expert token tiles and their prefix, one expert per lane:
     // items before expert e = nbn * (token tiles of experts < e)
-    const int my_tiles = lane < p.E ? (p.offsets[lane + 1] - p.offsets[lane] + C::BM - 1) / C::BM : 0;
+    const int my_rows = lane < p.E ? p.offsets[lane + 1] - p.offsets[lane] : 0;
+    const int my_tiles = (my_rows >= p.mlo && my_rows <= p.mhi) ? (my_rows + C::BM - 1) / C::BM : 0;
     int in_tiles = my_tiles;
 #pragma unroll
     for (int o = 1; o < 64; o <<= 1) {
@@ -421,6 +423,8 @@ hipError_t launch_tiled_up(const UpArgs& a, hipStream_t stream)
     p.K = a.d;
     p.E = a.E;
     p.h_out = a.h;
+    p.mlo = a.mlo;
+    p.mhi = a.mhi;
     return run_q<true>(p, a.A, stream);
 }
 
@@ -436,6 +440,8 @@ hipError_t launch_tiled_down(const DownArgs& a, hipStream_t stream)
     p.y_out = a.y;
     p.topk_w = a.topk_w;
     p.perm = a.perm;
+    p.mlo = a.mlo;
+    p.mhi = a.mhi;
     return run_q<false>(p, a.A, stream);
 }
 

@@ -48,6 +48,10 @@ struct UpArgs {
     const float* s1 = nullptr;
     const uint8_t* q3 = nullptr;
     const float* s3 = nullptr;
+    // only experts with mlo <= rows <= mhi (the others are another launch's)
+    int mlo = 0, mhi = 0x7fffffff;
+    // streaming kernels: 16-row token groups per pass (0 = by rows per expert)
+    int groups = 0;
 };
 
 struct DownArgs {
@@ -62,6 +66,8 @@ struct DownArgs {
     // 8-bit weights (then w2 is unused): E4M3 bytes [E,d,ffn], scales [E,d]
     const uint8_t* q2 = nullptr;
     const float* s2 = nullptr;
+    int mlo = 0, mhi = 0x7fffffff;
+    int groups = 0;
 };
 
 enum GemmVariant { VARIANT_AUTO = 0, VARIANT_STREAM = 1, VARIANT_TILED = 2 };

@@ -138,6 +138,13 @@ def test_workspace_size(L):
 def test_variant_switch(L):
     assert L.moe_gemm_variant_for(64, 4096, 14336, 8, 2) == 1
     assert L.moe_gemm_variant_for(64, 4096, 14336, 8, 9) == 0
+    # streaming regime with T > 64: split by rows per expert; mean above 64: tiled
+    assert L.moe_gemm_variant_for(256, 4096, 14336, 8, 2) == 3
+    assert L.moe_gemm_variant_for(4096, 4096, 14336, 8, 2) == 2
+    assert L.moe_gemm_variant_for(257, 4096, 14336, 8, 2) == 2
+    prev = L.moe_set_gemm_variant(1)
+    assert L.moe_gemm_variant_for(256, 4096, 14336, 8, 2) == 1
+    L.moe_set_gemm_variant(prev)
     prev = L.moe_set_gemm_variant(1)
     assert L.moe_set_gemm_variant(2) == 1
     assert L.moe_set_gemm_variant(7) == -1

@@ -207,6 +207,25 @@ def test_forward_heavy_expert(variant):
     _forward_check(c, variant=variant)
 
 
+@pytest.mark.parametrize("shape", [
+    (256, 256, 512, 8, 2),    # heavy experts take the tiled up kernel
+    (256, 192, 320, 8, 2),    # no tiled shape: heavy experts stream in 128-row passes
+    (130, 128, 256, 4, 1),    # k = 1, T just above 64
+])
+def test_forward_split_by_rows(shape):
+    """Automatic choice in the streaming regime with T > 64: a +2 logit bias
+    gives expert 0 more than 64 rows and the rest fewer, so each expert GEMM
+    runs as two launches split on the device by rows per expert."""
+    say(f"[forward] split by rows {shape}")
+    bias = [2.0] + [0.0] * (shape[3] - 1)
+    c = small_case(*shape, seed=23, bias=bias)
+    assert B.moe_gemm_variant_for(c.T, c.d, c.ffn, c.E, c.k) == 3
+    _, _, offs, _, _ = gpu_route(c)
+    rows = np.diff(offs.cpu().numpy())
+    assert rows.max() > 64 and (rows[rows > 0] <= 64).any(), rows
+    _forward_check(c, variant=0)
+
+
 def test_forward_t0():
     c = small_case(3, 64, 64, 4, 2)
     out = torch.zeros(0, 64, dtype=torch.bfloat16, device=DEV)
