@@ -404,3 +404,144 @@ int oracle_rmsnorm(const float* h, const uint16_t* gamma, int64_t T, int64_t d, 
     }
     return ORACLE_OK;
 }
+
+/* ==========================================================================
+ * The decoder layer around the MoE block, for one decode step.
+ *
+ * The paper's engine serves the whole Mixtral model with FlashAttention- and
+ * PagedAttention-style attention kernels (Sec. 2 and Sec. 4.1).  One decoder
+ * layer of the model is, per decode token (the request's next position p):
+ *
+ *   a   = bf16( RMSNorm(h) * gamma_attn )
+ *   q   = Wq a, k = Wk a, v = Wv a            Hq query heads, Hkv key/value
+ *                                             heads of hd values (Hq/Hkv
+ *                                             query heads share one KV head)
+ *   q, k rotated by position p (RoPE)
+ *   the KV cache stores k, v (bf16) at position p of the request
+ *   o_h = sum_{s <= p} softmax_s( q_h . k_s / sqrt(hd) ) v_s   (KV head of h)
+ *   h   = h + Wo [o_0 .. o_{Hq-1}]
+ *   h   = h + MoE( bf16( RMSNorm(h) * gamma_moe ) )
+ *
+ * The functions below are the steps that are not already above: RoPE,
+ * attention over a paged cache, and rounding to bf16 (the cache's storage
+ * precision).  The projections are plain matrix products.
+ * ========================================================================== */
+
+/* Round to the nearest bf16 value, ties to even, straight from double (no
+ * intermediate float rounding).  Finite inputs within the bf16 range. */
+static uint16_t round_to_bf16(double x)
+{
+    const uint16_t sign = signbit(x) ? 0x8000 : 0;
+    if (x == 0.0) return sign;
+    int e;
+    const double f = frexp(fabs(x), &e); /* |x| = f * 2^e, f in [0.5, 1) */
+    /* 8 significant bits for normals (exponent e - 1 >= -126), fewer below */
+    int bits = 8;
+    if (e - 1 < -126) bits = 8 - (-126 - (e - 1));
+    /* bits = 0: |x| in [2^-134, 2^-133), rounds to 0 or the smallest subnormal */
+    double v = 0.0;
+    if (bits >= 0) v = ldexp(nearbyint(ldexp(f, bits)), e - bits); /* nearbyint: ties to even */
+    const float fv = (float)v; /* exact: v has at most 8 significant bits */
+    uint32_t u;
+    memcpy(&u, &fv, sizeof u);
+    return (uint16_t)(u >> 16) | sign;
+}
+
+int oracle_round_bf16(const double* x, int64_t n, uint16_t* out)
+{
+    if (n < 0) return ORACLE_BAD_ARG;
+    for (int64_t i = 0; i < n; ++i) {
+        if (!isfinite(x[i])) return ORACLE_NONFINITE;
+        out[i] = round_to_bf16(x[i]);
+    }
+    return ORACLE_OK;
+}
+
+/* RoPE, the rotate-half pairing of the Mixtral checkpoints: element i pairs
+ * with element i + hd/2 of the same head, rotated by the angle
+ * pos * base^(-2i/hd), i < hd/2:
+ *   y[i]        = x[i] cos - x[i + hd/2] sin
+ *   y[i + hd/2] = x[i + hd/2] cos + x[i] sin
+ * In place on x [T, H, hd]; token t has position pos[t]. */
+int oracle_rope(double* x, int64_t T, int H, int hd, const int32_t* pos, double base)
+{
+    if (T < 0 || H <= 0 || hd <= 0 || hd % 2 || !(base > 0.0)) return ORACLE_BAD_ARG;
+    const int half = hd / 2;
+    for (int64_t t = 0; t < T; ++t) {
+        if (pos[t] < 0) return ORACLE_BAD_ARG;
+        for (int h = 0; h < H; ++h) {
+            double* v = x + (t * H + h) * hd;
+            for (int i = 0; i < half; ++i) {
+                const double ang = (double)pos[t] * pow(base, -2.0 * i / hd);
+                const double c = cos(ang), s = sin(ang);
+                const double a = v[i], b = v[i + half];
+                v[i] = a * c - b * s;
+                v[i + half] = b * c + a * s;
+            }
+        }
+    }
+    return ORACLE_OK;
+}
+
+/* Decode attention over a paged KV cache.
+ *   cache layout: kc, vc [pages, Hkv, page, hd] bf16 bits;
+ *   token t attends to its request's positions s = 0 .. ctx[t]-1, position s
+ *   stored in physical page page_table[t * maxp + s / page], slot s % page;
+ *   query head h reads KV head h / (Hq / Hkv);
+ *   out[t, h, :] = sum_s w_s V_s / sum_s w_s,
+ *   w_s = exp(scale * q[t,h,:] . K_s - max_s'(scale * q . K_s'))
+ * (the usual shift by the largest score; it leaves the softmax unchanged). */
+int oracle_attention_decode(const double* q, const uint16_t* kc, const uint16_t* vc,
+                            const int32_t* page_table, int64_t maxp, int64_t npages,
+                            const int32_t* ctx, int64_t T, int Hq, int Hkv, int hd, int page,
+                            double scale, double* out)
+{
+    if (T < 0 || Hq <= 0 || Hkv <= 0 || Hq % Hkv || hd <= 0 || page <= 0 || maxp <= 0 ||
+        npages <= 0)
+        return ORACLE_BAD_ARG;
+    for (int64_t t = 0; t < T; ++t) {
+        if (ctx[t] < 1 || ctx[t] > maxp * page) return ORACLE_BAD_ARG;
+        for (int64_t j = 0; j < (ctx[t] + page - 1) / page; ++j) {
+            const int32_t pg = page_table[t * maxp + j];
+            if (pg < 0 || pg >= npages) return ORACLE_BAD_ARG;
+        }
+    }
+    const int group = Hq / Hkv;
+    int bad = 0;
+#pragma omp parallel for collapse(2) schedule(dynamic)
+    for (int64_t t = 0; t < T; ++t) {
+        for (int h = 0; h < Hq; ++h) {
+            const int g = h / group;
+            const int L = ctx[t];
+            const double* qv = q + (t * Hq + h) * hd;
+            double* sc = (double*)malloc(sizeof(double) * (size_t)L);
+            double* acc = out + (t * Hq + h) * hd;
+            if (!sc) {
+#pragma omp atomic write
+                bad = 1;
+                continue;
+            }
+            double mx = -INFINITY;
+            for (int s = 0; s < L; ++s) {
+                const int64_t pg = page_table[t * maxp + s / page];
+                const uint16_t* kr = kc + ((pg * Hkv + g) * page + s % page) * hd;
+                double dot = 0.0;
+                for (int i = 0; i < hd; ++i) dot += qv[i] * widen(kr[i]);
+                sc[s] = scale * dot;
+                if (sc[s] > mx) mx = sc[s];
+            }
+            double den = 0.0;
+            for (int i = 0; i < hd; ++i) acc[i] = 0.0;
+            for (int s = 0; s < L; ++s) {
+                const int64_t pg = page_table[t * maxp + s / page];
+                const uint16_t* vr = vc + ((pg * Hkv + g) * page + s % page) * hd;
+                const double w = exp(sc[s] - mx);
+                den += w;
+                for (int i = 0; i < hd; ++i) acc[i] += w * widen(vr[i]);
+            }
+            for (int i = 0; i < hd; ++i) acc[i] /= den;
+            free(sc);
+        }
+    }
+    return bad ? ORACLE_NO_MEMORY : ORACLE_OK;
+}

@@ -62,9 +62,14 @@ class Oracle:
                                            ctypes.c_int, ctypes.c_int, _p, _p, _p]
         L.oracle_moe_layer_fp8.argtypes = [_p, _p, _p, _p, _p, _p, _p, _p, _p, _i64, _i64, _i64,
                                            ctypes.c_int, ctypes.c_int, _p, _p, _p, _p]
+        L.oracle_round_bf16.argtypes = [_p, _i64, _p]
+        L.oracle_rope.argtypes = [_p, _i64, ctypes.c_int, ctypes.c_int, _p, _f64]
+        L.oracle_attention_decode.argtypes = [_p, _p, _p, _p, _i64, _i64, _p, _i64, ctypes.c_int,
+                                              ctypes.c_int, ctypes.c_int, ctypes.c_int, _f64, _p]
         for f in ("oracle_router_logits", "oracle_topk_gate", "oracle_gates_for_ids", "oracle_dispatch",
                   "oracle_moe_apply", "oracle_moe_layer", "oracle_rmsnorm", "oracle_fp8_e4m3",
-                  "oracle_moe_apply_fp8", "oracle_moe_layer_fp8"):
+                  "oracle_moe_apply_fp8", "oracle_moe_layer_fp8", "oracle_round_bf16", "oracle_rope",
+                  "oracle_attention_decode"):
             getattr(L, f).restype = ctypes.c_int
 
     # -- helpers -----------------------------------------------------------
@@ -234,6 +239,80 @@ class Oracle:
         self._check(self.lib.oracle_rmsnorm(self._ptr(h), self._ptr(gamma), T, d, float(eps),
                                             self._ptr(a)), "rmsnorm")
         return a
+
+    # -- the decoder layer around the MoE block (one decode step) --------------
+
+    def round_bf16(self, x):
+        """float64 -> bf16 bit patterns, round to nearest, ties to even."""
+        x = np.ascontiguousarray(x, dtype=np.float64)
+        out = np.empty(x.shape, np.uint16)
+        self._check(self.lib.oracle_round_bf16(self._ptr(x), x.size, self._ptr(out)), "round_bf16")
+        return out
+
+    def rope(self, x, pos, base):
+        """RoPE of x [T, H, hd] (float64) at positions pos [T]; returns a copy."""
+        x = np.array(x, dtype=np.float64, order="C", copy=True)
+        T, H, hd = x.shape
+        pos = np.ascontiguousarray(pos, dtype=np.int32)
+        self._check(self.lib.oracle_rope(self._ptr(x), T, H, hd, self._ptr(pos), float(base)), "rope")
+        return x
+
+    def attention_decode(self, q, k_cache, v_cache, page_table, ctx, scale):
+        """q [T, Hq, hd] float64; caches [pages, Hkv, page, hd] bf16 bits;
+        page_table [T, maxp] int32; ctx [T] positions attended per token."""
+        q = np.ascontiguousarray(q, dtype=np.float64)
+        T, Hq, hd = q.shape
+        P, Hkv, page, hd2 = k_cache.shape
+        assert hd2 == hd and v_cache.shape == k_cache.shape
+        kc, vc = self._bits(k_cache), self._bits(v_cache)
+        pt = np.ascontiguousarray(page_table, dtype=np.int32)
+        ctx = np.ascontiguousarray(ctx, dtype=np.int32)
+        out = np.empty((T, Hq, hd), np.float64)
+        self._check(self.lib.oracle_attention_decode(
+            self._ptr(q), self._ptr(kc), self._ptr(vc), self._ptr(pt), pt.shape[1], P, self._ptr(ctx),
+            T, Hq, Hkv, hd, page, float(scale), self._ptr(out)), "attention_decode")
+        return out
+
+    def decoder_layer(self, h, gamma_attn, wq, wk, wv, wo, k_cache, v_cache, page_table, pos,
+                      gamma_moe, wr, w1, w3, w2, k, hq, hkv, theta, eps):
+        """One decode step of a decoder layer for T tokens (one per request):
+        h [T, d] float32 residual stream; projections bf16 bits (nn.Linear
+        layout: wq [hq*hd, d], wk, wv [hkv*hd, d], wo [d, hq*hd]); the new
+        token of request t sits at position pos[t] (pos[t] earlier positions
+        are in the cache).  Returns the intermediates and the layer output
+        h2 (float64); the caches passed in are not modified (copies with the
+        new entries are returned)."""
+        h = np.ascontiguousarray(h, dtype=np.float32)
+        T, d = h.shape
+        hd = wq.shape[0] // hq
+        a = self.round_bf16(self.rmsnorm(h, gamma_attn, eps))
+        af = a.astype(np.uint32) << 16
+        A = af.view(np.float32).astype(np.float64)
+
+        def lin(w):
+            wf = (self._bits(w).astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+            return A @ wf.T
+
+        q = self.rope(lin(wq).reshape(T, hq, hd), pos, theta)
+        kn = self.rope(lin(wk).reshape(T, hkv, hd), pos, theta)
+        vn = lin(wv).reshape(T, hkv, hd)
+        kc, vc = np.array(k_cache, copy=True), np.array(v_cache, copy=True)
+        page = kc.shape[2]
+        pos = np.asarray(pos, dtype=np.int64)
+        for t in range(T):
+            pg = page_table[t, pos[t] // page]
+            kc[pg, :, pos[t] % page, :] = self.round_bf16(kn[t])
+            vc[pg, :, pos[t] % page, :] = self.round_bf16(vn[t])
+        o = self.attention_decode(q, kc, vc, page_table, pos + 1, 1.0 / np.sqrt(hd))
+        wof = (self._bits(wo).astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+        h1 = h.astype(np.float64) + o.reshape(T, hq * hd) @ wof.T
+        # the residual stream is kept in float32 between the two blocks
+        h1f = h1.astype(np.float32)
+        a2 = self.round_bf16(self.rmsnorm(h1f, gamma_moe, eps))
+        moe = self.moe_layer(a2, wr, w1, w3, w2, k)
+        h2 = h1f.astype(np.float64) + moe["out"]
+        return {"a": a, "q": q, "k_new": kn, "v_new": vn, "k_cache": kc, "v_cache": vc,
+                "attn": o, "h1": h1, "a2": a2, "moe": moe, "h2": h2}
 
 
 _default = None

@@ -15,7 +15,14 @@ the mutation test) and raises AssertionError if the oracle disagrees with:
   changes nothing, scaling W2 by a power of two scales the output exactly;
 * for 8-bit (OCP E4M3) expert weights: every byte against torch's
   float8_e4m3fn conversion, the values the OCP specification tabulates, and
-  the brute force fed with weights dequantized by torch.
+  the brute force fed with weights dequantized by torch;
+* for the decoder layer around the MoE block: bf16 rounding against torch's
+  float32 -> bfloat16 conversion and exact ties, RoPE on unit vectors in
+  closed form, paged attention against torch's fp64
+  scaled_dot_product_attention, GQA against repeated KV heads, page
+  relocation, one-position and equal-key closed forms, and the layer's
+  composition (Wo = 0 leaves the MoE block; position 0 returns the new
+  value rows).
 """
 
 from __future__ import annotations
@@ -390,6 +397,174 @@ def pin_fp8_row_scale(o):
     assert np.array_equal(r2["out"][:, keep], r["out"][:, keep])
 
 
+# ---- the decoder layer around the MoE block (one decode step) ---------------
+
+
+def pin_round_bf16(o):
+    """fp64 -> bf16 rounds to nearest, ties to even, in one step: float32
+    values round like torch's float32 -> bfloat16 conversion (a library
+    implementation), exact ties go to the even neighbour, and a value just
+    above a tie rounds up (rounding through float32 first would land on the
+    tie and round down)."""
+    g = np.random.default_rng(501)
+    f32 = np.concatenate([g.standard_normal(4000) * 10.0 ** g.integers(-40, 38, 4000),
+                          g.standard_normal(500) * 1e-39]).astype(np.float32)
+    f32 = f32[np.isfinite(f32) & (np.abs(f32) < 3e38)]
+    ref = torch.from_numpy(f32).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    assert np.array_equal(o.round_bf16(f32.astype(np.float64)), ref)
+    one_ulp = 2.0 ** -7
+    cases = [(1.0 + one_ulp / 2, 0x3F80), (1.0 + 1.5 * one_ulp, 0x3F82), (-(1.0 + one_ulp / 2), 0xBF80),
+             (1.0 + one_ulp / 2 + 2.0 ** -40, 0x3F81), (3.0, 0x4040), (0.0, 0x0000), (-0.0, 0x8000),
+             (2.0 ** -134, 0x0000), (1.5 * 2.0 ** -134, 0x0001), (3 * 2.0 ** -134, 0x0002)]
+    got = o.round_bf16(np.array([x for x, _ in cases], dtype=np.float64))
+    assert got.tolist() == [b for _, b in cases]
+
+
+def pin_rope_closed_form(o):
+    """RoPE of a unit vector e_i at position p is cos(p w_i) at i and
+    sin(p w_i) at i + hd/2 with w_i = base^(-2i/hd) (the rotate-half pairing);
+    position 0 is the identity; scores depend only on the position
+    difference."""
+    hd, base = 16, 10000.0
+    for i in (0, 3, 7):
+        for p in (1, 5, 1000):
+            x = np.zeros((1, 1, hd))
+            x[0, 0, i] = 1.0
+            y = o.rope(x, [p], base)[0, 0]
+            w = base ** (-2.0 * i / hd)
+            want = np.zeros(hd)
+            want[i], want[i + hd // 2] = math.cos(p * w), math.sin(p * w)
+            _close(y, want, rtol=1e-14, atol=1e-15)
+    g = np.random.default_rng(502)
+    x = g.standard_normal((3, 2, hd))
+    assert np.array_equal(o.rope(x, [0, 0, 0], base), x)
+    q, k = g.standard_normal((1, 1, hd)), g.standard_normal((1, 1, hd))
+    d1 = float(np.sum(o.rope(q, [9], base) * o.rope(k, [4], base)))
+    d2 = float(np.sum(o.rope(q, [1009], base) * o.rope(k, [1004], base)))
+    assert abs(d1 - d2) < 1e-12 * (1 + abs(d1))
+
+
+def _randn_bits(g, shape, scale=1.0):
+    """bf16 bit patterns of scaled normal draws (rounded by torch)."""
+    x = torch.from_numpy((g.standard_normal(shape) * scale).astype(np.float32))
+    return x.to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+
+
+def _attn_case(g, T, Hq, Hkv, hd, page, npages, maxp, ctx):
+    kc = _randn_bits(g, (npages, Hkv, page, hd))
+    vc = _randn_bits(g, (npages, Hkv, page, hd))
+    pt = np.stack([g.permutation(npages)[:maxp] for _ in range(T)]).astype(np.int32)
+    q = g.standard_normal((T, Hq, hd))
+    return q, kc, vc, pt, np.asarray(ctx, np.int32)
+
+
+def _gather(cache, pt_row, L):
+    page = cache.shape[2]
+    return np.stack([widen(cache[pt_row[s // page], :, s % page, :]) for s in range(L)])  # [L, Hkv, hd]
+
+
+def pin_attention_sdpa(o):
+    """Paged decode attention with one query head per KV head equals torch's
+    fp64 scaled_dot_product_attention on the gathered contiguous cache."""
+    g = np.random.default_rng(503)
+    T, H, hd, page = 3, 2, 8, 4
+    q, kc, vc, pt, ctx = _attn_case(g, T, H, H, hd, page, 9, 4, [1, 7, 16])
+    got = o.attention_decode(q, kc, vc, pt, ctx, 1 / math.sqrt(hd))
+    for t in range(T):
+        K = torch.from_numpy(_gather(kc, pt[t], ctx[t])).permute(1, 0, 2)  # [H, L, hd]
+        V = torch.from_numpy(_gather(vc, pt[t], ctx[t])).permute(1, 0, 2)
+        Q = torch.from_numpy(q[t][:, None, :])  # [H, 1, hd]
+        ref = torch.nn.functional.scaled_dot_product_attention(Q, K, V)[:, 0, :].numpy()
+        _close(got[t], ref, rtol=1e-12, atol=1e-13)
+
+
+def pin_attention_gqa_and_pages(o):
+    """Grouped heads: query head h reads KV head h // (Hq/Hkv), so GQA equals
+    attention over a cache whose KV heads are repeated per query head.
+    Relocating the pages (with the page table updated) changes nothing, one
+    cached position returns its value row, and identical keys average the
+    values."""
+    g = np.random.default_rng(504)
+    T, Hq, Hkv, hd, page, npages, maxp = 2, 8, 2, 8, 4, 10, 4
+    q, kc, vc, pt, ctx = _attn_case(g, T, Hq, Hkv, hd, page, npages, maxp, [5, 13])
+    sc = 1 / math.sqrt(hd)
+    got = o.attention_decode(q, kc, vc, pt, ctx, sc)
+    rep = np.repeat(np.arange(Hkv), Hq // Hkv)
+    assert np.array_equal(got, o.attention_decode(q, kc[:, rep], vc[:, rep], pt, ctx, sc))
+    perm = g.permutation(npages)
+    inv = np.argsort(perm)
+    kc2, vc2 = np.empty_like(kc), np.empty_like(vc)
+    kc2[perm], vc2[perm] = kc, vc
+    assert np.array_equal(got, o.attention_decode(q, kc2, vc2, perm[pt].astype(np.int32), ctx, sc))
+    del inv
+    one = o.attention_decode(q, kc, vc, pt, np.ones(T, np.int32), sc)
+    for t in range(T):
+        for h in range(Hq):
+            assert np.array_equal(one[t, h], widen(vc[pt[t, 0], h // (Hq // Hkv), 0]))
+    kc3 = kc.copy()
+    kc3[...] = kc[0, 0, 0]
+    avg = o.attention_decode(q, kc3, vc, pt, ctx, sc)
+    for t in range(T):
+        V = _gather(vc, pt[t], ctx[t])
+        for h in range(Hq):
+            _close(avg[t, h], V[:, h // (Hq // Hkv)].mean(axis=0), rtol=1e-13, atol=1e-14)
+
+
+def _decoder_case(g, T=3, d=16, hq=4, hkv=2, hd=4, ffn=8, E=4, k=2, page=4, npages=10, maxp=3):
+    def w(*shape):
+        return _randn_bits(g, shape, 1 / math.sqrt(shape[-1]))
+
+    def gamma():
+        return torch.from_numpy(g.uniform(0.5, 1.5, d).astype(np.float32)).to(
+            torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    c = {"h": g.standard_normal((T, d)).astype(np.float32),
+         "gamma_attn": gamma(), "gamma_moe": gamma(),
+         "wq": w(hq * hd, d), "wk": w(hkv * hd, d), "wv": w(hkv * hd, d), "wo": w(d, hq * hd),
+         "k_cache": _randn_bits(g, (npages, hkv, page, hd)),
+         "v_cache": _randn_bits(g, (npages, hkv, page, hd)),
+         # every request owns its pages (the new entries are written)
+         "page_table": g.permutation(npages)[:T * maxp].reshape(T, maxp).astype(np.int32),
+         "pos": g.integers(0, maxp * page, T).astype(np.int32),
+         "wr": w(E, d), "w1": w(E, ffn, d), "w3": w(E, ffn, d), "w2": w(E, d, ffn),
+         "k": k, "hq": hq, "hkv": hkv, "theta": 1e6, "eps": 1e-5}
+    return c
+
+
+def _decoder(o, c):
+    return o.decoder_layer(c["h"], c["gamma_attn"], c["wq"], c["wk"], c["wv"], c["wo"], c["k_cache"],
+                           c["v_cache"], c["page_table"], c["pos"], c["gamma_moe"], c["wr"], c["w1"],
+                           c["w3"], c["w2"], c["k"], c["hq"], c["hkv"], c["theta"], c["eps"])
+
+
+def pin_decoder_layer_composition(o):
+    """With Wo = 0 the attention block adds exactly nothing and the layer is
+    the MoE residual block of the stack; at position 0 (nothing cached yet)
+    the attention output of every query head is its KV head's new value row
+    as stored (bf16), so the block adds Wo applied to those rows; the new
+    key/value rows land in the cache at their request's position."""
+    g = np.random.default_rng(505)
+    c = _decoder_case(g)
+    c0 = dict(c, wo=np.zeros(c["wo"].shape, np.uint16))
+    r0 = _decoder(o, c0)
+    assert np.array_equal(r0["h1"], c["h"].astype(np.float64))
+    a2 = o.round_bf16(o.rmsnorm(c["h"], c["gamma_moe"], c["eps"]))
+    moe = o.moe_layer(a2, c["wr"], c["w1"], c["w3"], c["w2"], c["k"])
+    assert np.array_equal(r0["h2"], c["h"].astype(np.float64) + moe["out"])
+    cp = dict(c, pos=np.zeros(3, np.int32))
+    r = _decoder(o, cp)
+    vrow = widen(o.round_bf16(r["v_new"]))  # [T, hkv, hd]
+    grp = c["hq"] // c["hkv"]
+    o_ref = np.stack([np.concatenate([vrow[t, h // grp] for h in range(c["hq"])]) for t in range(3)])
+    assert np.array_equal(r["attn"].reshape(3, -1), o_ref)
+    _close(r["h1"], c["h"].astype(np.float64) + o_ref @ widen(c["wo"]).T, rtol=1e-13, atol=1e-13)
+    r = _decoder(o, c)
+    page = c["k_cache"].shape[2]
+    for t in range(3):
+        pg, sl = c["page_table"][t, c["pos"][t] // page], c["pos"][t] % page
+        assert np.array_equal(r["k_cache"][pg, :, sl], o.round_bf16(r["k_new"][t]))
+        assert np.array_equal(r["v_cache"][pg, :, sl], o.round_bf16(r["v_new"][t]))
+
+
 ALL_PINS = [
     pin_bruteforce_random,
     pin_bruteforce_ties,
@@ -410,4 +585,9 @@ ALL_PINS = [
     pin_fp8_spec_values,
     pin_fp8_layer_bruteforce,
     pin_fp8_row_scale,
+    pin_round_bf16,
+    pin_rope_closed_form,
+    pin_attention_sdpa,
+    pin_attention_gqa_and_pages,
+    pin_decoder_layer_composition,
 ]

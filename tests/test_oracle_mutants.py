@@ -46,6 +46,19 @@ MUTANTS = {
     "rmsnorm_mean_as_sum": ("sqrt(ss / (double)d + eps)", "sqrt(ss + eps)"),
     "rmsnorm_gamma_dropped": ("* inv * widen(gamma[i])", "* inv"),
     "topk_second_best_repeats": ("taken |= (s[m] == e);", "taken |= 0;"),
+    # the decoder layer around the MoE block
+    "rope_interleaved_pairs": ("const double a = v[i], b = v[i + half];\n                v[i] = a * c - b * s;\n"
+                               "                v[i + half] = b * c + a * s;",
+                               "const double a = v[2 * i], b = v[2 * i + 1];\n                v[2 * i] = a * c - b * s;\n"
+                               "                v[2 * i + 1] = b * c + a * s;"),
+    "rope_sign": ("v[i] = a * c - b * s;", "v[i] = a * c + b * s;"),
+    "rope_frequency": ("pow(base, -2.0 * i / hd)", "pow(base, -1.0 * i / hd)"),
+    "attention_scale_dropped": ("sc[s] = scale * dot;", "sc[s] = dot;"),
+    "attention_gqa_modulo": ("const int g = h / group;", "const int g = h % Hkv;"),
+    "attention_context_short": ("const int L = ctx[t];", "const int L = ctx[t] > 1 ? ctx[t] - 1 : 1;"),
+    "attention_slot_off_by_one": ("const uint16_t* vr = vc + ((pg * Hkv + g) * page + s % page) * hd;",
+                                  "const uint16_t* vr = vc + ((pg * Hkv + g) * page + (s + 1) % page) * hd;"),
+    "round_bf16_truncates": ("nearbyint(ldexp(f, bits))", "floor(ldexp(f, bits))"),
 }
 
 
