@@ -102,6 +102,9 @@ def main():
     if w.layers != 1:
         from paper_2408_00008_amd import stack
         return stack.bench_stack(args, w)
+    if w.hq:
+        from paper_2408_00008_amd import decoder
+        return decoder.bench_decoder(args, w)
     T, d, ffn, E, k = w.T, w.d, w.ffn, w.E, w.k
     A = T * k
     x = inputs.make_x(w, dev)

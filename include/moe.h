@@ -216,6 +216,63 @@ moe_status_t moe_forward_fp8_ex(const moe_bf16_t* x, const moe_bf16_t* router_w,
 moe_status_t moe_rmsnorm(const float* h, const moe_bf16_t* gamma, int64_t T, int32_t d, float eps,
                          moe_bf16_t* a, hipStream_t stream);
 
+/*
+ * ---- The decoder layer around the MoE block (one decode step) -------------
+ * The engine serves the whole model with paged, flash-style attention (Sec. 2;
+ * Sec. 4.1, "Other Optimizations").  With the calls below and moe_rmsnorm,
+ * moe_combine and moe_forward_ex, one decoder layer of a decode step runs on
+ * the device for T tokens, one per request:
+ *   a = RMSNorm(h) gamma_attn (bf16)        moe_rmsnorm
+ *   qkv = a [Wq; Wk; Wv]^T (f32)            moe_linear
+ *   RoPE(q, k); k, v -> cache (bf16)        moe_rope_kv_append
+ *   o = attention over the cache (bf16)     moe_attention_decode
+ *   h += o Wo^T (f32 residual)              moe_linear + moe_combine (k = 1)
+ *   h += MoE(RMSNorm(h) gamma_moe)          moe_rmsnorm + moe_forward_ex
+ * KV cache layout, keys and values alike: [npages, Hkv, page, hd] bf16; the
+ * request of token t stores position s in page page_table[t * maxp + s /
+ * page], slot s % page.  Page ids, positions and context lengths are device
+ * data: the kernels clamp values outside the cache (invalid input) so that
+ * nothing outside the cache is read or written.
+ */
+
+/*
+ * Dense projection y[t, n] = sum_i x[t, i] w[n, i] (bf16 operands, f32
+ * accumulate and output): x [T, K] bf16, w [N, K] bf16 (nn.Linear layout),
+ * y [T, N] f32.  K, N multiples of 64 (<= 65536).  The weight-streaming GEMM
+ * with one matrix.
+ */
+moe_status_t moe_linear(const moe_bf16_t* x, const moe_bf16_t* w, int64_t T, int32_t K, int32_t N,
+                        float* y, hipStream_t stream);
+
+/*
+ * Rotary position embedding and KV-cache append for the new token of each
+ * request.  qkv [T, (Hq + 2 Hkv) hd] f32 holds the token's query heads, then
+ * key heads, then value heads; pos [T] its position (the number of positions
+ * already cached).  Query and key heads are rotated, element i with element
+ * i + hd/2, by the angle pos * theta^(-2i/hd) (the rotate-half layout of
+ * Mixtral/Llama checkpoints; Mixtral: theta = 1e6).  Writes q_out [T, Hq, hd]
+ * and the key and value rows at position pos[t], all rounded to bf16.  hd even.
+ */
+moe_status_t moe_rope_kv_append(const float* qkv, const int32_t* pos, const int32_t* page_table,
+                                int64_t T, int32_t Hq, int32_t Hkv, int32_t hd, int32_t page,
+                                int32_t maxp, int64_t npages, double theta, moe_bf16_t* q_out,
+                                moe_bf16_t* k_cache, moe_bf16_t* v_cache, hipStream_t stream);
+
+/*
+ * Grouped-query decode attention over the paged cache (PagedAttention, with
+ * FlashAttention's one-pass softmax):
+ *   out[t, h, :] = sum_{s < ctx[t]} softmax_s(scale q[t,h,:] . K_s) V_s
+ * with K_s, V_s of KV head h / (Hq / Hkv) of token t's request.  q [T, Hq, hd]
+ * bf16, out [T, Hq * hd] bf16 (f32 softmax and accumulation).  ctx[t] in
+ * [1, maxp * page].  Supported: hd = 128, Hq / Hkv in {1, 2, 4, 8}, page a
+ * multiple of 8 (MOE_ERR_UNSUPPORTED otherwise).
+ */
+moe_status_t moe_attention_decode(const moe_bf16_t* q, const moe_bf16_t* k_cache,
+                                  const moe_bf16_t* v_cache, const int32_t* page_table,
+                                  const int32_t* ctx, int64_t T, int32_t Hq, int32_t Hkv,
+                                  int32_t hd, int32_t page, int32_t maxp, int64_t npages,
+                                  float scale, moe_bf16_t* out, hipStream_t stream);
+
 /* Bytes of scratch moe_forward_ex needs for these sizes (0 for invalid sizes). */
 size_t moe_workspace_size(int64_t T, int32_t d, int32_t ffn, int32_t E, int32_t k);
 

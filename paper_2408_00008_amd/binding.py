@@ -25,6 +25,7 @@ EXPORTS = (
     "moe_route", "moe_permute", "moe_swiglu_up", "moe_swiglu_down", "moe_grouped_swiglu",
     "moe_combine", "moe_forward", "moe_forward_ex", "moe_rmsnorm", "moe_workspace_size",
     "moe_swiglu_up_fp8", "moe_swiglu_down_fp8", "moe_forward_fp8_ex",
+    "moe_linear", "moe_rope_kv_append", "moe_attention_decode",
     "moe_set_gemm_variant", "moe_gemm_variant_for", "moe_status_string", "moe_last_error", "moe_version",
 )
 
@@ -66,6 +67,10 @@ def lib() -> ctypes.CDLL:
         "moe_swiglu_down_fp8": [p, p, p, p, p, p, i64, i32, i32, i32, i32, p, p],
         "moe_forward_fp8_ex": [p, p, p, p, p, p, p, p, p, i64, i32, i32, i32, i32, p, p, p, p,
                                sz, p],
+        "moe_linear": [p, p, i64, i32, i32, p, p],
+        "moe_rope_kv_append": [p, p, p, i64, i32, i32, i32, i32, i32, i64, ctypes.c_double, p, p,
+                               p, p],
+        "moe_attention_decode": [p, p, p, p, p, i64, i32, i32, i32, i32, i32, i64, f32, p, p],
     }
     for name, args in sig.items():
         fn = getattr(L, name)
@@ -216,6 +221,36 @@ def moe_forward_fp8_ex(x, router_w, w1q, w1s, w3q, w3s, w2q, w2s, k, out=None, o
         _ptr(w2q, u8, "w2q"), _ptr(w2s, f32, "w2s"), T, d, ffn, E, k,
         _ptr(residual, f32, "residual"), _ptr(out, bf16, "out"), _ptr(out_f32, f32, "out_f32"),
         _ptr(workspace, None, "workspace"), ws_bytes, _stream(stream)), "moe_forward_fp8_ex")
+
+
+def moe_linear(x, w, y, stream=None):
+    """y [T, N] f32 = x [T, K] bf16 . w [N, K]^T bf16."""
+    T, K = x.shape
+    N = w.shape[0]
+    _check(lib().moe_linear(_ptr(x, bf16, "x"), _ptr(w, bf16, "w"), T, K, N, _ptr(y, f32, "y"),
+                            _stream(stream)), "moe_linear")
+
+
+def moe_rope_kv_append(qkv, pos, page_table, Hq, Hkv, theta, q_out, k_cache, v_cache, stream=None):
+    """qkv [T, (Hq+2Hkv) hd] f32; caches [npages, Hkv, page, hd] bf16."""
+    T = qkv.shape[0]
+    npages, _, page, hd = k_cache.shape
+    _check(lib().moe_rope_kv_append(
+        _ptr(qkv, f32, "qkv"), _ptr(pos, i32, "pos"), _ptr(page_table, i32, "page_table"), T, Hq,
+        Hkv, hd, page, page_table.shape[1], npages, float(theta), _ptr(q_out, bf16, "q_out"),
+        _ptr(k_cache, bf16, "k_cache"), _ptr(v_cache, bf16, "v_cache"), _stream(stream)),
+        "moe_rope_kv_append")
+
+
+def moe_attention_decode(q, k_cache, v_cache, page_table, ctx, scale, out, stream=None):
+    """q [T, Hq, hd] bf16; out [T, Hq*hd] bf16."""
+    T, Hq, hd = q.shape
+    npages, Hkv, page, _ = k_cache.shape
+    _check(lib().moe_attention_decode(
+        _ptr(q, bf16, "q"), _ptr(k_cache, bf16, "k_cache"), _ptr(v_cache, bf16, "v_cache"),
+        _ptr(page_table, i32, "page_table"), _ptr(ctx, i32, "ctx"), T, Hq, Hkv, hd, page,
+        page_table.shape[1], npages, float(scale), _ptr(out, bf16, "out"), _stream(stream)),
+        "moe_attention_decode")
 
 
 def moe_rmsnorm(h, gamma, eps, a, stream=None):

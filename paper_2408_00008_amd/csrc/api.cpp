@@ -8,6 +8,7 @@
 #include <atomic>
 #include <cstdarg>
 #include <cstdio>
+#include <cmath>
 #include <cstring>
 #include <mutex>
 #include <vector>
@@ -498,6 +499,30 @@ ExpertWeights fp8_weights(const uint8_t* q1, const float* s1, const uint8_t* q3,
 
 }  // namespace
 
+namespace {
+constexpr int kMaxHeads = 256, kMaxHd = 1024;
+
+moe_status_t check_heads(int32_t Hq, int32_t Hkv, int32_t hd)
+{
+    if (Hq < 1 || Hkv < 1 || Hq % Hkv)
+        return fail(MOE_ERR_INVALID_ARG, "Hq=%d must be a positive multiple of Hkv=%d", Hq, Hkv);
+    if (Hq > kMaxHeads) return fail(MOE_ERR_UNSUPPORTED, "Hq=%d exceeds %d", Hq, kMaxHeads);
+    if (hd < 2 || hd % 2 || hd > kMaxHd)
+        return fail(MOE_ERR_INVALID_ARG, "hd=%d must be even, 2..%d", hd, kMaxHd);
+    return MOE_OK;
+}
+
+moe_status_t check_cache(int32_t page, int32_t maxp, int64_t npages)
+{
+    if (page < 1 || maxp < 1 || npages < 1)
+        return fail(MOE_ERR_INVALID_ARG, "page=%d, maxp=%d, npages=%lld must be >= 1", page, maxp,
+                    (long long)npages);
+    if ((int64_t)page * maxp >= (int64_t(1) << 31) || npages >= (int64_t(1) << 31))
+        return fail(MOE_ERR_UNSUPPORTED, "cache geometry too large");
+    return MOE_OK;
+}
+}  // namespace
+
 extern "C" {
 
 moe_status_t moe_route(const moe_bf16_t* x, const moe_bf16_t* router_w, const float* router_bias,
@@ -688,6 +713,89 @@ moe_status_t moe_rmsnorm(const float* h, const moe_bf16_t* gamma, int64_t T, int
     if (T == 0) return ok();
     hipError_t e = moe::launch_rmsnorm(h, gamma, T, d, eps, a, stream);
     return e == hipSuccess ? ok() : hip_fail(e, "rmsnorm kernel launch");
+}
+
+moe_status_t moe_linear(const moe_bf16_t* x, const moe_bf16_t* w, int64_t T, int32_t K, int32_t N,
+                        float* y, hipStream_t stream)
+{
+    TRY(check_T(T, 1));
+    TRY(check_dim("K", K));
+    TRY(check_dim("N", N));
+    TRY(need_rows(x, "x", T));
+    TRY(need(w, "w"));
+    TRY(need_rows(y, "y", T));
+    TRY(no_overlap("y", {y, (size_t)T * N * 4}, {{"x", {x, (size_t)T * K * 2}},
+                   {"w", {w, (size_t)N * K * 2}}}));
+    if (T == 0) return ok();
+    // one matrix through the weight-streaming kernel: offsets NULL
+    moe::DownArgs a{x, nullptr, w, nullptr, nullptr, y, T, N, K, 1};
+    hipError_t e = moe::launch_stream_down(a, T, stream);
+    return e == hipSuccess ? ok() : hip_fail(e, "linear kernel launch");
+}
+
+
+moe_status_t moe_rope_kv_append(const float* qkv, const int32_t* pos, const int32_t* page_table,
+                                int64_t T, int32_t Hq, int32_t Hkv, int32_t hd, int32_t page,
+                                int32_t maxp, int64_t npages, double theta, moe_bf16_t* q_out,
+                                moe_bf16_t* k_cache, moe_bf16_t* v_cache, hipStream_t stream)
+{
+    TRY(check_T(T, Hq + 2 * Hkv));
+    TRY(check_heads(Hq, Hkv, hd));
+    TRY(check_cache(page, maxp, npages));
+    if (!(theta > 0.0) || !std::isfinite(theta)) return fail(MOE_ERR_INVALID_ARG, "theta must be > 0");
+    TRY(need_rows(qkv, "qkv", T));
+    TRY(need_rows(pos, "pos", T));
+    TRY(need_rows(page_table, "page_table", T));
+    TRY(need_rows(q_out, "q_out", T));
+    TRY(need(k_cache, "k_cache"));
+    TRY(need(v_cache, "v_cache"));
+    const size_t cache = (size_t)npages * Hkv * page * hd * 2;
+    const Range rk{k_cache, cache}, rv{v_cache, cache}, rq{q_out, (size_t)T * Hq * hd * 2};
+    const std::initializer_list<std::pair<const char*, Range>> ins = {
+        {"qkv", {qkv, (size_t)T * (Hq + 2 * Hkv) * hd * 4}}, {"pos", {pos, (size_t)T * 4}},
+        {"page_table", {page_table, (size_t)T * maxp * 4}}};
+    TRY(no_overlap("q_out", rq, ins));
+    TRY(no_overlap("k_cache", rk, ins));
+    TRY(no_overlap("v_cache", rv, ins));
+    TRY(no_overlap("k_cache", rk, {{"v_cache", rv}, {"q_out", rq}}));
+    TRY(no_overlap("v_cache", rv, {{"q_out", rq}}));
+    if (T == 0) return ok();
+    hipError_t e = moe::launch_rope_append(qkv, pos, page_table, maxp, static_cast<int>(npages), T,
+                                           Hq, Hkv, hd, page, theta, q_out, k_cache, v_cache,
+                                           stream);
+    return e == hipSuccess ? ok() : hip_fail(e, "rope/append kernel launch");
+}
+
+moe_status_t moe_attention_decode(const moe_bf16_t* q, const moe_bf16_t* k_cache,
+                                  const moe_bf16_t* v_cache, const int32_t* page_table,
+                                  const int32_t* ctx, int64_t T, int32_t Hq, int32_t Hkv,
+                                  int32_t hd, int32_t page, int32_t maxp, int64_t npages,
+                                  float scale, moe_bf16_t* out, hipStream_t stream)
+{
+    TRY(check_T(T, Hkv));
+    TRY(check_heads(Hq, Hkv, hd));
+    TRY(check_cache(page, maxp, npages));
+    if (!moe::attention_supported(Hq, Hkv, hd, page))
+        return fail(MOE_ERR_UNSUPPORTED,
+                    "attention needs hd = 128, Hq/Hkv in {1, 2, 4, 8} and page a multiple of 8 "
+                    "(got hd=%d, Hq=%d, Hkv=%d, page=%d)", hd, Hq, Hkv, page);
+    if (!(scale > 0.0f) || !std::isfinite(scale)) return fail(MOE_ERR_INVALID_ARG, "scale must be > 0");
+    TRY(need_rows(q, "q", T));
+    TRY(need(k_cache, "k_cache"));
+    TRY(need(v_cache, "v_cache"));
+    TRY(need_rows(page_table, "page_table", T));
+    TRY(need_rows(ctx, "ctx", T));
+    TRY(need_rows(out, "out", T));
+    const size_t cache = (size_t)npages * Hkv * page * hd * 2;
+    TRY(no_overlap("out", {out, (size_t)T * Hq * hd * 2},
+                   {{"q", {q, (size_t)T * Hq * hd * 2}}, {"k_cache", {k_cache, cache}},
+                    {"v_cache", {v_cache, cache}}, {"page_table", {page_table, (size_t)T * maxp * 4}},
+                    {"ctx", {ctx, (size_t)T * 4}}}));
+    if (T == 0) return ok();
+    hipError_t e = moe::launch_attention_decode(q, k_cache, v_cache, page_table, maxp,
+                                                static_cast<int>(npages), ctx, T, Hq, Hkv, page,
+                                                scale, out, stream);
+    return e == hipSuccess ? ok() : hip_fail(e, "attention kernel launch");
 }
 
 int moe_gemm_variant_for(int64_t T, int32_t d, int32_t ffn, int32_t E, int32_t k)

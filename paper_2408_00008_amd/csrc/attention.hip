@@ -1,0 +1,263 @@
+// Attention of one decode step over a paged KV cache, gfx950: the rotary
+// position embedding of the new token's query and key, its key/value append
+// to the cache, and grouped-query attention of every query head over its
+// request's cached positions.
+//
+// Cache layout: [pages, Hkv, page, hd] bf16 for keys and values alike, so one
+// page of one KV head (page * hd values) is contiguous.  Position s of the
+// request of token t lives in page page_table[t * maxp + s / page], slot
+// s % page.
+//
+// Decode attention is bound by reading the cache (2 * hd * 2 bytes per
+// position and KV head): every cached byte is read once, and the query heads
+// that share a KV head (the GQA group) are all served from that one read.
+#include "common.hpp"
+#include "launch.hpp"
+
+namespace moe {
+
+namespace {
+
+// One thread per (token, head, pair i < hd/2) over the Hq query, Hkv key and
+// Hkv value heads of qkv [T, (Hq + 2 Hkv) hd] (f32 projections).  Query and
+// key heads are rotated: element i pairs with i + hd/2, angle
+// pos * theta^(-2i/hd), computed in double (positions reach tens of
+// thousands, where a float angle would be off by ~1e-3 rad), then the pair is
+// rotated in f32.  Queries go to q_out [T, Hq, hd]; keys and values into the
+// cache at the token's position, all rounded to bf16.
+__global__ __launch_bounds__(256) void rope_append_kernel(const float* qkv, const int32_t* pos,
+                                                          const int32_t* page_table, int maxp,
+                                                          int npages, int64_t T, int Hq, int Hkv,
+                                                          int hd, int page, double theta,
+                                                          bf16_t* q_out, bf16_t* kc, bf16_t* vc)
+{
+    const int half = hd / 2;
+    const int nh = Hq + 2 * Hkv;
+    const int64_t idx = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (idx >= T * nh * half) return;
+    const int64_t t = idx / (nh * half);
+    const int r = static_cast<int>(idx - t * nh * half);
+    const int head = r / half, i = r - head * half;
+    const int p = pos[t];
+    const float* src = qkv + (t * nh + head) * hd;
+    float a = src[i], b = src[i + half];
+    if (head < Hq + Hkv) {
+        double s, c;
+        sincos(static_cast<double>(p) * pow(theta, -2.0 * i / hd), &s, &c);
+        const float cf = static_cast<float>(c), sf = static_cast<float>(s);
+        const float ra = a * cf - b * sf, rb = b * cf + a * sf;
+        a = ra;
+        b = rb;
+    }
+    bf16_t* dst;
+    if (head < Hq) {
+        dst = q_out + (t * Hq + head) * hd;
+    } else {
+        // a position or page outside the cache (invalid input) writes nothing
+        if (p < 0 || p >= maxp * page) return;
+        const int64_t pg = page_table[t * maxp + p / page];
+        if (pg < 0 || pg >= npages) return;
+        const bool key = head < Hq + Hkv;
+        const int g = key ? head - Hq : head - Hq - Hkv;
+        dst = (key ? kc : vc) + ((pg * Hkv + g) * page + p % page) * hd;
+    }
+    dst[i] = f32_to_bf16(a);
+    dst[i + half] = f32_to_bf16(b);
+}
+
+constexpr int HD = 128;   // head dimension of these kernels
+constexpr int LPP = 8;    // lanes per position: 16 dims each
+constexpr int DPL = HD / LPP;
+constexpr int NWAVE = 4;  // waves per workgroup
+
+__device__ __forceinline__ void widen16(const uint4& lo, const uint4& hi, float* f)
+{
+    const uint32_t w[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        f[2 * j] = __uint_as_float(w[j] << 16);
+        f[2 * j + 1] = __uint_as_float(w[j] & 0xFFFF0000u);
+    }
+}
+
+// One workgroup per (token t, KV head g); the GROUP query heads of g share
+// every key/value read.  A wave takes blocks of 8 positions (8 lanes per
+// position, 16 dims per lane) and keeps, per lane group, its own running max,
+// sum and weighted value sum (online softmax in base 2: the query is
+// pre-scaled by scale * log2(e)); two blocks are loaded before either is
+// used.  The lane groups are merged by shuffles, the waves through LDS.
+template <int GROUP>
+__global__ __launch_bounds__(NWAVE * 64) void attn_decode_kernel(
+    const bf16_t* q, const bf16_t* kc, const bf16_t* vc, const int32_t* page_table, int maxp,
+    const int32_t* ctx, int npages, int Hq, int Hkv, int page, float scale, bf16_t* out)
+{
+    __shared__ float s_acc[NWAVE][GROUP][HD];
+    __shared__ float s_ml[NWAVE][GROUP][2];
+    const int t = blockIdx.x / Hkv, g = blockIdx.x - t * Hkv;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int sub = lane & (LPP - 1), pp = lane / LPP;
+    // a context outside [1, maxp * page] or a page id outside the cache
+    // (invalid input) is clamped: no read leaves the cache
+    const int L = min(max(ctx[t], 1), maxp * page);
+    const float qs = scale * 1.44269504088896340736f;  // scores in base 2
+
+    float qv[GROUP][DPL];
+#pragma unroll
+    for (int h = 0; h < GROUP; ++h) {
+        const bf16_t* qr = q + ((int64_t)t * Hq + g * GROUP + h) * HD + DPL * sub;
+        float f[DPL];
+        widen16(ldg16(qr), ldg16(qr + 8), f);
+#pragma unroll
+        for (int i = 0; i < DPL; ++i) qv[h][i] = f[i] * qs;
+    }
+    float m[GROUP], l[GROUP], acc[GROUP][DPL];
+#pragma unroll
+    for (int h = 0; h < GROUP; ++h) {
+        m[h] = -INFINITY;
+        l[h] = 0.0f;
+#pragma unroll
+        for (int i = 0; i < DPL; ++i) acc[h][i] = 0.0f;
+    }
+
+    const int nblk = (L + 7) / 8;
+    auto addr = [&](int b) {
+        int s = 8 * b + pp;
+        s = s < L ? s : L - 1;  // dead positions read the last one (not used)
+        int64_t pg = page_table[(int64_t)t * maxp + s / page];
+        pg = pg < 0 ? 0 : (pg >= npages ? npages - 1 : pg);
+        return ((pg * Hkv + g) * page + s % page) * HD + DPL * sub;
+    };
+    auto update = [&](int b, const uint4* kv) {
+        if (8 * b + pp >= L) return;  // uniform over the lane group
+        float kf[DPL], vf[DPL];
+        widen16(kv[0], kv[1], kf);
+        widen16(kv[2], kv[3], vf);
+        float sd[GROUP];
+#pragma unroll
+        for (int h = 0; h < GROUP; ++h) {
+            float d = 0.0f;
+#pragma unroll
+            for (int i = 0; i < DPL; ++i) d = fmaf(qv[h][i], kf[i], d);
+            sd[h] = d;
+        }
+#pragma unroll
+        for (int o = 1; o < LPP; o <<= 1)
+#pragma unroll
+            for (int h = 0; h < GROUP; ++h) sd[h] += __shfl_xor(sd[h], o, 64);
+#pragma unroll
+        for (int h = 0; h < GROUP; ++h) {
+            const float mn = fmaxf(m[h], sd[h]);
+            const float cold = exp2f(m[h] - mn);  // 0 while nothing was seen (m = -inf)
+            const float p = exp2f(sd[h] - mn);
+            l[h] = fmaf(l[h], cold, p);
+#pragma unroll
+            for (int i = 0; i < DPL; ++i) acc[h][i] = fmaf(acc[h][i], cold, p * vf[i]);
+            m[h] = mn;
+        }
+    };
+    for (int b = wave; b < nblk; b += 2 * NWAVE) {
+        const int b2 = b + NWAVE;
+        const int64_t o1 = addr(b), o2 = addr(b2 < nblk ? b2 : b);
+        uint4 kv1[4] = {ldg16(kc + o1), ldg16(kc + o1 + 8), ldg16(vc + o1), ldg16(vc + o1 + 8)};
+        uint4 kv2[4] = {ldg16(kc + o2), ldg16(kc + o2 + 8), ldg16(vc + o2), ldg16(vc + o2 + 8)};
+        update(b, kv1);
+        if (b2 < nblk) update(b2, kv2);
+    }
+
+    // merge the 8 lane groups of the wave (same dims, disjoint positions)
+#pragma unroll
+    for (int o = LPP; o < 64; o <<= 1) {
+#pragma unroll
+        for (int h = 0; h < GROUP; ++h) {
+            const float mo = __shfl_xor(m[h], o, 64);
+            const float lo = __shfl_xor(l[h], o, 64);
+            const float mn = fmaxf(m[h], mo);
+            const float ca = mn == -INFINITY ? 0.0f : exp2f(m[h] - mn);
+            const float cb = mn == -INFINITY ? 0.0f : exp2f(mo - mn);
+            l[h] = l[h] * ca + lo * cb;
+#pragma unroll
+            for (int i = 0; i < DPL; ++i) {
+                const float ao = __shfl_xor(acc[h][i], o, 64);
+                acc[h][i] = acc[h][i] * ca + ao * cb;
+            }
+            m[h] = mn;
+        }
+    }
+    if (pp == 0) {
+#pragma unroll
+        for (int h = 0; h < GROUP; ++h) {
+#pragma unroll
+            for (int i = 0; i < DPL; ++i) s_acc[wave][h][DPL * sub + i] = acc[h][i];
+            if (sub == 0) {
+                s_ml[wave][h][0] = m[h];
+                s_ml[wave][h][1] = l[h];
+            }
+        }
+    }
+    __syncthreads();
+    // merge the waves and normalise: one thread per (head, dim)
+    for (int j = tid; j < GROUP * HD; j += NWAVE * 64) {
+        const int h = j / HD, dd = j - h * HD;
+        float mt = -INFINITY;
+#pragma unroll
+        for (int w = 0; w < NWAVE; ++w) mt = fmaxf(mt, s_ml[w][h][0]);
+        float lt = 0.0f, at = 0.0f;
+#pragma unroll
+        for (int w = 0; w < NWAVE; ++w) {
+            const float c = exp2f(s_ml[w][h][0] - mt);  // an empty wave has m = -inf: 0
+            lt = fmaf(s_ml[w][h][1], c, lt);
+            at = fmaf(s_acc[w][h][dd], c, at);
+        }
+        out[((int64_t)t * Hq + g * GROUP + h) * HD + dd] = f32_to_bf16(at / lt);
+    }
+}
+
+}  // namespace
+
+bool attention_supported(int Hq, int Hkv, int hd, int page)
+{
+    if (hd != HD || Hkv < 1 || Hq % Hkv || page < 8 || page % 8) return false;
+    const int group = Hq / Hkv;
+    return group == 1 || group == 2 || group == 4 || group == 8;
+}
+
+hipError_t launch_rope_append(const float* qkv, const int32_t* pos, const int32_t* page_table,
+                              int maxp, int npages, int64_t T, int Hq, int Hkv, int hd, int page,
+                              double theta, bf16_t* q_out, bf16_t* kc, bf16_t* vc,
+                              hipStream_t stream)
+{
+    const int64_t n = T * (Hq + 2 * Hkv) * (hd / 2);
+    const unsigned blocks = static_cast<unsigned>((n + 255) / 256);
+    rope_append_kernel<<<blocks, 256, 0, stream>>>(qkv, pos, page_table, maxp, npages, T, Hq, Hkv,
+                                                   hd, page, theta, q_out, kc, vc);
+    return hipGetLastError();
+}
+
+hipError_t launch_attention_decode(const bf16_t* q, const bf16_t* kc, const bf16_t* vc,
+                                   const int32_t* page_table, int maxp, int npages,
+                                   const int32_t* ctx, int64_t T, int Hq, int Hkv, int page,
+                                   float scale, bf16_t* out, hipStream_t stream)
+{
+    const unsigned blocks = static_cast<unsigned>(T * Hkv);
+    switch (Hq / Hkv) {
+    case 1:
+        attn_decode_kernel<1><<<blocks, NWAVE * 64, 0, stream>>>(q, kc, vc, page_table, maxp, ctx,
+                                                                 npages, Hq, Hkv, page, scale, out);
+        break;
+    case 2:
+        attn_decode_kernel<2><<<blocks, NWAVE * 64, 0, stream>>>(q, kc, vc, page_table, maxp, ctx,
+                                                                 npages, Hq, Hkv, page, scale, out);
+        break;
+    case 4:
+        attn_decode_kernel<4><<<blocks, NWAVE * 64, 0, stream>>>(q, kc, vc, page_table, maxp, ctx,
+                                                                 npages, Hq, Hkv, page, scale, out);
+        break;
+    default:
+        attn_decode_kernel<8><<<blocks, NWAVE * 64, 0, stream>>>(q, kc, vc, page_table, maxp, ctx,
+                                                                 npages, Hq, Hkv, page, scale, out);
+        break;
+    }
+    return hipGetLastError();
+}
+
+}  // namespace moe

@@ -52,7 +52,18 @@ struct StreamParams {
     const int32_t* perm;     // DOWN
     int passes;              // workgroups per slab (each takes every passes-th pass)
     int mlo, mhi;            // experts with mlo <= rows <= mhi only
+    int rows;                // dense (offsets null): one matrix, rows [0, rows)
 };
+
+// rows of expert e and its first row (dense: one matrix holding every row)
+__device__ __forceinline__ int expert_rows(const StreamParams& p, int e)
+{
+    return p.offsets ? p.offsets[e + 1] - p.offsets[e] : (e == 0 ? p.rows : 0);
+}
+__device__ __forceinline__ int expert_row0(const StreamParams& p, int e)
+{
+    return p.offsets ? p.offsets[e] : 0;
+}
 
 // SPLIT (UP only): waves ns < NS/2 stream w1 rows, waves ns >= NS/2 the same
 // rows of w3; u and v meet in LDS for the SiLU*mul epilogue.  Each wave then
@@ -357,7 +368,7 @@ __global__ __launch_bounds__(64 * NS * KS) void stream_kernel(StreamParams p)
         const int t = threadIdx.x;
         int items = 0;
         if (t < p.E) {
-            const int Mt = p.offsets[t + 1] - p.offsets[t];
+            const int Mt = expert_rows(p, t);
             const int P = (Mt + C::MT - 1) / C::MT;
             if (Mt >= p.mlo && Mt <= p.mhi) items = nbn8 * (P < p.passes ? P : p.passes);
         }
@@ -383,8 +394,8 @@ __global__ __launch_bounds__(64 * NS * KS) void stream_kernel(StreamParams p)
     }
     int e = 0;
     while (s_first[e + 1] <= b) ++e;
-    const int row0 = p.offsets[e];
-    const int M = p.offsets[e + 1] - row0;
+    const int row0 = expert_row0(p, e);
+    const int M = expert_rows(p, e);
     const int npass = (M + C::MT - 1) / C::MT;
     const int nslot = npass < p.passes ? npass : p.passes;
     const int local = b - s_first[e];
@@ -544,7 +555,18 @@ hipError_t launch_stream_down(const DownArgs& a, int64_t rows_max, hipStream_t s
     p.perm = a.perm;
     p.mlo = a.mlo;
     p.mhi = a.mhi;
+    p.rows = static_cast<int>(a.A);
     const int G = a.groups ? a.groups : stream_groups(a.A, a.E, rows_max);
+    if (!a.offsets) {
+        // dense projection (one matrix): 4 output-row waves x 4 reduction
+        // shares, so that even a 4096-row matrix spreads over 64+ workgroups
+        // of 16 waves; 64-row passes (more rows take more passes)
+        if (a.ffn % 256 == 0) {
+            if (G == 2) return run<false, 4, 4, 2, 64>(p, rows_max, stream);
+            return run<false, 4, 4, 4, 64>(p, rows_max, stream);
+        }
+        return run<false, 4, 1, 4, 64>(p, rows_max, stream);
+    }
     if (a.q2) {
         if (G == 2) {
             if (a.d % 128 == 0 && a.ffn % 256 == 0)

@@ -30,6 +30,19 @@ hipError_t launch_combine(const float* y, const float* residual, int64_t T, int 
 hipError_t launch_rmsnorm(const float* h, const bf16_t* gamma, int64_t T, int d, float eps,
                           bf16_t* a, hipStream_t stream);
 
+// Decode attention (attention.hip): RoPE of the new token's query/key heads
+// and the key/value append to the paged cache; grouped-query attention over
+// the cache.  Cache layout [pages, Hkv, page, hd] bf16.
+bool attention_supported(int Hq, int Hkv, int hd, int page);
+hipError_t launch_rope_append(const float* qkv, const int32_t* pos, const int32_t* page_table,
+                              int maxp, int npages, int64_t T, int Hq, int Hkv, int hd, int page,
+                              double theta, bf16_t* q_out, bf16_t* kc, bf16_t* vc,
+                              hipStream_t stream);
+hipError_t launch_attention_decode(const bf16_t* q, const bf16_t* kc, const bf16_t* vc,
+                                   const int32_t* page_table, int maxp, int npages,
+                                   const int32_t* ctx, int64_t T, int Hq, int Hkv, int page,
+                                   float scale, bf16_t* out, hipStream_t stream);
+
 // Expert GEMMs.  `rows_hint` = T*k (an upper bound of any expert's rows) picks
 // the tile shape; the real per-expert row counts are read on the device.
 struct UpArgs {

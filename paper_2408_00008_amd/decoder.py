@@ -1,0 +1,177 @@
+"""One decoder layer of the served model (Mixtral-8x7B) for a decode step,
+sequenced on the device through the C ABI of libmoe.
+
+Per token t (one per request; the new token sits at position pos[t]):
+
+    a   = bf16(RMSNorm(h) * gamma_attn)              moe_rmsnorm
+    qkv = a [Wq; Wk; Wv]^T                            moe_linear (one fused matrix)
+    RoPE(q, k); k, v -> paged cache                   moe_rope_kv_append
+    o   = attention over the request's positions      moe_attention_decode
+    h  += o Wo^T                                      moe_linear + moe_combine (k = 1)
+    h  += MoE(bf16(RMSNorm(h) * gamma_moe))           moe_rmsnorm + moe_forward_ex
+
+h is the float32 residual stream and is updated in place.  Every step runs in
+the library's HIP kernels; torch only provides the buffers and the stream.
+The sequence issues no host synchronisation, so a step can be captured into a
+HIP graph.
+"""
+
+from __future__ import annotations
+
+import math
+
+import torch
+
+from . import binding as B
+
+
+class DecoderLayer:
+    """Weights of one layer, kept resident: the query/key/value projections
+    are stored as one [(hq + 2 hkv) hd, d] matrix (a layout choice made once,
+    at load time), so one streaming GEMM reads them all."""
+
+    def __init__(self, attn: dict, moe: dict, hq: int, hkv: int, k: int, theta: float,
+                 eps: float = 1e-5):
+        self.wqkv = torch.cat([attn["wq"], attn["wk"], attn["wv"]], dim=0).contiguous()
+        self.wo = attn["wo"].contiguous()
+        self.gamma_attn, self.gamma_moe = attn["gamma_attn"], attn["gamma_moe"]
+        self.router_w, self.router_bias = moe["router_w"], moe.get("router_bias")
+        self.w1, self.w3, self.w2 = moe["w1"], moe["w3"], moe["w2"]
+        self.hq, self.hkv, self.k, self.theta, self.eps = hq, hkv, k, theta, eps
+        self.d = self.wo.shape[0]
+        self.hd = self.wo.shape[1] // hq
+        self._bufs = {}
+
+    def buffers(self, T: int, device):
+        """Per-step scratch for T tokens (allocated once per T)."""
+        if T not in self._bufs:
+            d, nqkv, nq = self.d, self.wqkv.shape[0], self.hq * self.hd
+            self._bufs[T] = {
+                "a": torch.empty(T, d, dtype=torch.bfloat16, device=device),
+                "qkv": torch.empty(T, nqkv, dtype=torch.float32, device=device),
+                "q": torch.empty(T, self.hq, self.hd, dtype=torch.bfloat16, device=device),
+                "attn": torch.empty(T, nq, dtype=torch.bfloat16, device=device),
+                "o": torch.empty(T, d, dtype=torch.float32, device=device),
+                "a2": torch.empty(T, d, dtype=torch.bfloat16, device=device),
+            }
+        return self._bufs[T]
+
+    def step(self, h, k_cache, v_cache, page_table, pos, ctx, stream=None):
+        """One decode step for the T tokens of h [T, d] (float32, updated in
+        place).  pos [T]: the new token's position; ctx [T] = pos + 1, the
+        positions attended (engine metadata, like the page table)."""
+        T = h.shape[0]
+        b = self.buffers(T, h.device)
+        B.moe_rmsnorm(h, self.gamma_attn, self.eps, b["a"], stream=stream)
+        B.moe_linear(b["a"], self.wqkv, b["qkv"], stream=stream)
+        B.moe_rope_kv_append(b["qkv"], pos, page_table, self.hq, self.hkv, self.theta, b["q"],
+                             k_cache, v_cache, stream=stream)
+        B.moe_attention_decode(b["q"], k_cache, v_cache, page_table, ctx,
+                               1.0 / math.sqrt(self.hd), b["attn"], stream=stream)
+        B.moe_linear(b["attn"], self.wo, b["o"], stream=stream)
+        B.moe_combine(b["o"], T, self.d, 1, out_f32=h, residual=h, stream=stream)
+        B.moe_rmsnorm(h, self.gamma_moe, self.eps, b["a2"], stream=stream)
+        B.moe_forward_ex(b["a2"], self.router_w, self.w1, self.w3, self.w2, self.k, out_f32=h,
+                         router_bias=self.router_bias, residual=h, stream=stream)
+        return h
+
+
+def bench_decoder(args, w):
+    """bench.py for a decoder-layer workload: one decode step of the layer
+    for w.T requests; prints one JSON line.  Each step rewrites the same
+    cache slot and advances h, so every step does the same work."""
+    import json
+    import time
+
+    import numpy as np
+
+    from . import inputs
+
+    HBM_PEAK_GBS = 8000.0
+    dev = "cuda:0"
+    attn = inputs.make_attention(w, 0, dev)
+    moe = inputs.make_layer(w, 0, dev)
+    kv = inputs.make_kv_cache(w, 0, dev)
+    layer = DecoderLayer(attn, moe, w.hq, w.hkv, w.k, w.theta, w.eps)
+    h = inputs.make_h(w, dev)
+    stream = torch.cuda.current_stream()
+    T, d = w.T, w.d
+    b = layer.buffers(T, h.device)
+
+    def step(ev=None):
+        B.moe_rmsnorm(h, layer.gamma_attn, layer.eps, b["a"], stream=stream)
+        B.moe_linear(b["a"], layer.wqkv, b["qkv"], stream=stream)
+        B.moe_rope_kv_append(b["qkv"], kv["pos"], kv["page_table"], w.hq, w.hkv, w.theta, b["q"],
+                             kv["k_cache"], kv["v_cache"], stream=stream)
+        if ev is not None:
+            ev[0].record(stream)
+        B.moe_attention_decode(b["q"], kv["k_cache"], kv["v_cache"], kv["page_table"], kv["ctx"],
+                               1.0 / math.sqrt(layer.hd), b["attn"], stream=stream)
+        if ev is not None:
+            ev[1].record(stream)
+        B.moe_linear(b["attn"], layer.wo, b["o"], stream=stream)
+        B.moe_combine(b["o"], T, d, 1, out_f32=h, residual=h, stream=stream)
+        B.moe_rmsnorm(h, layer.gamma_moe, layer.eps, b["a2"], stream=stream)
+        B.moe_forward_ex(b["a2"], layer.router_w, layer.w1, layer.w3, layer.w2, layer.k, out_f32=h,
+                         router_bias=layer.router_bias, residual=h, stream=stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(args.steps)]
+    bounds = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    t0 = time.perf_counter()
+    bounds[0].record(stream)
+    for i in range(args.steps):
+        step(evs[i])
+        bounds[i + 1].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms = bounds[0].elapsed_time(bounds[-1]) / args.steps
+    step_ms = np.array([bounds[i].elapsed_time(bounds[i + 1]) for i in range(args.steps)])
+    attn_us = float(np.mean([a.elapsed_time(z) for a, z in evs])) * 1e3
+
+    # algorithmic bytes: every weight once (attention projections, router,
+    # the routed experts), the cached keys/values each request attends to,
+    # the new key/value rows and the residual stream in and out
+    ctx = kv["ctx"].cpu().numpy().astype(np.int64)
+    kv_bytes = int(ctx.sum()) * w.hkv * w.hd * 2 * 2
+    proj_bytes = (layer.wqkv.numel() + layer.wo.numel()) * 2
+    ids = torch.empty(T, w.k, dtype=torch.int32, device=dev)
+    gw = torch.empty(T, w.k, dtype=torch.float32, device=dev)
+    offs = torch.empty(w.E + 1, dtype=torch.int32, device=dev)
+    perm = torch.empty(T * w.k, dtype=torch.int32, device=dev)
+    B.moe_route(b["a2"], layer.router_w, w.k, ids, gw, offs, perm)
+    active = int((torch.diff(offs) > 0).sum())
+    moe_bytes = active * 3 * w.ffn * d * 2 + w.E * d * 2
+    step_bytes = proj_bytes + moe_bytes + kv_bytes + T * d * 4 * 2
+    gbs = step_bytes / (ms * 1e-3) / 1e9
+    attn_gbs = kv_bytes / (attn_us * 1e-6) / 1e9
+    rec = {
+        "metric": "decoder-layer tokens/s",
+        "value": round(T / (ms * 1e-3), 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "step_ms_p10_p50_p90": [round(float(np.percentile(step_ms, q)), 4) for q in (10, 50, 90)],
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded normals: one random-init Mixtral-8x7B decoder layer, random KV cache)",
+        "config": {"workload": args.workload, "T": T, "d": d, "ffn": w.ffn, "E": w.E, "k": w.k,
+                   "hq": w.hq, "hkv": w.hkv, "hd": w.hd, "page": w.page,
+                   "cached_positions": int(ctx.sum() - T), "active_experts": active},
+        "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": None,
+                     "kernel": "whole step (attention block + MoE block)",
+                     "algorithmic_bytes_per_launch": step_bytes},
+        "attention": {"avg_launch_us": round(attn_us, 2), "kv_bytes": kv_bytes,
+                      "achieved_gbs": round(attn_gbs, 1), "frac": round(attn_gbs / HBM_PEAK_GBS, 4)},
+        "cpu_baseline": None,
+        "wall_s_timed": round(wall, 3),
+    }
+    print(json.dumps(rec), flush=True)

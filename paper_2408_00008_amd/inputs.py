@@ -9,7 +9,9 @@ deviation, from its own ``torch.Generator`` seeded with
 ``seed * 65536 + layer * 16 + tensor_id`` and rounded to bfloat16 with
 round-to-nearest-even (the cast ``Tensor.to(torch.bfloat16)`` performs).
 
-Tensor ids: x=0, router_w=1, w1=2, w3=3, w2=4, gamma=5.
+Tensor ids: x=0, router_w=1, w1=2, w3=3, w2=4, gamma=5; for the decoder layer
+around the MoE block: wq=6, wk=7, wv=8, wo=9, gamma_attn=10, k_cache=11,
+v_cache=12, page assignment=13, cached lengths=14, residual stream h=15.
 
 Layouts follow ``nn.Linear`` (out x in, reduction dimension contiguous), the
 convention of Mixtral checkpoints:
@@ -40,6 +42,8 @@ from typing import Optional
 import torch
 
 TID_X, TID_ROUTER, TID_W1, TID_W3, TID_W2, TID_GAMMA = 0, 1, 2, 3, 4, 5
+TID_WQ, TID_WK, TID_WV, TID_WO, TID_GAMMA_ATTN = 6, 7, 8, 9, 10
+TID_KC, TID_VC, TID_PAGES, TID_LENS, TID_H = 11, 12, 13, 14, 15
 
 
 @dataclasses.dataclass(frozen=True)
@@ -62,6 +66,15 @@ class Workload:
     eps: float = 1e-5  # RMSNorm epsilon for stacks
     seed: int = 0
     fp8: bool = False  # expert weights as E4M3 bytes with per-row scales
+    # decoder layer around the MoE block (hq = 0: the MoE layer alone)
+    hq: int = 0          # query heads
+    hkv: int = 0         # key/value heads
+    hd: int = 128        # head dimension
+    page: int = 16       # KV-cache positions per page
+    ctx: int = 0         # positions already cached per request (the largest, if ragged)
+    ctx_ragged: bool = False  # cached lengths uniform in [0, ctx] instead of all ctx
+    theta: float = 1e6   # RoPE base
+    std_attn: float = 0.02  # std of the attention projections
 
     def replace(self, **kw) -> "Workload":
         return dataclasses.replace(self, **kw)
@@ -102,6 +115,11 @@ WORKLOADS = {
     # prefill chunk in one call
     "mixed_t576": Workload("mixed_t576", 576, MIXTRAL_D, MIXTRAL_FFN, MIXTRAL_E, MIXTRAL_K,
                            1.0, 0.02, 0.02, 0.02, 0.02),
+    # one decoder layer of Mixtral-8x7B (32 query heads, 8 KV heads of 128),
+    # decode step of 64 requests with 1024 positions cached each
+    "decoder_t64_ctx1024": Workload("decoder_t64_ctx1024", 64, MIXTRAL_D, MIXTRAL_FFN, MIXTRAL_E,
+                                    MIXTRAL_K, 1.0, 0.02, 0.02, 0.02, 0.02, hq=32, hkv=8,
+                                    ctx=1024),
     # 32 stacked layers, RMSNorm + residual around each, one decode step of 64
     "stack32_t64": Workload("stack32_t64", 64, MIXTRAL_D, MIXTRAL_FFN, MIXTRAL_E, MIXTRAL_K,
                             1.0, 0.02, 0.02, 0.02, 0.02, layers=32),
@@ -210,3 +228,51 @@ def from_bits(a, device="cpu") -> torch.Tensor:
 
     a = np.ascontiguousarray(a, dtype=np.uint16)
     return torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).to(device)
+
+
+# ---- the decoder layer around the MoE block -----------------------------------
+
+def make_attention(w: Workload, layer: int = 0, device="cpu") -> dict:
+    """Attention projections (nn.Linear layout) and the two RMSNorm scales:
+    wq [hq*hd, d], wk, wv [hkv*hd, d], wo [d, hq*hd] bf16 with std w.std_attn;
+    gamma_attn, gamma_moe U(0.5, 1.5) bf16."""
+    d, qd, kd = w.d, w.hq * w.hd, w.hkv * w.hd
+    g = _gen(w.seed, layer, TID_GAMMA_ATTN, device)
+    ga = (torch.rand(d, generator=g, device=device) + 0.5).to(torch.bfloat16)
+    return {"wq": randn_bf16((qd, d), w.std_attn, w.seed, layer, TID_WQ, device),
+            "wk": randn_bf16((kd, d), w.std_attn, w.seed, layer, TID_WK, device),
+            "wv": randn_bf16((kd, d), w.std_attn, w.seed, layer, TID_WV, device),
+            "wo": randn_bf16((d, qd), w.std_attn, w.seed, layer, TID_WO, device),
+            "gamma_attn": ga, "gamma_moe": make_gamma(w, layer, device, random=True)}
+
+
+def make_kv_cache(w: Workload, layer: int = 0, device="cpu") -> dict:
+    """A paged KV cache holding the requests' earlier positions.  Request t
+    has pos[t] positions cached (w.ctx, or uniform in [0, w.ctx]) and owns
+    maxp = ceil((w.ctx + 1) / page) pages, taken from a seeded permutation of
+    all T * maxp pages; its new token goes to position pos[t].  Cached keys
+    and values are N(0, 1) bf16 (every slot is filled; slots at or past a
+    request's position are never read before they are written).  Returns
+    k_cache, v_cache [T*maxp, hkv, page, hd] bf16, page_table [T, maxp] int32,
+    pos [T] and ctx = pos + 1 [T] int32."""
+    maxp = (w.ctx + 1 + w.page - 1) // w.page
+    npages = w.T * maxp
+    shape = (npages, w.hkv, w.page, w.hd)
+    kc = randn_bf16(shape, 1.0, w.seed, layer, TID_KC, device)
+    vc = randn_bf16(shape, 1.0, w.seed, layer, TID_VC, device)
+    gp = _gen(w.seed, layer, TID_PAGES, "cpu")
+    table = torch.randperm(npages, generator=gp).reshape(w.T, maxp).to(torch.int32)
+    if w.ctx_ragged:
+        gl = _gen(w.seed, layer, TID_LENS, "cpu")
+        pos = torch.randint(0, w.ctx + 1, (w.T,), generator=gl, dtype=torch.int32)
+    else:
+        pos = torch.full((w.T,), w.ctx, dtype=torch.int32)
+    return {"k_cache": kc, "v_cache": vc, "page_table": table.to(device), "pos": pos.to(device),
+            "ctx": (pos + 1).to(device)}
+
+
+def make_h(w: Workload, device="cpu") -> torch.Tensor:
+    """The residual stream entering the layer, float32 N(0, 1)."""
+    g = _gen(w.seed, 0, TID_H, device)
+    return torch.randn(w.T, w.d, generator=g, device=device, dtype=torch.float32)
+

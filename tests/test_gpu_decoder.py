@@ -1,0 +1,244 @@
+"""GPU parity of the decoder layer around the MoE block (one decode step)
+against the fp64 oracle: the dense projection, RoPE + KV-cache append,
+paged grouped-query decode attention, and the whole layer.
+
+Rounding points of the GPU path (readings of the layer's definition): the
+norm outputs, the rotated query, the cached keys/values and the attention
+output are bf16; projections, scores, softmax and the residual stream are
+f32.  Outputs are checked with the row-wise relative rule of the MoE layer;
+a layer's output is checked on its delta h_out - h_in (the residual
+dominates h itself), as for the stack."""
+
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from gpu_common import DEV, bf16_to_f64, orc, say
+from parity import OUT_TOL, check_routing, rowwise_rel
+from paper_2408_00008_amd import binding as B
+from paper_2408_00008_amd import inputs
+from paper_2408_00008_amd.decoder import DecoderLayer
+
+pytestmark = pytest.mark.gpu
+
+
+def bits(t):
+    return inputs.bf16_bits(t)
+
+
+def widen(b):
+    return (np.asarray(b).astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+
+
+def small_workload(T, d, hq, hkv, ctx, page=16, ffn=256, E=8, k=2, ragged=True, seed=0):
+    std = 1 / math.sqrt(d)
+    return inputs.Workload("dec", T, d, ffn, E, k, 1.0, std, std, std, 1 / math.sqrt(ffn), seed=seed,
+                           hq=hq, hkv=hkv, hd=128, page=page, ctx=ctx, ctx_ragged=ragged,
+                           std_attn=std)
+
+
+@pytest.mark.parametrize("T,K,N", [(1, 64, 64), (37, 512, 320), (64, 4096, 6144), (130, 256, 512),
+                                   (64, 448, 192)])
+def test_linear(T, K, N):
+    say(f"[decoder] linear T={T} K={K} N={N}")
+    g = torch.Generator(device=DEV).manual_seed(T + K + N)
+    x = torch.randn(T, K, generator=g, device=DEV).to(torch.bfloat16)
+    w = (torch.randn(N, K, generator=g, device=DEV) / math.sqrt(K)).to(torch.bfloat16)
+    y = torch.empty(T, N, dtype=torch.float32, device=DEV)
+    B.moe_linear(x, w, y)
+    torch.cuda.synchronize()
+    ref = widen(bits(x)) @ widen(bits(w)).T
+    err = rowwise_rel(y.cpu().numpy().astype(np.float64), ref)
+    say(f"  rowwise rel {err:.2e}")
+    assert err < 1e-5
+
+
+@pytest.mark.parametrize("hq,hkv,page", [(4, 1, 16), (8, 2, 8), (32, 8, 16)])
+def test_rope_append(hq, hkv, page):
+    say(f"[decoder] rope+append hq={hq} hkv={hkv} page={page}")
+    w = small_workload(9, 256, hq, hkv, ctx=70, page=page, seed=3)
+    kv = inputs.make_kv_cache(w, 0, DEV)
+    g = torch.Generator(device=DEV).manual_seed(7)
+    qkv = torch.randn(w.T, (hq + 2 * hkv) * 128, generator=g, device=DEV)
+    q = torch.empty(w.T, hq, 128, dtype=torch.bfloat16, device=DEV)
+    kc0, vc0 = bits(kv["k_cache"]), bits(kv["v_cache"])
+    B.moe_rope_kv_append(qkv, kv["pos"], kv["page_table"], hq, hkv, w.theta, q, kv["k_cache"],
+                         kv["v_cache"])
+    torch.cuda.synchronize()
+    o = orc()
+    pos = kv["pos"].cpu().numpy()
+    x = qkv.cpu().numpy().astype(np.float64).reshape(w.T, hq + 2 * hkv, 128)
+    q_ref = o.rope(x[:, :hq], pos, w.theta)
+    k_ref = o.rope(x[:, hq:hq + hkv], pos, w.theta)
+    # rounded once, to nearest-even bf16, from the exact rotation (f32 rotation on the GPU)
+    assert rowwise_rel(widen(bits(q)).reshape(w.T, -1), q_ref.reshape(w.T, -1)) < 1e-2
+    kc, vc = bits(kv["k_cache"]), bits(kv["v_cache"])
+    pt = kv["page_table"].cpu().numpy()
+    written = np.zeros(kc.shape[:1] + kc.shape[2:3], bool)  # [pages, slots]
+    for t in range(w.T):
+        pg, sl = pt[t, pos[t] // page], pos[t] % page
+        written[pg, sl] = True
+        assert rowwise_rel(widen(kc[pg, :, sl]), k_ref[t]) < 1e-2
+        assert np.array_equal(vc[pg, :, sl], o.round_bf16(x[t, hq + hkv:]))
+    # nothing else in the cache changed
+    mask = np.broadcast_to(written[:, None, :, None], kc.shape)
+    assert np.array_equal(kc[~mask], kc0[~mask]) and np.array_equal(vc[~mask], vc0[~mask])
+
+
+@pytest.mark.parametrize("hq,hkv,page,ctx", [
+    (4, 4, 16, 40),      # one query head per KV head
+    (8, 4, 8, 100),      # groups of 2, 8-position pages
+    (32, 8, 16, 300),    # Mixtral's groups of 4
+    (16, 2, 32, 70),     # groups of 8, 32-position pages
+])
+def test_attention(hq, hkv, page, ctx):
+    """Ragged cached lengths (including a single position) against the
+    oracle on the same query bits and cache."""
+    say(f"[decoder] attention hq={hq} hkv={hkv} page={page} ctx<={ctx}")
+    w = small_workload(11, 256, hq, hkv, ctx=ctx, page=page, seed=5)
+    kv = inputs.make_kv_cache(w, 0, DEV)
+    lens = kv["ctx"].clone()
+    lens[0] = 1
+    lens[1] = page
+    lens[2] = page + 1
+    lens[3] = min(ctx + 1, 2 * page + 3)
+    g = torch.Generator(device=DEV).manual_seed(9)
+    q = (torch.randn(w.T, hq, 128, generator=g, device=DEV) * 1.5).to(torch.bfloat16)
+    out = torch.empty(w.T, hq * 128, dtype=torch.bfloat16, device=DEV)
+    scale = 1 / math.sqrt(128)
+    B.moe_attention_decode(q, kv["k_cache"], kv["v_cache"], kv["page_table"], lens, scale, out)
+    torch.cuda.synchronize()
+    ref = orc().attention_decode(widen(bits(q)), bits(kv["k_cache"]), bits(kv["v_cache"]),
+                                 kv["page_table"].cpu().numpy(), lens.cpu().numpy(), scale)
+    err = rowwise_rel(bf16_to_f64(out).reshape(w.T * hq, 128), ref.reshape(w.T * hq, 128))
+    say(f"  rowwise rel over {w.T * hq} heads {err:.2e}")
+    assert err < OUT_TOL
+
+
+def test_attention_unsupported_shapes_rejected():
+    q = torch.zeros(1, 4, 64, dtype=torch.bfloat16, device=DEV)
+    kc = torch.zeros(2, 1, 16, 64, dtype=torch.bfloat16, device=DEV)
+    out = torch.empty(1, 256, dtype=torch.bfloat16, device=DEV)
+    pt = torch.zeros(1, 2, dtype=torch.int32, device=DEV)
+    ctx = torch.ones(1, dtype=torch.int32, device=DEV)
+    with pytest.raises(B.MoeError, match="UNSUPPORTED"):
+        B.moe_attention_decode(q, kc, kc.clone(), pt, ctx, 0.125, out)
+
+
+def _layer(w):
+    attn = inputs.make_attention(w, 0, DEV)
+    moe = inputs.make_layer(w, 0, DEV)
+    kv = inputs.make_kv_cache(w, 0, DEV)
+    return attn, moe, kv
+
+
+def _check_layer(w, rows):
+    """The GPU layer against the oracle, block by block on the GPU's own
+    block inputs: the attention block (h -> h1) on the layer input, the MoE
+    block on the GPU's h1 (a routing decision near a tie is judged by the
+    margin rule, as for the MoE layer)."""
+    attn, moe, kv = _layer(w)
+    h0 = inputs.make_h(w, DEV)
+    kc0, vc0 = bits(kv["k_cache"]), bits(kv["v_cache"])
+    kc, vc = kv["k_cache"].clone(), kv["v_cache"].clone()  # for the whole-layer run
+    layer = DecoderLayer(attn, moe, w.hq, w.hkv, w.k, w.theta)
+    # the attention block alone: the same sequence up to the first residual add
+    h1 = h0.clone()
+    b = layer.buffers(w.T, DEV)
+    B.moe_rmsnorm(h1, layer.gamma_attn, layer.eps, b["a"])
+    B.moe_linear(b["a"], layer.wqkv, b["qkv"])
+    B.moe_rope_kv_append(b["qkv"], kv["pos"], kv["page_table"], w.hq, w.hkv, w.theta, b["q"],
+                         kv["k_cache"], kv["v_cache"])
+    B.moe_attention_decode(b["q"], kv["k_cache"], kv["v_cache"], kv["page_table"], kv["ctx"],
+                           1 / math.sqrt(w.hd), b["attn"])
+    B.moe_linear(b["attn"], layer.wo, b["o"])
+    B.moe_combine(b["o"], w.T, w.d, 1, out_f32=h1, residual=h1)
+    # the whole layer from the same input and cache
+    h2 = h0.clone()
+    layer.step(h2, kc, vc, kv["page_table"], kv["pos"], kv["ctx"])
+    torch.cuda.synchronize()
+
+    o = orc()
+    h0n, h1n, h2n = (t.cpu().numpy() for t in (h0, h1, h2))
+    pt, pos = kv["page_table"].cpu().numpy(), kv["pos"].cpu().numpy()
+    sub = lambda a: a[rows]  # noqa: E731
+    ref = o.decoder_layer(sub(h0n), bits(attn["gamma_attn"]), bits(attn["wq"]), bits(attn["wk"]),
+                          bits(attn["wv"]), bits(attn["wo"]), kc0, vc0, sub(pt), sub(pos),
+                          bits(attn["gamma_moe"]), bits(moe["router_w"]), bits(moe["w1"]),
+                          bits(moe["w3"]), bits(moe["w2"]), w.k, w.hq, w.hkv, w.theta, w.eps)
+    e_attn = rowwise_rel(sub(h1n).astype(np.float64) - sub(h0n), ref["h1"] - sub(h0n))
+    # MoE block on the GPU's h1
+    a2 = o.round_bf16(o.rmsnorm(sub(h1n), bits(attn["gamma_moe"]), w.eps))
+    mo = o.moe_layer(a2, bits(moe["router_w"]), bits(moe["w1"]), bits(moe["w3"]), bits(moe["w2"]), w.k)
+    ids = torch.empty(w.T, w.k, dtype=torch.int32, device=DEV)
+    gw = torch.empty(w.T, w.k, dtype=torch.float32, device=DEV)
+    offs = torch.empty(w.E + 1, dtype=torch.int32, device=DEV)
+    perm = torch.empty(w.T * w.k, dtype=torch.int32, device=DEV)
+    B.moe_route(b["a2"], moe["router_w"], w.k, ids, gw, offs, perm)
+    torch.cuda.synchronize()
+    g_ids = ids.cpu().numpy()[rows]
+    amb = check_routing(g_ids, mo["logits"], w.k)
+    moe_ref = mo["out"]
+    if amb.any():
+        gates = o.gates_for_ids(mo["logits"], np.ascontiguousarray(g_ids, np.int32))
+        moe_ref = o.moe_apply(a2, bits(moe["w1"]), bits(moe["w3"]), bits(moe["w2"]), g_ids, gates)
+    e_moe = rowwise_rel(sub(h2n).astype(np.float64) - sub(h1n), moe_ref)
+    say(f"  {w.name}: attention block {e_attn:.2e}, MoE block {e_moe:.2e} over {len(rows)} tokens")
+    assert e_attn < OUT_TOL and e_moe < OUT_TOL
+    # the step wrote each request's new key/value row at its position, and only there
+    page = w.page
+    kcn = bits(kc)
+    for t in rows:
+        pg, sl = pt[t, pos[t] // page], pos[t] % page
+        assert rowwise_rel(widen(kcn[pg, :, sl]), ref["k_new"][list(rows).index(t)]) < 1e-2
+
+
+def test_decoder_layer_small():
+    say("[decoder] layer, ragged contexts")
+    w = small_workload(24, 512, 4, 2, ctx=90, page=16, ffn=512, seed=11)
+    _check_layer(w, np.arange(w.T))
+
+
+def test_decoder_layer_mixtral_decode():
+    """The Mixtral-8x7B layer (32 query / 8 KV heads, d = 4096), 64 requests
+    with 1024 cached positions each; sampled tokens."""
+    say("[decoder] layer, decoder_t64_ctx1024 (sampled tokens)")
+    w = inputs.WORKLOADS["decoder_t64_ctx1024"]
+    _check_layer(w, np.array([0, 9, 31, 63]))
+
+
+def test_decoder_step_graph_replays():
+    """The step issues no host synchronisation: captured into a HIP graph and
+    replayed on fresh inputs, it matches the eager step bitwise."""
+    say("[decoder] graph capture")
+    w = small_workload(16, 256, 4, 1, ctx=40, page=16, seed=13)
+    attn, moe, kv = _layer(w)
+    layer = DecoderLayer(attn, moe, w.hq, w.hkv, w.k, w.theta)
+    h0 = inputs.make_h(w, DEV)
+    kc0, vc0 = kv["k_cache"].clone(), kv["v_cache"].clone()
+    h_e = h0.clone()
+    layer.step(h_e, kv["k_cache"], kv["v_cache"], kv["page_table"], kv["pos"], kv["ctx"])
+    torch.cuda.synchronize()
+    kc_e = kv["k_cache"].clone()
+    # library scratch exists now; capture on a side stream
+    h_g = h0.clone()
+    s = torch.cuda.Stream()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(s):
+        kv["k_cache"].copy_(kc0)
+        kv["v_cache"].copy_(vc0)
+        torch.cuda.synchronize()
+        with torch.cuda.graph(graph, stream=s):
+            layer.step(h_g, kv["k_cache"], kv["v_cache"], kv["page_table"], kv["pos"], kv["ctx"],
+                       stream=s)
+    for _ in range(3):
+        h_g.copy_(h0)
+        kv["k_cache"].copy_(kc0)
+        kv["v_cache"].copy_(vc0)
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(h_g, h_e)
+        assert torch.equal(kv["k_cache"], kc_e)
