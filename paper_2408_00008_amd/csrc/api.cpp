@@ -775,10 +775,11 @@ moe_status_t moe_attention_decode(const moe_bf16_t* q, const moe_bf16_t* k_cache
     TRY(check_T(T, Hkv));
     TRY(check_heads(Hq, Hkv, hd));
     TRY(check_cache(page, maxp, npages));
-    if (!moe::attention_supported(Hq, Hkv, hd, page))
+    if (!moe::attention_supported(Hq, Hkv, hd, page, maxp))
         return fail(MOE_ERR_UNSUPPORTED,
-                    "attention needs hd = 128, Hq/Hkv in {1, 2, 4, 8} and page a multiple of 8 "
-                    "(got hd=%d, Hq=%d, Hkv=%d, page=%d)", hd, Hq, Hkv, page);
+                    "attention needs hd = 128, Hq/Hkv in {1, 2, 4, 8}, page a multiple of 8 and "
+                    "maxp <= 4096 (got hd=%d, Hq=%d, Hkv=%d, page=%d, maxp=%d)", hd, Hq, Hkv, page,
+                    maxp);
     if (!(scale > 0.0f) || !std::isfinite(scale)) return fail(MOE_ERR_INVALID_ARG, "scale must be > 0");
     TRY(need_rows(q, "q", T));
     TRY(need(k_cache, "k_cache"));

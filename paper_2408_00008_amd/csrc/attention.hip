@@ -68,7 +68,9 @@ __global__ __launch_bounds__(256) void rope_append_kernel(const float* qkv, cons
 constexpr int HD = 128;   // head dimension of these kernels
 constexpr int LPP = 8;    // lanes per position: 16 dims each
 constexpr int DPL = HD / LPP;
+constexpr int PPB = 64 / LPP;  // positions per wave block
 constexpr int NWAVE = 4;  // waves per workgroup
+constexpr int MAXP = 4096;  // page-table entries per request held in LDS
 
 __device__ __forceinline__ void widen16(const uint4& lo, const uint4& hi, float* f)
 {
@@ -80,12 +82,31 @@ __device__ __forceinline__ void widen16(const uint4& lo, const uint4& hi, float*
     }
 }
 
+// Sum over an aligned group of 8 lanes, by DPP lane permutations (xor 1 and
+// xor 2 within quads, then the mirror within the 8 lanes); every lane of the
+// group ends with the sum.
+template <int CTRL>
+__device__ __forceinline__ float dpp(float x)
+{
+    return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), CTRL,
+                                                                 0xF, 0xF, false));
+}
+
+__device__ __forceinline__ float sum8(float v)
+{
+    v += dpp<0xB1>(v);   // quad_perm [1, 0, 3, 2]
+    v += dpp<0x4E>(v);   // quad_perm [2, 3, 0, 1]
+    v += dpp<0x141>(v);  // row_half_mirror: quads 0 and 1 of each 8 lanes
+    return v;
+}
+
 // One workgroup per (token t, KV head g); the GROUP query heads of g share
 // every key/value read.  A wave takes blocks of 8 positions (8 lanes per
 // position, 16 dims per lane) and keeps, per lane group, its own running max,
 // sum and weighted value sum (online softmax in base 2: the query is
-// pre-scaled by scale * log2(e)); two blocks are loaded before either is
-// used.  The lane groups are merged by shuffles, the waves through LDS.
+// pre-scaled by scale * log2(e)).  The wave's blocks are loaded through a
+// ring of NB register sets, NB - 1 blocks ahead of the one being multiplied.
+// The lane groups are merged by shuffles, the waves through LDS.
 template <int GROUP>
 __global__ __launch_bounds__(NWAVE * 64) void attn_decode_kernel(
     const bf16_t* q, const bf16_t* kc, const bf16_t* vc, const int32_t* page_table, int maxp,
@@ -93,12 +114,23 @@ __global__ __launch_bounds__(NWAVE * 64) void attn_decode_kernel(
 {
     __shared__ float s_acc[NWAVE][GROUP][HD];
     __shared__ float s_ml[NWAVE][GROUP][2];
+    __shared__ int s_page[MAXP];
     const int t = blockIdx.x / Hkv, g = blockIdx.x - t * Hkv;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int sub = lane & (LPP - 1), pp = lane / LPP;
     // a context outside [1, maxp * page] or a page id outside the cache
     // (invalid input) is clamped: no read leaves the cache
     const int L = min(max(ctx[t], 1), maxp * page);
+    // the request's page ids, once, in LDS: a block's address then waits on
+    // an LDS read, not on a memory load (memory loads retire in order, so
+    // waiting for a page id would also wait for every key/value load before
+    // it)
+    const int npg = (L + page - 1) / page;
+    for (int j = tid; j < npg; j += NWAVE * 64) {
+        const int pg = page_table[(int64_t)t * maxp + j];
+        s_page[j] = pg < 0 ? 0 : (pg >= npages ? npages - 1 : pg);
+    }
+    __syncthreads();
     const float qs = scale * 1.44269504088896340736f;  // scores in base 2
 
     float qv[GROUP][DPL];
@@ -119,16 +151,15 @@ __global__ __launch_bounds__(NWAVE * 64) void attn_decode_kernel(
         for (int i = 0; i < DPL; ++i) acc[h][i] = 0.0f;
     }
 
-    const int nblk = (L + 7) / 8;
+    const int nblk = (L + PPB - 1) / PPB;
     auto addr = [&](int b) {
-        int s = 8 * b + pp;
+        int s = PPB * b + pp;
         s = s < L ? s : L - 1;  // dead positions read the last one (not used)
-        int64_t pg = page_table[(int64_t)t * maxp + s / page];
-        pg = pg < 0 ? 0 : (pg >= npages ? npages - 1 : pg);
+        const int64_t pg = s_page[s / page];
         return ((pg * Hkv + g) * page + s % page) * HD + DPL * sub;
     };
     auto update = [&](int b, const uint4* kv) {
-        if (8 * b + pp >= L) return;  // uniform over the lane group
+        if (PPB * b + pp >= L) return;  // uniform over the lane group
         float kf[DPL], vf[DPL];
         widen16(kv[0], kv[1], kf);
         widen16(kv[2], kv[3], vf);
@@ -141,9 +172,7 @@ __global__ __launch_bounds__(NWAVE * 64) void attn_decode_kernel(
             sd[h] = d;
         }
 #pragma unroll
-        for (int o = 1; o < LPP; o <<= 1)
-#pragma unroll
-            for (int h = 0; h < GROUP; ++h) sd[h] += __shfl_xor(sd[h], o, 64);
+        for (int h = 0; h < GROUP; ++h) sd[h] = sum8(sd[h]);
 #pragma unroll
         for (int h = 0; h < GROUP; ++h) {
             const float mn = fmaxf(m[h], sd[h]);
@@ -155,16 +184,30 @@ __global__ __launch_bounds__(NWAVE * 64) void attn_decode_kernel(
             m[h] = mn;
         }
     };
-    for (int b = wave; b < nblk; b += 2 * NWAVE) {
-        const int b2 = b + NWAVE;
-        const int64_t o1 = addr(b), o2 = addr(b2 < nblk ? b2 : b);
-        uint4 kv1[4] = {ldg16(kc + o1), ldg16(kc + o1 + 8), ldg16(vc + o1), ldg16(vc + o1 + 8)};
-        uint4 kv2[4] = {ldg16(kc + o2), ldg16(kc + o2 + 8), ldg16(vc + o2), ldg16(vc + o2 + 8)};
-        update(b, kv1);
-        if (b2 < nblk) update(b2, kv2);
+    // blocks past the last are clamped to real positions (loaded, not used),
+    // so every load is issued and the memory-counter waits stay static
+    constexpr int NB = 3;
+    uint4 ring[NB][4];
+    auto load = [&](uint4* r, int b) {
+        const int64_t o = addr(b < nblk ? b : nblk - 1);
+        r[0] = ldg16(kc + o);
+        r[1] = ldg16(kc + o + 8);
+        r[2] = ldg16(vc + o);
+        r[3] = ldg16(vc + o + 8);
+    };
+#pragma unroll
+    for (int i = 0; i < NB - 1; ++i) load(ring[i], wave + i * NWAVE);
+    for (int b0 = wave; b0 < nblk; b0 += NB * NWAVE) {
+#pragma unroll
+        for (int i = 0; i < NB; ++i) {
+            const int b = b0 + i * NWAVE;
+            if (b >= nblk) break;  // uniform over the wave
+            load(ring[(i + NB - 1) % NB], b + (NB - 1) * NWAVE);
+            update(b, ring[i]);
+        }
     }
 
-    // merge the 8 lane groups of the wave (same dims, disjoint positions)
+    // merge the lane groups of the wave (same dims, disjoint positions)
 #pragma unroll
     for (int o = LPP; o < 64; o <<= 1) {
 #pragma unroll
@@ -214,9 +257,9 @@ __global__ __launch_bounds__(NWAVE * 64) void attn_decode_kernel(
 
 }  // namespace
 
-bool attention_supported(int Hq, int Hkv, int hd, int page)
+bool attention_supported(int Hq, int Hkv, int hd, int page, int maxp)
 {
-    if (hd != HD || Hkv < 1 || Hq % Hkv || page < 8 || page % 8) return false;
+    if (hd != HD || Hkv < 1 || Hq % Hkv || page < 8 || page % 8 || maxp > MAXP) return false;
     const int group = Hq / Hkv;
     return group == 1 || group == 2 || group == 4 || group == 8;
 }

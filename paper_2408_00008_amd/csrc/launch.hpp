@@ -33,7 +33,7 @@ hipError_t launch_rmsnorm(const float* h, const bf16_t* gamma, int64_t T, int d,
 // Decode attention (attention.hip): RoPE of the new token's query/key heads
 // and the key/value append to the paged cache; grouped-query attention over
 // the cache.  Cache layout [pages, Hkv, page, hd] bf16.
-bool attention_supported(int Hq, int Hkv, int hd, int page);
+bool attention_supported(int Hq, int Hkv, int hd, int page, int maxp);
 hipError_t launch_rope_append(const float* qkv, const int32_t* pos, const int32_t* page_table,
                               int maxp, int npages, int64_t T, int Hq, int Hkv, int hd, int page,
                               double theta, bf16_t* q_out, bf16_t* kc, bf16_t* vc,
