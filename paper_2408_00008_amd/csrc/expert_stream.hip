@@ -558,9 +558,13 @@ hipError_t launch_stream_down(const DownArgs& a, int64_t rows_max, hipStream_t s
     p.rows = static_cast<int>(a.A);
     const int G = a.groups ? a.groups : stream_groups(a.A, a.E, rows_max);
     if (!a.offsets) {
-        // dense projection (one matrix): 4 output-row waves x 4 reduction
-        // shares, so that even a 4096-row matrix spreads over 64+ workgroups
-        // of 16 waves; 64-row passes (more rows take more passes)
+        // dense projection (one matrix): several reduction shares per
+        // workgroup, so that a single matrix still spreads over the CUs.
+        // Measured on MI355X at 64 tokens, K = 4096: up to 4096 output rows,
+        // 2 row waves x 4 shares with 32-token passes (2 workgroups per slab,
+        // the second re-reading it from L2; 4096 rows: 23 -> 14 us); more
+        // rows, 4 x 4 with 64-token passes (6144 rows: 24 us)
+        if (a.d <= 4096 && a.ffn % 512 == 0) return run<false, 2, 4, 2, 128>(p, rows_max, stream);
         if (a.ffn % 256 == 0) {
             if (G == 2) return run<false, 4, 4, 2, 64>(p, rows_max, stream);
             return run<false, 4, 4, 4, 64>(p, rows_max, stream);
