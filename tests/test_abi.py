@@ -180,3 +180,43 @@ def test_fp8_entry_points_reject(L):
     assert st == B.MOE_ERR_INVALID_ARG and b"w2q is NULL" in L.moe_last_error()
     assert L.moe_swiglu_up_fp8(None, None, 0x700000, q1, s1, q3, s3, 0, 128, 256, 8, 2, None,
                                None) == B.MOE_OK
+
+
+def test_decoder_entry_points_reject(L):
+    """moe_linear, moe_rope_kv_append and moe_attention_decode validate
+    shapes, head layouts, cache geometry, scale/theta and aliasing before
+    touching the GPU; T = 0 is a no-op."""
+    big = 1 << 40
+    x, w, y, q, kc, vc, pt, ctx, out = (big * (i + 1) for i in range(9))
+    c_double, c_float = ctypes.c_double, ctypes.c_float
+    # linear
+    assert L.moe_linear(x, w, 4, 100, 128, y, None) == B.MOE_ERR_UNSUPPORTED
+    assert L.moe_linear(x, w, 4, 128, 128, w + 64, None) == B.MOE_ERR_INVALID_ARG
+    assert b"overlaps w" in L.moe_last_error()
+    assert L.moe_linear(None, w, 0, 128, 128, None, None) == B.MOE_OK
+
+    def rope(**kw):
+        a = dict(T=4, Hq=32, Hkv=8, hd=128, page=16, maxp=4, npages=64, theta=1e6, q_out=q, kc=kc)
+        a.update(kw)
+        return L.moe_rope_kv_append(x, ctx, pt, a["T"], a["Hq"], a["Hkv"], a["hd"], a["page"], a["maxp"],
+                                    a["npages"], c_double(a["theta"]), a["q_out"], a["kc"], vc, None)
+    assert rope(Hq=30) == B.MOE_ERR_INVALID_ARG and b"multiple of Hkv" in L.moe_last_error()
+    assert rope(hd=127) == B.MOE_ERR_INVALID_ARG
+    assert rope(theta=0.0) == B.MOE_ERR_INVALID_ARG
+    assert rope(page=0) == B.MOE_ERR_INVALID_ARG
+    assert rope(q_out=kc + 32) == B.MOE_ERR_INVALID_ARG and b"overlaps" in L.moe_last_error()
+    assert rope(kc=vc) == B.MOE_ERR_INVALID_ARG
+    assert rope(T=0) == B.MOE_OK
+
+    def attn(**kw):
+        a = dict(T=4, Hq=32, Hkv=8, hd=128, page=16, maxp=4, npages=64, scale=0.088, out=out)
+        a.update(kw)
+        return L.moe_attention_decode(q, kc, vc, pt, ctx, a["T"], a["Hq"], a["Hkv"], a["hd"], a["page"],
+                                      a["maxp"], a["npages"], c_float(a["scale"]), a["out"], None)
+    assert attn(hd=64) == B.MOE_ERR_UNSUPPORTED
+    assert attn(page=12) == B.MOE_ERR_UNSUPPORTED
+    assert attn(Hq=48, Hkv=3) == B.MOE_ERR_UNSUPPORTED  # group of 16
+    assert attn(maxp=5000) == B.MOE_ERR_UNSUPPORTED
+    assert attn(scale=0.0) == B.MOE_ERR_INVALID_ARG
+    assert attn(out=q + 16) == B.MOE_ERR_INVALID_ARG and b"overlaps q" in L.moe_last_error()
+    assert attn(T=0) == B.MOE_OK
