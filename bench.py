@@ -99,12 +99,12 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = "cuda:0"
     w = inputs.WORKLOADS[args.workload].replace(seed=args.seed)
-    if w.layers != 1:
-        from paper_2408_00008_amd import stack
-        return stack.bench_stack(args, w)
     if w.hq:
         from paper_2408_00008_amd import decoder
         return decoder.bench_decoder(args, w)
+    if w.layers != 1:
+        from paper_2408_00008_amd import stack
+        return stack.bench_stack(args, w)
     T, d, ffn, E, k = w.T, w.d, w.ffn, w.E, w.k
     A = T * k
     x = inputs.make_x(w, dev)

@@ -76,10 +76,115 @@ class DecoderLayer:
         return h
 
 
+class DecoderStack:
+    """w.layers decoder layers with their own weights and KV caches (all
+    resident), sharing the requests' page table and positions.  A step runs
+    every layer in order; it can be captured once into a HIP graph."""
+
+    def __init__(self, w, device="cuda:0"):
+        from . import inputs
+
+        self.w = w
+        self.layers, self.caches = [], []
+        for l in range(w.layers):
+            attn = inputs.make_attention(w, l, device)
+            moe = inputs.make_layer(w, l, device)
+            kv = inputs.make_kv_cache(w, l, device)
+            self.layers.append(DecoderLayer(attn, moe, w.hq, w.hkv, w.k, w.theta, w.eps))
+            self.caches.append((kv["k_cache"], kv["v_cache"]))
+            self.page_table, self.pos, self.ctx = kv["page_table"], kv["pos"], kv["ctx"]
+        self.graph = None
+
+    def step(self, h, stream=None):
+        for layer, (kc, vc) in zip(self.layers, self.caches):
+            layer.step(h, kc, vc, self.page_table, self.pos, self.ctx, stream=stream)
+        return h
+
+    def capture(self, h):
+        """Capture one step on h's buffer (run it once eagerly first, so that
+        every scratch buffer exists)."""
+        self.step(h)
+        torch.cuda.synchronize()
+        s = torch.cuda.Stream()
+        self.graph = torch.cuda.CUDAGraph()
+        with torch.cuda.stream(s):
+            with torch.cuda.graph(self.graph, stream=s):
+                self.step(h, stream=s)
+        torch.cuda.synchronize()
+
+    def replay(self):
+        self.graph.replay()
+
+
+def bench_decoder_stack(args, w):
+    """bench.py for a stack of decoder layers: one decode step of the whole
+    model (graph replays); prints one JSON line."""
+    import json
+    import time
+
+    import numpy as np
+
+    from . import inputs
+
+    HBM_PEAK_GBS = 8000.0
+    st = DecoderStack(w)
+    h = inputs.make_h(w, "cuda:0")
+    st.capture(h)
+    stream = torch.cuda.current_stream()
+    for _ in range(args.warmup):
+        st.replay()
+    torch.cuda.synchronize()
+    bounds = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    t0 = time.perf_counter()
+    bounds[0].record(stream)
+    for i in range(args.steps):
+        st.replay()
+        bounds[i + 1].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms = bounds[0].elapsed_time(bounds[-1]) / args.steps
+    step_ms = np.array([bounds[i].elapsed_time(bounds[i + 1]) for i in range(args.steps)])
+    T, d = w.T, w.d
+    ctx = st.ctx.cpu().numpy().astype(np.int64)
+    kv_bytes = int(ctx.sum()) * w.hkv * w.hd * 2 * 2
+    proj_bytes = (st.layers[0].wqkv.numel() + st.layers[0].wo.numel()) * 2
+    layer_bytes = proj_bytes + w.E * 3 * w.ffn * d * 2 + w.E * d * 2 + kv_bytes + T * d * 4 * 2
+    step_bytes = w.layers * layer_bytes
+    gbs = step_bytes / (ms * 1e-3) / 1e9
+    rec = {
+        "metric": "model decode tokens/s",
+        "value": round(T / (ms * 1e-3), 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "step_ms_p10_p50_p90": [round(float(np.percentile(step_ms, q)), 4) for q in (10, 50, 90)],
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded normals: %d random-init Mixtral-8x7B decoder layers, random KV caches)"
+                % w.layers,
+        "config": {"workload": args.workload, "T": T, "d": d, "ffn": w.ffn, "E": w.E, "k": w.k,
+                   "layers": w.layers, "hq": w.hq, "hkv": w.hkv, "hd": w.hd, "page": w.page,
+                   "cached_positions_per_layer": int(ctx.sum() - T), "graph": True},
+        "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": None,
+                     "kernel": "whole step (%d x attention block + MoE block)" % w.layers,
+                     "algorithmic_bytes_per_launch": step_bytes},
+        "cpu_baseline": None,
+        "wall_s_timed": round(wall, 3),
+    }
+    print(json.dumps(rec), flush=True)
+
+
 def bench_decoder(args, w):
     """bench.py for a decoder-layer workload: one decode step of the layer
     for w.T requests; prints one JSON line.  Each step rewrites the same
     cache slot and advances h, so every step does the same work."""
+    if w.layers > 1:
+        return bench_decoder_stack(args, w)
     import json
     import time
 

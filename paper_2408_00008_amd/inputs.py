@@ -120,6 +120,11 @@ WORKLOADS = {
     "decoder_t64_ctx1024": Workload("decoder_t64_ctx1024", 64, MIXTRAL_D, MIXTRAL_FFN, MIXTRAL_E,
                                     MIXTRAL_K, 1.0, 0.02, 0.02, 0.02, 0.02, hq=32, hkv=8,
                                     ctx=1024),
+    # the whole model: 32 decoder layers, one decode step of 64 requests with
+    # 1024 positions cached each (every layer has its own cache)
+    "decoder32_t64_ctx1024": Workload("decoder32_t64_ctx1024", 64, MIXTRAL_D, MIXTRAL_FFN,
+                                      MIXTRAL_E, MIXTRAL_K, 1.0, 0.02, 0.02, 0.02, 0.02,
+                                      layers=32, hq=32, hkv=8, ctx=1024),
     # 32 stacked layers, RMSNorm + residual around each, one decode step of 64
     "stack32_t64": Workload("stack32_t64", 64, MIXTRAL_D, MIXTRAL_FFN, MIXTRAL_E, MIXTRAL_K,
                             1.0, 0.02, 0.02, 0.02, 0.02, layers=32),

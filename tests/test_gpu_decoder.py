@@ -242,3 +242,34 @@ def test_decoder_step_graph_replays():
         torch.cuda.synchronize()
         assert torch.equal(h_g, h_e)
         assert torch.equal(kv["k_cache"], kc_e)
+
+
+def test_decoder_stack_equals_layers():
+    """A stack step is its layers' steps in order, each on its own cache
+    (bitwise); the captured stack replays bitwise."""
+    say("[decoder] 3-layer stack")
+    from paper_2408_00008_amd.decoder import DecoderStack
+    w = small_workload(12, 256, 4, 2, ctx=30, page=16, seed=17).replace(layers=3)
+    st = DecoderStack(w, DEV)
+    caches0 = [(k.clone(), v.clone()) for k, v in st.caches]
+    h0 = inputs.make_h(w, DEV)
+    h_ref = h0.clone()
+    for layer, (k, v) in zip(st.layers, [(k.clone(), v.clone()) for k, v in caches0]):
+        layer.step(h_ref, k, v, st.page_table, st.pos, st.ctx)
+    h = h0.clone()
+    st.step(h)
+    torch.cuda.synchronize()
+    assert torch.equal(h, h_ref)
+    assert not torch.equal(h, h0)
+    hg = h0.clone()
+    for (k, v), (k0, v0) in zip(st.caches, caches0):
+        k.copy_(k0)
+        v.copy_(v0)
+    st.capture(hg)  # runs one eager step first
+    for _ in range(2):
+        hg.copy_(h0)
+        torch.cuda.synchronize()
+        st.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(hg, h_ref)
+
