@@ -265,7 +265,13 @@ moe_status_t moe_rope_kv_append(const float* qkv, const int32_t* pos, const int3
  * with K_s, V_s of KV head h / (Hq / Hkv) of token t's request.  q [T, Hq, hd]
  * bf16, out [T, Hq * hd] bf16 (f32 softmax and accumulation).  ctx[t] in
  * [1, maxp * page].  Supported: hd = 128, Hq / Hkv in {1, 2, 4, 8}, page a
- * multiple of 8, maxp <= 4096 (MOE_ERR_UNSUPPORTED otherwise).
+ * multiple of 8, maxp <= 4096 (MOE_ERR_UNSUPPORTED otherwise).  When T * Hkv
+ * is small and contexts long, the positions are split over several
+ * workgroups whose partial states go to library-owned scratch (per device,
+ * grown on demand like moe_forward's, refused with MOE_ERR_NO_MEMORY while
+ * `stream` is captured into a graph if it must grow) and are merged in a
+ * fixed order: results do not depend on the split.  Calls that use this
+ * scratch on one device must not overlap on different streams.
  */
 moe_status_t moe_attention_decode(const moe_bf16_t* q, const moe_bf16_t* k_cache,
                                   const moe_bf16_t* v_cache, const int32_t* page_table,

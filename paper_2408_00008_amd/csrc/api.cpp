@@ -166,15 +166,17 @@ struct DeviceScratch {
     size_t bytes = 0;
 };
 std::mutex g_ws_mu;
-std::unordered_map<int, DeviceScratch> g_ws;
+// per device: slot 0 serves moe_forward / moe_forward_ex, slot 1 the
+// partial states of moe_attention_decode
+std::unordered_map<int, DeviceScratch> g_ws[2];
 
-moe_status_t library_workspace(size_t need_bytes, hipStream_t stream, void** out)
+moe_status_t library_workspace(size_t need_bytes, hipStream_t stream, void** out, int slot = 0)
 {
     int dev = 0;
     hipError_t e = hipGetDevice(&dev);
     if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
     std::lock_guard<std::mutex> lk(g_ws_mu);
-    DeviceScratch& s = g_ws[dev];
+    DeviceScratch& s = g_ws[slot][dev];
     if (s.bytes < need_bytes) {
         hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
         e = hipStreamIsCapturing(stream, &cs);
@@ -793,9 +795,14 @@ moe_status_t moe_attention_decode(const moe_bf16_t* q, const moe_bf16_t* k_cache
                     {"v_cache", {v_cache, cache}}, {"page_table", {page_table, (size_t)T * maxp * 4}},
                     {"ctx", {ctx, (size_t)T * 4}}}));
     if (T == 0) return ok();
+    const int nsplit = moe::attention_splits(T, Hkv, maxp, page);
+    void* part = nullptr;
+    const size_t pbytes = moe::attention_scratch_bytes(T, Hq, Hkv, nsplit);
+    if (pbytes) TRY(library_workspace(pbytes, stream, &part, 1));
     hipError_t e = moe::launch_attention_decode(q, k_cache, v_cache, page_table, maxp,
                                                 static_cast<int>(npages), ctx, T, Hq, Hkv, page,
-                                                scale, out, stream);
+                                                scale, nsplit, static_cast<float*>(part), out,
+                                                stream);
     return e == hipSuccess ? ok() : hip_fail(e, "attention kernel launch");
 }
 

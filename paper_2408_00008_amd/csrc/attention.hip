@@ -107,15 +107,24 @@ __device__ __forceinline__ float sum8(float v)
 // pre-scaled by scale * log2(e)).  The wave's blocks are loaded through a
 // ring of NB register sets, NB - 1 blocks ahead of the one being multiplied.
 // The lane groups are merged by shuffles, the waves through LDS.
+//
+// With nsplit > 1 (few tokens, long contexts) the request's position blocks
+// are cut into nsplit contiguous ranges, one workgroup each (workgroup
+// (t, g, s) = blockIdx (t * Hkv + g) * nsplit + s); each writes its running
+// max, sum and unnormalised weighted value sum to part [.., nsplit, GROUP,
+// HD + 2] and attn_merge_kernel combines the ranges in order.
 template <int GROUP>
 __global__ __launch_bounds__(NWAVE * 64) void attn_decode_kernel(
     const bf16_t* q, const bf16_t* kc, const bf16_t* vc, const int32_t* page_table, int maxp,
-    const int32_t* ctx, int npages, int Hq, int Hkv, int page, float scale, bf16_t* out)
+    const int32_t* ctx, int npages, int Hq, int Hkv, int page, float scale, int nsplit,
+    float* part, bf16_t* out)
 {
     __shared__ float s_acc[NWAVE][GROUP][HD];
     __shared__ float s_ml[NWAVE][GROUP][2];
     __shared__ int s_page[MAXP];
-    const int t = blockIdx.x / Hkv, g = blockIdx.x - t * Hkv;
+    const int split = blockIdx.x % nsplit;
+    const int tg = blockIdx.x / nsplit;
+    const int t = tg / Hkv, g = tg - t * Hkv;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int sub = lane & (LPP - 1), pp = lane / LPP;
     // a context outside [1, maxp * page] or a page id outside the cache
@@ -151,7 +160,11 @@ __global__ __launch_bounds__(NWAVE * 64) void attn_decode_kernel(
         for (int i = 0; i < DPL; ++i) acc[h][i] = 0.0f;
     }
 
-    const int nblk = (L + PPB - 1) / PPB;
+    // this workgroup's blocks [bbeg, bend) of the request's position blocks
+    const int nblk_all = (L + PPB - 1) / PPB;
+    const int per = (nblk_all + nsplit - 1) / nsplit;
+    const int bbeg = split * per;
+    const int nblk = min(nblk_all, bbeg + per);  // blocks are numbered from 0; this range ends here
     auto addr = [&](int b) {
         int s = PPB * b + pp;
         s = s < L ? s : L - 1;  // dead positions read the last one (not used)
@@ -195,9 +208,11 @@ __global__ __launch_bounds__(NWAVE * 64) void attn_decode_kernel(
         r[2] = ldg16(vc + o);
         r[3] = ldg16(vc + o + 8);
     };
+    if (bbeg < nblk) {
 #pragma unroll
-    for (int i = 0; i < NB - 1; ++i) load(ring[i], wave + i * NWAVE);
-    for (int b0 = wave; b0 < nblk; b0 += NB * NWAVE) {
+        for (int i = 0; i < NB - 1; ++i) load(ring[i], bbeg + wave + i * NWAVE);
+    }
+    for (int b0 = bbeg + wave; b0 < nblk; b0 += NB * NWAVE) {
 #pragma unroll
         for (int i = 0; i < NB; ++i) {
             const int b = b0 + i * NWAVE;
@@ -238,18 +253,54 @@ __global__ __launch_bounds__(NWAVE * 64) void attn_decode_kernel(
         }
     }
     __syncthreads();
-    // merge the waves and normalise: one thread per (head, dim)
+    // merge the waves and normalise (or hand the range's state over): one
+    // thread per (head, dim)
     for (int j = tid; j < GROUP * HD; j += NWAVE * 64) {
         const int h = j / HD, dd = j - h * HD;
         float mt = -INFINITY;
 #pragma unroll
         for (int w = 0; w < NWAVE; ++w) mt = fmaxf(mt, s_ml[w][h][0]);
         float lt = 0.0f, at = 0.0f;
+        if (mt != -INFINITY) {  // -inf: an empty range (only with nsplit > 1)
 #pragma unroll
-        for (int w = 0; w < NWAVE; ++w) {
-            const float c = exp2f(s_ml[w][h][0] - mt);  // an empty wave has m = -inf: 0
-            lt = fmaf(s_ml[w][h][1], c, lt);
-            at = fmaf(s_acc[w][h][dd], c, at);
+            for (int w = 0; w < NWAVE; ++w) {
+                const float c = exp2f(s_ml[w][h][0] - mt);  // an empty wave has m = -inf: 0
+                lt = fmaf(s_ml[w][h][1], c, lt);
+                at = fmaf(s_acc[w][h][dd], c, at);
+            }
+        }
+        if (nsplit == 1) {
+            out[((int64_t)t * Hq + g * GROUP + h) * HD + dd] = f32_to_bf16(at / lt);
+        } else {
+            float* pr = part + (((int64_t)tg * nsplit + split) * GROUP + h) * (HD + 2);
+            pr[dd] = at;
+            if (dd == 0) {
+                pr[HD] = mt;
+                pr[HD + 1] = lt;
+            }
+        }
+    }
+}
+
+// Combines the nsplit ranges of attn_decode_kernel, in range order: one
+// workgroup per (token, KV head), one thread per (head, dim).
+template <int GROUP>
+__global__ __launch_bounds__(256) void attn_merge_kernel(const float* part, int nsplit, int Hq,
+                                                         int Hkv, bf16_t* out)
+{
+    const int tg = blockIdx.x;
+    const int t = tg / Hkv, g = tg - t * Hkv;
+    for (int j = threadIdx.x; j < GROUP * HD; j += 256) {
+        const int h = j / HD, dd = j - h * HD;
+        const float* pr = part + ((int64_t)tg * nsplit * GROUP + h) * (HD + 2);
+        const int64_t step = (int64_t)GROUP * (HD + 2);
+        float mt = -INFINITY;
+        for (int s = 0; s < nsplit; ++s) mt = fmaxf(mt, pr[s * step + HD]);
+        float lt = 0.0f, at = 0.0f;
+        for (int s = 0; s < nsplit; ++s) {
+            const float c = exp2f(pr[s * step + HD] - mt);  // an empty range: m = -inf, 0
+            lt = fmaf(pr[s * step + HD + 1], c, lt);
+            at = fmaf(pr[s * step + dd], c, at);
         }
         out[((int64_t)t * Hq + g * GROUP + h) * HD + dd] = f32_to_bf16(at / lt);
     }
@@ -276,30 +327,43 @@ hipError_t launch_rope_append(const float* qkv, const int32_t* pos, const int32_
     return hipGetLastError();
 }
 
+int attention_splits(int64_t T, int Hkv, int maxp, int page)
+{
+    // enough workgroups for every CU (two per CU), ranges of at least 256
+    // positions, at most 32 ranges
+    const int64_t base = T * Hkv;
+    const int64_t want = (512 + base - 1) / base;
+    const int64_t most = ((int64_t)maxp * page + 255) / 256;
+    int64_t s = want < most ? want : most;
+    s = s < 1 ? 1 : (s > 32 ? 32 : s);
+    return static_cast<int>(s);
+}
+
+size_t attention_scratch_bytes(int64_t T, int Hq, int Hkv, int nsplit)
+{
+    return nsplit > 1 ? (size_t)T * Hkv * nsplit * (Hq / Hkv) * (HD + 2) * sizeof(float) : 0;
+}
+
 hipError_t launch_attention_decode(const bf16_t* q, const bf16_t* kc, const bf16_t* vc,
                                    const int32_t* page_table, int maxp, int npages,
                                    const int32_t* ctx, int64_t T, int Hq, int Hkv, int page,
-                                   float scale, bf16_t* out, hipStream_t stream)
+                                   float scale, int nsplit, float* part, bf16_t* out,
+                                   hipStream_t stream)
 {
-    const unsigned blocks = static_cast<unsigned>(T * Hkv);
+    const unsigned blocks = static_cast<unsigned>(T * Hkv * nsplit);
+    const unsigned merge = static_cast<unsigned>(T * Hkv);
+#define MOE_ATTN(GROUP_)                                                                          \
+    attn_decode_kernel<GROUP_><<<blocks, NWAVE * 64, 0, stream>>>(q, kc, vc, page_table, maxp, ctx, \
+                                                                  npages, Hq, Hkv, page, scale,   \
+                                                                  nsplit, part, out);             \
+    if (nsplit > 1) attn_merge_kernel<GROUP_><<<merge, 256, 0, stream>>>(part, nsplit, Hq, Hkv, out);
     switch (Hq / Hkv) {
-    case 1:
-        attn_decode_kernel<1><<<blocks, NWAVE * 64, 0, stream>>>(q, kc, vc, page_table, maxp, ctx,
-                                                                 npages, Hq, Hkv, page, scale, out);
-        break;
-    case 2:
-        attn_decode_kernel<2><<<blocks, NWAVE * 64, 0, stream>>>(q, kc, vc, page_table, maxp, ctx,
-                                                                 npages, Hq, Hkv, page, scale, out);
-        break;
-    case 4:
-        attn_decode_kernel<4><<<blocks, NWAVE * 64, 0, stream>>>(q, kc, vc, page_table, maxp, ctx,
-                                                                 npages, Hq, Hkv, page, scale, out);
-        break;
-    default:
-        attn_decode_kernel<8><<<blocks, NWAVE * 64, 0, stream>>>(q, kc, vc, page_table, maxp, ctx,
-                                                                 npages, Hq, Hkv, page, scale, out);
-        break;
+    case 1: MOE_ATTN(1) break;
+    case 2: MOE_ATTN(2) break;
+    case 4: MOE_ATTN(4) break;
+    default: MOE_ATTN(8) break;
     }
+#undef MOE_ATTN
     return hipGetLastError();
 }
 

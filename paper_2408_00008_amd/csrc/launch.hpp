@@ -38,10 +38,15 @@ hipError_t launch_rope_append(const float* qkv, const int32_t* pos, const int32_
                               int maxp, int npages, int64_t T, int Hq, int Hkv, int hd, int page,
                               double theta, bf16_t* q_out, bf16_t* kc, bf16_t* vc,
                               hipStream_t stream);
+// Position ranges per (token, KV head) so that the grid fills the GPU (few
+// tokens, long contexts); the partial states need attention_scratch_bytes.
+int attention_splits(int64_t T, int Hkv, int maxp, int page);
+size_t attention_scratch_bytes(int64_t T, int Hq, int Hkv, int nsplit);
 hipError_t launch_attention_decode(const bf16_t* q, const bf16_t* kc, const bf16_t* vc,
                                    const int32_t* page_table, int maxp, int npages,
                                    const int32_t* ctx, int64_t T, int Hq, int Hkv, int page,
-                                   float scale, bf16_t* out, hipStream_t stream);
+                                   float scale, int nsplit, float* part, bf16_t* out,
+                                   hipStream_t stream);
 
 // Expert GEMMs.  `rows_hint` = T*k (an upper bound of any expert's rows) picks
 // the tile shape; the real per-expert row counts are read on the device.

@@ -120,6 +120,11 @@ WORKLOADS = {
     "decoder_t64_ctx1024": Workload("decoder_t64_ctx1024", 64, MIXTRAL_D, MIXTRAL_FFN, MIXTRAL_E,
                                     MIXTRAL_K, 1.0, 0.02, 0.02, 0.02, 0.02, hq=32, hkv=8,
                                     ctx=1024),
+    # few requests with long contexts: 8 requests x 8192 cached positions (the
+    # same cache bytes per layer as 64 x 1024)
+    "decoder_t8_ctx8192": Workload("decoder_t8_ctx8192", 8, MIXTRAL_D, MIXTRAL_FFN, MIXTRAL_E,
+                                   MIXTRAL_K, 1.0, 0.02, 0.02, 0.02, 0.02, hq=32, hkv=8,
+                                   ctx=8192),
     # the whole model: 32 decoder layers, one decode step of 64 requests with
     # 1024 positions cached each (every layer has its own cache)
     "decoder32_t64_ctx1024": Workload("decoder32_t64_ctx1024", 64, MIXTRAL_D, MIXTRAL_FFN,

@@ -117,6 +117,35 @@ def test_attention(hq, hkv, page, ctx):
     assert err < OUT_TOL
 
 
+@pytest.mark.parametrize("T,hq,hkv,page,ctx", [
+    (2, 32, 8, 16, 3000),    # 16 (token, KV head) pairs: positions split over 12 workgroups
+    (1, 8, 1, 32, 5000),     # one request, one KV head: 20 ranges
+    (3, 16, 2, 8, 1500),
+])
+def test_attention_long_context_split(T, hq, hkv, page, ctx):
+    """Few tokens and long contexts: each (token, KV head) is split over
+    several workgroups and merged; ragged lengths leave some ranges empty."""
+    say(f"[decoder] split attention T={T} hq={hq} hkv={hkv} page={page} ctx<={ctx}")
+    w = small_workload(T, 256, hq, hkv, ctx=ctx, page=page, seed=19, ragged=False)
+    kv = inputs.make_kv_cache(w, 0, DEV)
+    lens = kv["ctx"].clone()
+    lens[0] = 1 if T > 1 else ctx + 1
+    g = torch.Generator(device=DEV).manual_seed(21)
+    q = (torch.randn(T, hq, 128, generator=g, device=DEV) * 1.5).to(torch.bfloat16)
+    out = torch.empty(T, hq * 128, dtype=torch.bfloat16, device=DEV)
+    scale = 1 / math.sqrt(128)
+    B.moe_attention_decode(q, kv["k_cache"], kv["v_cache"], kv["page_table"], lens, scale, out)
+    out2 = torch.empty_like(out)
+    B.moe_attention_decode(q, kv["k_cache"], kv["v_cache"], kv["page_table"], lens, scale, out2)
+    torch.cuda.synchronize()
+    assert torch.equal(out, out2)
+    ref = orc().attention_decode(widen(bits(q)), bits(kv["k_cache"]), bits(kv["v_cache"]),
+                                 kv["page_table"].cpu().numpy(), lens.cpu().numpy(), scale)
+    err = rowwise_rel(bf16_to_f64(out).reshape(T * hq, 128), ref.reshape(T * hq, 128))
+    say(f"  rowwise rel over {T * hq} heads {err:.2e}")
+    assert err < OUT_TOL
+
+
 def test_attention_unsupported_shapes_rejected():
     q = torch.zeros(1, 4, 64, dtype=torch.bfloat16, device=DEV)
     kc = torch.zeros(2, 1, 16, 64, dtype=torch.bfloat16, device=DEV)
