@@ -36,7 +36,12 @@ class DecoderLayer:
         self.wo = attn["wo"].contiguous()
         self.gamma_attn, self.gamma_moe = attn["gamma_attn"], attn["gamma_moe"]
         self.router_w, self.router_bias = moe["router_w"], moe.get("router_bias")
-        self.w1, self.w3, self.w2 = moe["w1"], moe["w3"], moe["w2"]
+        # expert weights: bf16 (w1, w3, w2) or E4M3 bytes with row scales
+        self.fp8 = "w1q" in moe
+        if self.fp8:
+            self.q = [moe[n] for n in ("w1q", "w1s", "w3q", "w3s", "w2q", "w2s")]
+        else:
+            self.w1, self.w3, self.w2 = moe["w1"], moe["w3"], moe["w2"]
         self.hq, self.hkv, self.k, self.theta, self.eps = hq, hkv, k, theta, eps
         self.d = self.wo.shape[0]
         self.hd = self.wo.shape[1] // hq
@@ -71,9 +76,17 @@ class DecoderLayer:
         B.moe_linear(b["attn"], self.wo, b["o"], stream=stream)
         B.moe_combine(b["o"], T, self.d, 1, out_f32=h, residual=h, stream=stream)
         B.moe_rmsnorm(h, self.gamma_moe, self.eps, b["a2"], stream=stream)
-        B.moe_forward_ex(b["a2"], self.router_w, self.w1, self.w3, self.w2, self.k, out_f32=h,
-                         router_bias=self.router_bias, residual=h, stream=stream)
+        self.moe_block(b["a2"], h, stream)
         return h
+
+    def moe_block(self, a2, h, stream=None):
+        """h += MoE(a2), the f32 residual updated in place."""
+        if self.fp8:
+            B.moe_forward_fp8_ex(a2, self.router_w, *self.q, self.k, out_f32=h,
+                                 router_bias=self.router_bias, residual=h, stream=stream)
+        else:
+            B.moe_forward_ex(a2, self.router_w, self.w1, self.w3, self.w2, self.k, out_f32=h,
+                             router_bias=self.router_bias, residual=h, stream=stream)
 
 
 class DecoderStack:
@@ -88,7 +101,7 @@ class DecoderStack:
         self.layers, self.caches = [], []
         for l in range(w.layers):
             attn = inputs.make_attention(w, l, device)
-            moe = inputs.make_layer(w, l, device)
+            moe = inputs.make_layer_fp8(w, l, device) if w.fp8 else inputs.make_layer(w, l, device)
             kv = inputs.make_kv_cache(w, l, device)
             self.layers.append(DecoderLayer(attn, moe, w.hq, w.hkv, w.k, w.theta, w.eps))
             self.caches.append((kv["k_cache"], kv["v_cache"]))
@@ -148,7 +161,8 @@ def bench_decoder_stack(args, w):
     ctx = st.ctx.cpu().numpy().astype(np.int64)
     kv_bytes = int(ctx.sum()) * w.hkv * w.hd * 2 * 2
     proj_bytes = (st.layers[0].wqkv.numel() + st.layers[0].wo.numel()) * 2
-    layer_bytes = proj_bytes + w.E * 3 * w.ffn * d * 2 + w.E * d * 2 + kv_bytes + T * d * 4 * 2
+    expert_bytes = w.E * 3 * w.ffn * d * (1 if w.fp8 else 2) + w.E * (2 * w.ffn + d) * 4 * w.fp8
+    layer_bytes = proj_bytes + expert_bytes + w.E * d * 2 + kv_bytes + T * d * 4 * 2
     step_bytes = w.layers * layer_bytes
     gbs = step_bytes / (ms * 1e-3) / 1e9
     rec = {
@@ -164,8 +178,8 @@ def bench_decoder_stack(args, w):
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "bf16",
-        "data": "synthetic (seeded normals: %d random-init Mixtral-8x7B decoder layers, random KV caches)"
-                % w.layers,
+        "data": "synthetic (seeded normals: %d random-init Mixtral-8x7B decoder layers%s, random KV caches)"
+                % (w.layers, ", E4M3 expert weights" if w.fp8 else ""),
         "config": {"workload": args.workload, "T": T, "d": d, "ffn": w.ffn, "E": w.E, "k": w.k,
                    "layers": w.layers, "hq": w.hq, "hkv": w.hkv, "hd": w.hd, "page": w.page,
                    "cached_positions_per_layer": int(ctx.sum() - T), "graph": True},
@@ -195,7 +209,7 @@ def bench_decoder(args, w):
     HBM_PEAK_GBS = 8000.0
     dev = "cuda:0"
     attn = inputs.make_attention(w, 0, dev)
-    moe = inputs.make_layer(w, 0, dev)
+    moe = inputs.make_layer_fp8(w, 0, dev) if w.fp8 else inputs.make_layer(w, 0, dev)
     kv = inputs.make_kv_cache(w, 0, dev)
     layer = DecoderLayer(attn, moe, w.hq, w.hkv, w.k, w.theta, w.eps)
     h = inputs.make_h(w, dev)
@@ -217,8 +231,7 @@ def bench_decoder(args, w):
         B.moe_linear(b["attn"], layer.wo, b["o"], stream=stream)
         B.moe_combine(b["o"], T, d, 1, out_f32=h, residual=h, stream=stream)
         B.moe_rmsnorm(h, layer.gamma_moe, layer.eps, b["a2"], stream=stream)
-        B.moe_forward_ex(b["a2"], layer.router_w, layer.w1, layer.w3, layer.w2, layer.k, out_f32=h,
-                         router_bias=layer.router_bias, residual=h, stream=stream)
+        layer.moe_block(b["a2"], h, stream)
 
     for _ in range(args.warmup):
         step()
@@ -249,7 +262,8 @@ def bench_decoder(args, w):
     perm = torch.empty(T * w.k, dtype=torch.int32, device=dev)
     B.moe_route(b["a2"], layer.router_w, w.k, ids, gw, offs, perm)
     active = int((torch.diff(offs) > 0).sum())
-    moe_bytes = active * 3 * w.ffn * d * 2 + w.E * d * 2
+    moe_bytes = (active * 3 * w.ffn * d * (1 if w.fp8 else 2) + active * (2 * w.ffn + d) * 4 * w.fp8
+                 + w.E * d * 2)
     step_bytes = proj_bytes + moe_bytes + kv_bytes + T * d * 4 * 2
     gbs = step_bytes / (ms * 1e-3) / 1e9
     attn_gbs = kv_bytes / (attn_us * 1e-6) / 1e9

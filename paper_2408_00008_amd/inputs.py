@@ -130,6 +130,11 @@ WORKLOADS = {
     "decoder32_t64_ctx1024": Workload("decoder32_t64_ctx1024", 64, MIXTRAL_D, MIXTRAL_FFN,
                                       MIXTRAL_E, MIXTRAL_K, 1.0, 0.02, 0.02, 0.02, 0.02,
                                       layers=32, hq=32, hkv=8, ctx=1024),
+    # the same with 8-bit (E4M3, per-row scale) expert weights, the paper's
+    # 8-bit Mixtral
+    "decoder32_t64_ctx1024_fp8": Workload("decoder32_t64_ctx1024_fp8", 64, MIXTRAL_D, MIXTRAL_FFN,
+                                          MIXTRAL_E, MIXTRAL_K, 1.0, 0.02, 0.02, 0.02, 0.02,
+                                          layers=32, hq=32, hkv=8, ctx=1024, fp8=True),
     # 32 stacked layers, RMSNorm + residual around each, one decode step of 64
     "stack32_t64": Workload("stack32_t64", 64, MIXTRAL_D, MIXTRAL_FFN, MIXTRAL_E, MIXTRAL_K,
                             1.0, 0.02, 0.02, 0.02, 0.02, layers=32),

@@ -302,3 +302,42 @@ def test_decoder_stack_equals_layers():
         torch.cuda.synchronize()
         assert torch.equal(hg, h_ref)
 
+
+def test_decoder_layer_fp8_experts():
+    """With E4M3 expert weights the MoE block goes through the 8-bit path:
+    the layer's MoE delta matches the oracle's 8-bit layer on the GPU's own
+    block input."""
+    say("[decoder] layer with 8-bit experts")
+    w = small_workload(16, 256, 4, 2, ctx=40, page=16, ffn=256, seed=23).replace(fp8=True)
+    attn = inputs.make_attention(w, 0, DEV)
+    moe = inputs.make_layer_fp8(w, 0, DEV)
+    kv = inputs.make_kv_cache(w, 0, DEV)
+    layer = DecoderLayer(attn, moe, w.hq, w.hkv, w.k, w.theta)
+    h = inputs.make_h(w, DEV)
+    layer.step(h, kv["k_cache"], kv["v_cache"], kv["page_table"], kv["pos"], kv["ctx"])
+    torch.cuda.synchronize()
+    b = layer.buffers(w.T, DEV)
+    a2 = b["a2"]
+    h_before = h.clone()
+    h2 = h.clone()
+    layer.moe_block(a2, h2)
+    torch.cuda.synchronize()
+    o = orc()
+    ws = [moe[n].cpu().numpy() for n in ("w1q", "w1s", "w3q", "w3s", "w2q", "w2s")]
+    r = o.moe_layer_fp8(bits(a2), bits(moe["router_w"]), *ws, w.k)
+    ids = torch.empty(w.T, w.k, dtype=torch.int32, device=DEV)
+    gw = torch.empty(w.T, w.k, dtype=torch.float32, device=DEV)
+    offs = torch.empty(w.E + 1, dtype=torch.int32, device=DEV)
+    perm = torch.empty(w.T * w.k, dtype=torch.int32, device=DEV)
+    B.moe_route(a2, moe["router_w"], w.k, ids, gw, offs, perm)
+    torch.cuda.synchronize()
+    g_ids = ids.cpu().numpy()
+    amb = check_routing(g_ids, r["logits"], w.k)
+    ref = r["out"]
+    if amb.any():
+        gates = o.gates_for_ids(r["logits"], np.ascontiguousarray(g_ids, np.int32))
+        ref = o.moe_apply_fp8(bits(a2), *ws, g_ids, gates)
+    err = rowwise_rel(h2.cpu().numpy().astype(np.float64) - h_before.cpu().numpy(), ref)
+    say(f"  MoE block (8-bit) {err:.2e}")
+    assert err < OUT_TOL
+
