@@ -124,7 +124,14 @@ def main():
     offs = torch.empty(E + 1, dtype=torch.int32, device=dev)
     perm = torch.empty(A, dtype=torch.int32, device=dev)
     h = torch.empty(A, ffn, dtype=torch.bfloat16, device=dev)
-    y = torch.empty(A, d, dtype=torch.float32, device=dev)
+    # where the tiled kernels run, the down GEMM may cut its reduction into up
+    # to 4 parts written as separate slices (as moe_forward does)
+    variant = {1: "stream", 2: "tiled", 3: "split"}[B.moe_gemm_variant_for(T, d, ffn, E, k)]
+    if w.fp8 and variant == "tiled":
+        variant = "stream"  # 8-bit weights always stream
+    cut = variant == "tiled"
+    y = torch.empty(4 if cut else 1, A, d, dtype=torch.float32, device=dev)
+    parts = torch.ones(1, dtype=torch.int32, device=dev)
     out = torch.empty(T, d, dtype=torch.bfloat16, device=dev)
     stream = torch.cuda.current_stream()
 
@@ -139,11 +146,17 @@ def main():
         if ev1 is not None:
             ev1.record(stream)
         if w.fp8:
-            B.moe_swiglu_down_fp8(h, offs, q[4], q[5], T, k, y, topk_w=gw, perm=perm,
+            B.moe_swiglu_down_fp8(h, offs, q[4], q[5], T, k, y[0], topk_w=gw, perm=perm,
                                   stream=stream)
+        elif cut:
+            B.moe_swiglu_down_parts(h, offs, w2, T, k, y, parts, topk_w=gw, perm=perm,
+                                    stream=stream)
         else:
-            B.moe_swiglu_down(h, offs, w2, T, k, y, topk_w=gw, perm=perm, stream=stream)
-        B.moe_combine(y, T, d, k, out=out, stream=stream)
+            B.moe_swiglu_down(h, offs, w2, T, k, y[0], topk_w=gw, perm=perm, stream=stream)
+        if cut:
+            B.moe_combine_parts(y, parts, T, d, k, out=out, stream=stream)
+        else:
+            B.moe_combine(y[0], T, d, k, out=out, stream=stream)
 
     for _ in range(args.warmup):
         step()
@@ -170,9 +183,6 @@ def main():
 
     counts = np.diff(offs.cpu().numpy())
     active = int((counts > 0).sum())
-    variant = {1: "stream", 2: "tiled", 3: "split"}[B.moe_gemm_variant_for(T, d, ffn, E, k)]
-    if w.fp8 and variant == "tiled":
-        variant = "stream"  # 8-bit weights always stream
     # algorithmic work of the up kernel: each active expert's w1 and w3 once
     # (bf16, or E4M3 bytes plus one f32 scale per row), the routed token rows
     # read once, h written once; 4*d*ffn FLOP per row
@@ -223,7 +233,8 @@ def main():
         "config": {"workload": args.workload, "T": T, "d": d, "ffn": ffn, "E": E, "k": k,
                    "expert_weights": "e4m3 + f32 row scale" if w.fp8 else "bf16",
                    "router_bias0": w.bias0, "seed": args.seed, "active_experts": active,
-                   "rows_per_expert": counts.tolist()},
+                   "rows_per_expert": counts.tolist(),
+                   "down_reduction_parts": int(parts.item()) if cut else 1},
         "layer": {"tflops": round(layer_flops / (ms_per_step * 1e-3) / 1e12, 2),
                   "gbs": round(layer_bytes / (ms_per_step * 1e-3) / 1e9, 1),
                   "hbm_frac": round(layer_bytes / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),

@@ -121,6 +121,27 @@ moe_status_t moe_swiglu_down(const moe_bf16_t* h, const int32_t* expert_offsets,
                              hipStream_t stream);
 
 /*
+ * moe_swiglu_down with its reduction over ffn cut into parts (the same sums:
+ * y of moe_swiglu_down = the sum of the slices written here), for prefill
+ * sizes where the persistent tiled kernel runs (more than 64 rows per
+ * expert on average) and a few hundred output tiles would leave its last
+ * round of workgroups mostly idle.  y is [max_parts, T*k, d] f32: slice s
+ * receives the partial sum over the s-th part of ffn, gate-weighted and
+ * scattered as in moe_swiglu_down.  The number of parts used (1, 2 or 4; at
+ * most max_parts and at most ffn/512) is chosen on the device from the routed
+ * row counts and stored to *parts (device int32, 4-byte aligned); where the
+ * weight-streaming kernel runs the result is uncut and *parts = 1.  Slices at
+ * or past *parts are not written.  moe_combine_parts sums the slices;
+ * moe_forward runs this pair.  Errors as moe_swiglu_down, and
+ * MOE_ERR_INVALID_ARG for max_parts < 1 or parts NULL.
+ */
+moe_status_t moe_swiglu_down_parts(const moe_bf16_t* h, const int32_t* expert_offsets,
+                                   const moe_bf16_t* w2, const float* topk_w, const int32_t* perm,
+                                   int64_t T, int32_t d, int32_t ffn, int32_t E, int32_t k,
+                                   int32_t max_parts, float* y, int32_t* parts,
+                                   hipStream_t stream);
+
+/*
  * The grouped SwiGLU expert FFN on permuted rows: moe_swiglu_up(x_perm,
  * perm = NULL) into h_ws, then moe_swiglu_down into y (same meaning of
  * topk_w / perm as there).
@@ -145,11 +166,26 @@ moe_status_t moe_combine(const float* y, const float* residual, int64_t T, int32
                          moe_bf16_t* out, float* out_f32, hipStream_t stream);
 
 /*
+ * moe_combine over the slices of moe_swiglu_down_parts: y [max_parts,T*k,d]
+ * f32; each slot first sums its slices 0 .. n-1 in ascending order, with n =
+ * *parts (device int32, read by the kernel, clamped to [1, max_parts]), then
+ * the slots are summed as in moe_combine.
+ */
+moe_status_t moe_combine_parts(const float* y, const int32_t* parts, int32_t max_parts,
+                               const float* residual, int64_t T, int32_t d, int32_t k,
+                               moe_bf16_t* out, float* out_f32, hipStream_t stream);
+
+/*
  * The whole layer: route -> SwiGLU experts (the gather of token rows is fused
  * into the first expert GEMM) -> combine.  out [T,d] bf16, must not overlap
  * any input.  Scratch is owned by the library, cached per device and grown on
  * demand (a growth is refused with MOE_ERR_NO_MEMORY while `stream` is being
  * captured into a graph; call once outside capture first).
+ * At prefill sizes the down GEMM runs as moe_swiglu_down_parts with up to 4
+ * parts (the count depends on the routed row counts and the GPU's compute
+ * units) and the combine as moe_combine_parts, so the result can differ in
+ * the last bits from the uncut staged calls moe_grouped_swiglu + moe_combine;
+ * for the same inputs on the same GPU it is deterministic.
  */
 moe_status_t moe_forward(const moe_bf16_t* x, const moe_bf16_t* router_w, const moe_bf16_t* w1,
                          const moe_bf16_t* w3, const moe_bf16_t* w2, int64_t T, int32_t d,

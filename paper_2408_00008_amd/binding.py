@@ -22,8 +22,8 @@ MOE_OK, MOE_ERR_INVALID_ARG, MOE_ERR_UNSUPPORTED, MOE_ERR_NO_MEMORY, MOE_ERR_HIP
 VARIANT_AUTO, VARIANT_STREAM, VARIANT_TILED = 0, 1, 2
 
 EXPORTS = (
-    "moe_route", "moe_permute", "moe_swiglu_up", "moe_swiglu_down", "moe_grouped_swiglu",
-    "moe_combine", "moe_forward", "moe_forward_ex", "moe_rmsnorm", "moe_workspace_size",
+    "moe_route", "moe_permute", "moe_swiglu_up", "moe_swiglu_down", "moe_swiglu_down_parts",
+    "moe_grouped_swiglu", "moe_combine", "moe_combine_parts", "moe_forward", "moe_forward_ex", "moe_rmsnorm", "moe_workspace_size",
     "moe_swiglu_up_fp8", "moe_swiglu_down_fp8", "moe_forward_fp8_ex",
     "moe_linear", "moe_rope_kv_append", "moe_attention_decode",
     "moe_set_gemm_variant", "moe_gemm_variant_for", "moe_status_string", "moe_last_error", "moe_version",
@@ -59,7 +59,9 @@ def lib() -> ctypes.CDLL:
         "moe_swiglu_up": [p, p, p, p, p, i64, i32, i32, i32, i32, p, p],
         "moe_swiglu_down": [p, p, p, p, p, i64, i32, i32, i32, i32, p, p],
         "moe_grouped_swiglu": [p, p, p, p, p, p, p, i64, i32, i32, i32, i32, p, p, p],
+        "moe_swiglu_down_parts": [p, p, p, p, p, i64, i32, i32, i32, i32, i32, p, p, p],
         "moe_combine": [p, p, i64, i32, i32, p, p, p],
+        "moe_combine_parts": [p, p, i32, p, i64, i32, i32, p, p, p],
         "moe_forward": [p, p, p, p, p, i64, i32, i32, i32, i32, p, p],
         "moe_forward_ex": [p, p, p, p, p, p, i64, i32, i32, i32, i32, p, p, p, p, sz, p],
         "moe_rmsnorm": [p, p, i64, i32, f32, p, p],
@@ -154,6 +156,17 @@ def moe_swiglu_down(h, expert_offsets, w2, T, k, y, topk_w=None, perm=None, stre
                                  _stream(stream)), "moe_swiglu_down")
 
 
+def moe_swiglu_down_parts(h, expert_offsets, w2, T, k, y, parts, topk_w=None, perm=None,
+                          stream=None):
+    """y: [max_parts, T*k, d] f32 slices; parts: one device int32 receiving the count used."""
+    E, d, ffn = w2.shape
+    max_parts = y.shape[0]
+    _check(lib().moe_swiglu_down_parts(
+        _ptr(h, bf16, "h"), _ptr(expert_offsets, i32, "offsets"), _ptr(w2, bf16, "w2"),
+        _ptr(topk_w, f32, "topk_w"), _ptr(perm, i32, "perm"), T, d, ffn, E, k, max_parts,
+        _ptr(y, f32, "y"), _ptr(parts, i32, "parts"), _stream(stream)), "moe_swiglu_down_parts")
+
+
 def moe_grouped_swiglu(x_perm, expert_offsets, w1, w3, w2, T, k, h_ws, y, topk_w=None,
                        perm=None, stream=None):
     E, ffn, d = w1.shape
@@ -168,6 +181,14 @@ def moe_combine(y, T, d, k, out=None, out_f32=None, residual=None, stream=None):
     _check(lib().moe_combine(_ptr(y, f32, "y"), _ptr(residual, f32, "residual"), T, d, k,
                              _ptr(out, bf16, "out"), _ptr(out_f32, f32, "out_f32"),
                              _stream(stream)), "moe_combine")
+
+
+def moe_combine_parts(y, parts, T, d, k, out=None, out_f32=None, residual=None, stream=None):
+    """y: [max_parts, T*k, d] f32 slices of moe_swiglu_down_parts, parts its device count."""
+    _check(lib().moe_combine_parts(_ptr(y, f32, "y"), _ptr(parts, i32, "parts"), y.shape[0],
+                                   _ptr(residual, f32, "residual"), T, d, k,
+                                   _ptr(out, bf16, "out"), _ptr(out_f32, f32, "out_f32"),
+                                   _stream(stream)), "moe_combine_parts")
 
 
 def moe_forward(x, router_w, w1, w3, w2, k, out, stream=None):

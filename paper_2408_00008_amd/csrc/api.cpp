@@ -142,21 +142,45 @@ moe_status_t no_overlap(const char* oname, Range o, std::initializer_list<std::p
 
 size_t align256(size_t v) { return (v + 255) & ~size_t(255); }
 
+// Reduction parts the tiled down GEMM may use inside moe_forward: 1, 2 or 4,
+// each part at least 8 steps of 64 (the kernel picks the count on the
+// device from the real tile count).  Only where the tiled kernel runs by
+// default and the tiles fill fewer than 16 rounds of 256 workgroups, where a
+// cut evens out the last round.
+int parts_cap(int32_t ffn, int requested)
+{
+    const int steps = ffn / 64;
+    const int cap = steps >= 32 ? 4 : steps >= 16 ? 2 : 1;
+    const int r = requested >= 4 ? 4 : requested >= 2 ? 2 : 1;
+    return r < cap ? r : cap;
+}
+
+int down_split_max(int64_t A, int32_t d, int32_t ffn, int32_t E)
+{
+    if (A <= 64LL * E || !moe::tiled_supported(d, ffn)) return 1;
+    const int64_t items = (int64_t)(d / 256) * (A / 256 + E);
+    if (items >= 16 * 256) return 1;
+    return parts_cap(ffn, 4);
+}
+
 struct Layout {
-    size_t ids, w, off, perm, h, y, total;
+    size_t ids, w, off, perm, h, y, ns, total;
+    int nsplit;  // slices of y
 };
 
 Layout layout(int64_t T, int32_t d, int32_t ffn, int32_t E, int32_t k)
 {
     const size_t A = static_cast<size_t>(T) * k;
     Layout L{};
+    L.nsplit = down_split_max(static_cast<int64_t>(A), d, ffn, E);
     size_t o = 0;
     L.ids = o;  o += align256(A * 4);
     L.w = o;    o += align256(A * 4);
     L.off = o;  o += align256(static_cast<size_t>(E + 1) * 4);
     L.perm = o; o += align256(A * 4);
     L.h = o;    o += align256(A * static_cast<size_t>(ffn) * 2);
-    L.y = o;    o += align256(A * static_cast<size_t>(d) * 4);
+    L.y = o;    o += align256(A * static_cast<size_t>(d) * 4 * L.nsplit);
+    L.ns = o;   o += 256;
     L.total = o;
     return L;
 }
@@ -313,8 +337,12 @@ hipError_t run_up(const moe::UpArgs& a, int64_t T, hipStream_t stream)
     return moe::launch_stream_up(a, rmax, stream);
 }
 
-hipError_t run_down(const moe::DownArgs& a, int64_t T, int32_t k, hipStream_t stream)
+// *sliced: whether y was written as the reduction-part slices of the tiled
+// kernel (their count at a.ksplit_out)
+hipError_t run_down(const moe::DownArgs& a, int64_t T, int32_t k, hipStream_t stream,
+                    bool* sliced = nullptr)
 {
+    if (sliced) *sliced = false;
     const int64_t rmax = rows_bound(T, k);
     if (split_by_rows(rmax, a.A, a.E)) {
         moe::DownArgs light = a, heavy = a;
@@ -327,8 +355,10 @@ hipError_t run_down(const moe::DownArgs& a, int64_t T, int32_t k, hipStream_t st
     }
     if (a.q2) return moe::launch_stream_down(a, rmax, stream);
     const int v = moe::resolve_variant(g_variant.load(), a.A, a.E);
-    if (v == moe::VARIANT_TILED && moe::tiled_supported(a.d, a.ffn))
+    if (v == moe::VARIANT_TILED && moe::tiled_supported(a.d, a.ffn)) {
+        if (sliced) *sliced = a.ksplit_out != nullptr;
         return moe::launch_tiled_down(a, stream);
+    }
     return moe::launch_stream_down(a, rmax, stream);
 }
 
@@ -377,10 +407,12 @@ moe_status_t swiglu_up_impl(const moe_bf16_t* x_perm, const int32_t* perm,
     return e == hipSuccess ? ok() : hip_fail(e, "expert up kernel launch");
 }
 
+// max_parts > 1 with parts != null: y holds max_parts slices [A,d] for the
+// reduction parts of the tiled kernel, their count stored to *parts
 moe_status_t swiglu_down_impl(const moe_bf16_t* h, const int32_t* expert_offsets,
                               const ExpertWeights& w, const float* topk_w, const int32_t* perm,
                               int64_t T, int32_t d, int32_t ffn, int32_t E, int32_t k, float* y,
-                              hipStream_t stream)
+                              hipStream_t stream, int max_parts = 1, int32_t* parts = nullptr)
 {
     TRY(check_Ek_stage(E, k));
     TRY(check_T(T, k));
@@ -398,14 +430,32 @@ moe_status_t swiglu_down_impl(const moe_bf16_t* h, const int32_t* expert_offsets
     ins.push_back({"topk_w", {topk_w, A * 4}});
     ins.push_back({"perm", {perm, A * 4}});
     ins.push_back({"expert_offsets", {expert_offsets, (size_t)(E + 1) * 4}});
-    TRY(no_overlap_v("y", {y, A * d * 4}, ins));
-    if (T == 0) return ok();
+    const size_t ybytes = A * d * 4 * static_cast<size_t>(max_parts);
+    if (parts) {
+        ins.push_back({"y", {y, ybytes}});
+        TRY(no_overlap_v("parts", {parts, 4}, ins));
+        ins.pop_back();
+    }
+    TRY(no_overlap_v("y", {y, ybytes}, ins));
+    if (T == 0) {
+        if (!parts) return ok();
+        hipError_t e = moe::launch_fill_i32(parts, 1, stream);
+        return e == hipSuccess ? ok() : hip_fail(e, "fill kernel launch");
+    }
     const bool scatter = topk_w && perm;
     moe::DownArgs a{h, expert_offsets, w.w2, scatter ? topk_w : nullptr, scatter ? perm : nullptr,
                     y, (int64_t)A, d, ffn, E};
     a.q2 = w.q2, a.s2 = w.s2;
-    hipError_t e = run_down(a, T, k, stream);
-    return e == hipSuccess ? ok() : hip_fail(e, "expert down kernel launch");
+    a.ksplit_max = parts ? parts_cap(ffn, max_parts) : 1;
+    a.ksplit_out = parts;
+    bool sliced = false;
+    hipError_t e = run_down(a, T, k, stream, &sliced);
+    if (e != hipSuccess) return hip_fail(e, "expert down kernel launch");
+    if (parts && !sliced) {
+        e = moe::launch_fill_i32(parts, 1, stream);
+        if (e != hipSuccess) return hip_fail(e, "fill kernel launch");
+    }
+    return ok();
 }
 
 moe_status_t forward_impl(const moe_bf16_t* x, const moe_bf16_t* router_w,
@@ -474,9 +524,13 @@ moe_status_t forward_impl(const moe_bf16_t* x, const moe_bf16_t* router_w,
     if (e != hipSuccess) return hip_fail(e, "expert up kernel launch");
     moe::DownArgs da{h, offs, w.w2, gw, perm, y, A, d, ffn, E};
     da.q2 = w.q2, da.s2 = w.s2;
-    e = run_down(da, T, k, stream);
+    da.ksplit_max = L.nsplit;
+    da.ksplit_out = reinterpret_cast<int*>(b + L.ns);
+    bool sliced = false;
+    e = run_down(da, T, k, stream, &sliced);
     if (e != hipSuccess) return hip_fail(e, "expert down kernel launch");
-    e = moe::launch_combine(y, residual, T, d, k, out, out_f32, stream);
+    e = moe::launch_combine(y, residual, T, d, k, out, out_f32, stream,
+                            sliced ? da.ksplit_out : nullptr, L.nsplit);
     if (e != hipSuccess) return hip_fail(e, "combine kernel launch");
     return ok();
 }
@@ -522,6 +576,37 @@ moe_status_t check_cache(int32_t page, int32_t maxp, int64_t npages)
     if ((int64_t)page * maxp >= (int64_t(1) << 31) || npages >= (int64_t(1) << 31))
         return fail(MOE_ERR_UNSUPPORTED, "cache geometry too large");
     return MOE_OK;
+}
+}  // namespace
+
+namespace {
+moe_status_t combine_impl(const float* y, const int32_t* parts, int32_t max_parts,
+                          const float* residual, int64_t T, int32_t d, int32_t k,
+                          moe_bf16_t* out, float* out_f32, hipStream_t stream)
+{
+    if (k < 1 || k > kMaxK) return fail(k < 1 ? MOE_ERR_INVALID_ARG : MOE_ERR_UNSUPPORTED,
+                                        "k=%d out of range", k);
+    TRY(check_T(T, k));
+    TRY(check_dim("d", d));
+    TRY(need_rows(y, "y", T));
+    TRY(maybe(residual, "residual"));
+    TRY(maybe(out, "out"));
+    TRY(maybe(out_f32, "out_f32"));
+    if (!out && !out_f32 && T > 0)
+        return fail(MOE_ERR_INVALID_ARG, "out and out_f32 are both NULL");
+    const size_t A = static_cast<size_t>(T) * k;
+    const size_t td = static_cast<size_t>(T) * d;
+    const size_t yb = A * d * 4 * static_cast<size_t>(max_parts);
+    TRY(no_overlap("out", {out, td * 2}, {{"y", {y, yb}}, {"residual", {residual, td * 4}},
+                   {"out_f32", {out_f32, td * 4}}, {"parts", {parts, 4}}}));
+    if (out_f32 != residual)
+        TRY(no_overlap("out_f32", {out_f32, td * 4}, {{"y", {y, yb}}, {"residual", {residual, td * 4}},
+                       {"parts", {parts, 4}}}));
+    else
+        TRY(no_overlap("out_f32", {out_f32, td * 4}, {{"y", {y, yb}}, {"parts", {parts, 4}}}));
+    if (T == 0) return ok();
+    hipError_t e = moe::launch_combine(y, residual, T, d, k, out, out_f32, stream, parts, max_parts);
+    return e == hipSuccess ? ok() : hip_fail(e, "combine kernel launch");
 }
 }  // namespace
 
@@ -592,6 +677,21 @@ moe_status_t moe_swiglu_down(const moe_bf16_t* h, const int32_t* expert_offsets,
                             T, d, ffn, E, k, y, stream);
 }
 
+moe_status_t moe_swiglu_down_parts(const moe_bf16_t* h, const int32_t* expert_offsets,
+                                   const moe_bf16_t* w2, const float* topk_w, const int32_t* perm,
+                                   int64_t T, int32_t d, int32_t ffn, int32_t E, int32_t k,
+                                   int32_t max_parts, float* y, int32_t* parts,
+                                   hipStream_t stream)
+{
+    if (max_parts < 1) return fail(MOE_ERR_INVALID_ARG, "max_parts=%d must be >= 1", max_parts);
+    if (!parts) return fail(MOE_ERR_INVALID_ARG, "parts is NULL");
+    if (reinterpret_cast<uintptr_t>(parts) & 3u)
+        return fail(MOE_ERR_INVALID_ARG, "parts is not 4-byte aligned");
+    // the slices the caller sized y for; the kernel uses at most parts_cap of them
+    return swiglu_down_impl(h, expert_offsets, bf16_weights(nullptr, nullptr, w2), topk_w, perm,
+                            T, d, ffn, E, k, y, stream, max_parts, parts);
+}
+
 moe_status_t moe_swiglu_up_fp8(const moe_bf16_t* x_perm, const int32_t* perm,
                                const int32_t* expert_offsets, const uint8_t* w1q,
                                const float* w1s, const uint8_t* w3q, const float* w3s, int64_t T,
@@ -638,27 +738,18 @@ moe_status_t moe_grouped_swiglu(const moe_bf16_t* x_perm, const int32_t* expert_
 moe_status_t moe_combine(const float* y, const float* residual, int64_t T, int32_t d, int32_t k,
                          moe_bf16_t* out, float* out_f32, hipStream_t stream)
 {
-    if (k < 1 || k > kMaxK) return fail(k < 1 ? MOE_ERR_INVALID_ARG : MOE_ERR_UNSUPPORTED,
-                                        "k=%d out of range", k);
-    TRY(check_T(T, k));
-    TRY(check_dim("d", d));
-    TRY(need_rows(y, "y", T));
-    TRY(maybe(residual, "residual"));
-    TRY(maybe(out, "out"));
-    TRY(maybe(out_f32, "out_f32"));
-    if (!out && !out_f32 && T > 0)
-        return fail(MOE_ERR_INVALID_ARG, "out and out_f32 are both NULL");
-    const size_t A = static_cast<size_t>(T) * k;
-    const size_t td = static_cast<size_t>(T) * d;
-    TRY(no_overlap("out", {out, td * 2}, {{"y", {y, A * d * 4}}, {"residual", {residual, td * 4}},
-                   {"out_f32", {out_f32, td * 4}}}));
-    if (out_f32 != residual)
-        TRY(no_overlap("out_f32", {out_f32, td * 4}, {{"y", {y, A * d * 4}}, {"residual", {residual, td * 4}}}));
-    else
-        TRY(no_overlap("out_f32", {out_f32, td * 4}, {{"y", {y, A * d * 4}}}));
-    if (T == 0) return ok();
-    hipError_t e = moe::launch_combine(y, residual, T, d, k, out, out_f32, stream);
-    return e == hipSuccess ? ok() : hip_fail(e, "combine kernel launch");
+    return combine_impl(y, nullptr, 1, residual, T, d, k, out, out_f32, stream);
+}
+
+moe_status_t moe_combine_parts(const float* y, const int32_t* parts, int32_t max_parts,
+                               const float* residual, int64_t T, int32_t d, int32_t k,
+                               moe_bf16_t* out, float* out_f32, hipStream_t stream)
+{
+    if (max_parts < 1) return fail(MOE_ERR_INVALID_ARG, "max_parts=%d must be >= 1", max_parts);
+    if (!parts) return fail(MOE_ERR_INVALID_ARG, "parts is NULL");
+    if (reinterpret_cast<uintptr_t>(parts) & 3u)
+        return fail(MOE_ERR_INVALID_ARG, "parts is not 4-byte aligned");
+    return combine_impl(y, parts, max_parts, residual, T, d, k, out, out_f32, stream);
 }
 
 size_t moe_workspace_size(int64_t T, int32_t d, int32_t ffn, int32_t E, int32_t k)

@@ -27,11 +27,16 @@ __global__ __launch_bounds__(256) void permute_kernel(const bf16_t* __restrict__
 // s = residual + sum_{j ascending} y[t*k+j]; out = bf16(s), out_f32 = s
 __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ y,
                                                       const float* residual, int64_t T, int d,
-                                                      int k, bf16_t* __restrict__ out,
+                                                      int k, const int* nslices,
+                                                      int max_slices, bf16_t* __restrict__ out,
                                                       float* out_f32)
 {
     const int cpr = d >> 2;  // float4 per row
     const int64_t total = T * cpr;
+    // y may hold the partial sums of several reduction parts, slice s at
+    // y + s * T * k * d; each slot sums its slices in ascending order
+    const int ns = nslices ? min(max(*nslices, 1), max_slices) : 1;
+    const int64_t slice = T * k * d;
     for (int64_t q = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; q < total;
          q += (int64_t)gridDim.x * blockDim.x) {
         const int64_t t = q / cpr;
@@ -39,7 +44,15 @@ __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ 
         float4 s = residual ? *reinterpret_cast<const float4*>(residual + t * d + c * 4)
                             : make_float4(0.f, 0.f, 0.f, 0.f);
         for (int j = 0; j < k; ++j) {
-            const float4 v = *reinterpret_cast<const float4*>(y + (t * k + j) * d + c * 4);
+            const float* yj = y + (t * k + j) * d + c * 4;
+            float4 v = *reinterpret_cast<const float4*>(yj);
+            for (int q = 1; q < ns; ++q) {
+                const float4 u = *reinterpret_cast<const float4*>(yj + q * slice);
+                v.x += u.x;
+                v.y += u.y;
+                v.z += u.z;
+                v.w += u.w;
+            }
             s.x += v.x;
             s.y += v.y;
             s.z += v.z;
@@ -110,11 +123,20 @@ hipError_t launch_permute(const bf16_t* x, const int32_t* perm, int64_t A, int d
 }
 
 hipError_t launch_combine(const float* y, const float* residual, int64_t T, int d, int k,
-                          bf16_t* out, float* out_f32, hipStream_t stream)
+                          bf16_t* out, float* out_f32, hipStream_t stream, const int* nslices,
+                          int max_slices)
 {
     if (T == 0) return hipSuccess;
-    combine_kernel<<<grid_for(T * (d / 4), 256), 256, 0, stream>>>(y, residual, T, d, k, out,
-                                                                   out_f32);
+    combine_kernel<<<grid_for(T * (d / 4), 256), 256, 0, stream>>>(y, residual, T, d, k, nslices,
+                                                                   max_slices, out, out_f32);
+    return hipGetLastError();
+}
+
+__global__ void fill_i32_kernel(int32_t* p, int32_t v) { *p = v; }
+
+hipError_t launch_fill_i32(int32_t* p, int32_t v, hipStream_t stream)
+{
+    fill_i32_kernel<<<1, 1, 0, stream>>>(p, v);
     return hipGetLastError();
 }
 

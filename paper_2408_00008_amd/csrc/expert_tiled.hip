@@ -17,7 +17,10 @@
 //     ordered expert, weight block, token tile, so the workgroups of one XCD
 //     work on the token tiles of a few weight blocks at a time and share both
 //     operands through that XCD's L2.  Per-expert tile counts are read from
-//     the device-side offsets: ragged row counts need no host synchronisation.
+//     the device-side offsets: ragged row counts need no host synchronisation;
+//   * DOWN may cut each tile's reduction into 2 or 4 parts (items then ordered
+//     expert, part, weight block, token tile), chosen on the device from the
+//     tile count, when that evens out the rounds of the persistent grid.
 #include <type_traits>
 
 #include "common.hpp"
@@ -40,6 +43,13 @@ struct TiledParams {
     const float* topk_w;     // DOWN, null = unweighted row order
     const int32_t* perm;     // DOWN
     int mlo, mhi;            // experts with mlo <= rows <= mhi only
+    // DOWN: the reduction may be cut into up to ksplit_max parts, part s
+    // writing the slice y_out + s * slice; the parts chosen are stored to
+    // *ksplit_out (if not null) for the kernel that sums the slices
+    int ksplit_max;
+    int64_t slice;
+    int* ksplit_out;
+    int64_t A;
 };
 
 int cu_count();
@@ -102,6 +112,32 @@ __device__ __forceinline__ void wait_vmem()
 // s_waitcnt lgkmcnt(0) with vmcnt/expcnt at max
 __device__ __forceinline__ void wait_lds() { __builtin_amdgcn_s_waitcnt(0xC07F); }
 
+// Parts of the down GEMM's reduction.  The persistent workgroups of an XCD
+// take its items in rounds, so the layer costs ceil(share / workgroups)
+// rounds of one item; with a few hundred 256 x 256 tiles over 256 CUs the
+// last round is mostly idle (560 tiles: 3 rounds for 2.2 rounds of work).
+// Cutting every tile's reduction into S parts gives S times as many items of
+// 1/S of the steps, which evens out the rounds, at the price of a start-up
+// and an output store per item and S - 1 more f32 slices for the combine to
+// read.  Cost in reduction steps (one step = 64 elements of the reduction,
+// ~1.5 us on the 4096 x 14336 shapes): per item nk / S + 6, per extra slice
+// A * N / 1.8e6 (its read at ~5 TB/s).
+__device__ __forceinline__ int down_parts(int total, int per_xcd, int nk, int64_t A, int N, int smax)
+{
+    int best = 1;
+    float best_cost = 3.0e38f;
+    for (int s = 1; s <= smax && s <= nk; s *= 2) {
+        const int share = (total * s + 7) / 8;
+        const int rounds = (share + per_xcd - 1) / per_xcd;
+        const float cost = rounds * ((float)nk / s + 6.0f) + (s - 1) * ((float)A * N / 1.8e6f);
+        if (cost < best_cost) {
+            best_cost = cost;
+            best = s;
+        }
+    }
+    return best;
+}
+
 template <bool UP>
 __global__ __launch_bounds__(256) void q_kernel(TiledParams p)
 {
@@ -125,14 +161,18 @@ __global__ __launch_bounds__(256) void q_kernel(TiledParams p)
         const int v = __shfl_up(in_tiles, o, 64);
         if (lane >= o) in_tiles += v;
     }
-    const int ex_items = nbn * (in_tiles - my_tiles);
-    const int total = nbn * __shfl(in_tiles, p.E - 1, 64);
     const int xcd = blockIdx.x & 7;
     const int per_xcd = gridDim.x >> 3;
     const int local = blockIdx.x >> 3;
+    const int nk = p.K / C::BK;
+    // items: expert, reduction part, weight block, token tile
+    const int nparts = UP ? 1 : down_parts(nbn * __shfl(in_tiles, p.E - 1, 64), per_xcd, nk, p.A, p.N,
+                                           p.ksplit_max);
+    if (!UP && p.ksplit_out && blockIdx.x == 0 && tid == 0) *p.ksplit_out = nparts;
+    const int ex_items = nparts * nbn * (in_tiles - my_tiles);
+    const int total = nparts * nbn * __shfl(in_tiles, p.E - 1, 64);
     const int beg = (int)((int64_t)total * xcd / 8);
     const int end = (int)((int64_t)total * (xcd + 1) / 8);
-    const int nk = p.K / C::BK;
 
     // a load covers 8 rows starting at a multiple of 8: lane l takes row l / 8
     // and the global chunk stored at slot l % 8 (odd loads start at 8 mod 16)
@@ -154,9 +194,14 @@ __global__ __launch_bounds__(256) void q_kernel(TiledParams p)
         const uint64_t le = __ballot(lane < p.E && my_tiles > 0 && ex_items <= w);
         const int e = 63 - __builtin_clzll(le);
         const int mt_e = __shfl(my_tiles, e, 64);
-        const int r = w - __shfl(ex_items, e, 64);
+        int r = w - __shfl(ex_items, e, 64);
+        const int part = r / (nbn * mt_e);
+        r -= part * nbn * mt_e;
         const int nb = r / mt_e;
         const int mtile = r - nb * mt_e;
+        // this item's reduction steps [k0, k0 + kn)
+        const int k0 = (int)((int64_t)nk * part / nparts);
+        const int kn = (int)((int64_t)nk * (part + 1) / nparts) - k0;
         const int row0 = p.offsets[e];
         const int M = p.offsets[e + 1] - row0;
         const int m0 = mtile * C::BM;
@@ -172,7 +217,7 @@ __global__ __launch_bounds__(256) void q_kernel(TiledParams p)
                 base = p.wb;
                 wrow -= C::BN / 2;
             }
-            abase = base + ((int64_t)e * p.N + wrow) * p.K;
+            abase = base + ((int64_t)e * p.N + wrow) * p.K + k0 * C::BK;
         }
         const bf16_t* aptr[2] = {abase + (int64_t)lrow * p.K + lchunk[0] * 8,
                                  abase + (int64_t)lrow * p.K + lchunk[1] * 8};
@@ -182,19 +227,19 @@ __global__ __launch_bounds__(256) void q_kernel(TiledParams p)
             const int tr = 64 * wave + 8 * i + lrow;
             const int rowm = row0 + m0 + (tr < Mp ? tr : Mp - 1);
             const int64_t src = (UP && p.gather) ? p.gather[rowm] / p.kslots : rowm;
-            bptr[i] = p.act + src * p.K + lchunk[i & 1] * 8;
+            bptr[i] = p.act + src * p.K + k0 * C::BK + lchunk[i & 1] * 8;
         }
         const int64_t astep = (int64_t)8 * p.K;  // elements between a wave's consecutive A loads
         auto load_a = [&](int s, int i) {
             unsigned char* st = ring + (s % 3) * C::SLOT;
-            int64_t ko = (int64_t)(s < nk ? s : nk - 1) * C::BK + i * astep;
+            int64_t ko = (int64_t)(s < kn ? s : kn - 1) * C::BK + i * astep;
             __builtin_amdgcn_global_load_lds(
                 (const void __attribute__((address_space(1)))*)(aptr[i & 1] + ko),
                 (void __attribute__((address_space(3)))*)(st + (64 * wave + 8 * i) * C::ROWB), 16, 0, 0);
         };
         auto load_b = [&](int s, int i) {
             unsigned char* st = ring + C::B_OFF + (s & 1) * C::SLOT;
-            const int ko = (s < nk ? s : nk - 1) * C::BK;
+            const int ko = (s < kn ? s : kn - 1) * C::BK;
             __builtin_amdgcn_global_load_lds(
                 (const void __attribute__((address_space(1)))*)(bptr[i] + ko),
                 (void __attribute__((address_space(3)))*)(st + (64 * wave + 8 * i) * C::ROWB), 16, 0, 0);
@@ -261,11 +306,11 @@ __global__ __launch_bounds__(256) void q_kernel(TiledParams p)
             // After k-step 2 every wave waits for its reads of step j's last
             // fragments and for its loads up to B(j+1), then one barrier makes
             // A(j+1), B(j+1) complete and frees the slots of A(j), B(j).
-            for (int j = 0; j < nk; ++j) {
+            for (int j = 0; j < kn; ++j) {
     #pragma unroll
                 for (int ks = 0; ks < 4; ++ks) {
                     const int cur = ks & 1;
-                    // (in the last step k-step 3 reads step nk's slots, which hold
+                    // (in the last step k-step 3 reads step kn's slots, which hold
                     // the redundant re-loads; the values are not used)
                     const int rs = ks < 3 ? j : j + 1, rk = ks < 3 ? ks + 1 : 0;
     #pragma unroll
@@ -333,7 +378,8 @@ __global__ __launch_bounds__(256) void q_kernel(TiledParams p)
                         orow = p.perm[rrow];
                         gw = p.topk_w[orow];
                     }
-                    float* yrow = p.y_out + orow * p.N + nb * C::NOUT + wr * 128 + 4 * (lane >> 5);
+                    float* yrow = p.y_out + part * p.slice + orow * p.N + nb * C::NOUT + wr * 128 +
+                                  4 * (lane >> 5);
     #pragma unroll
                     for (int nt = 0; nt < NT; ++nt) {
                         asm volatile("" : "+a"(acc[nt][mt]));
@@ -380,7 +426,7 @@ hipError_t run_q(const TiledParams& p, int64_t A, hipStream_t stream)
         attr_set = true;
     }
     const int64_t nbn = p.N / C::NOUT;
-    const int64_t items = nbn * (A / C::BM + p.E);
+    const int64_t items = nbn * (A / C::BM + p.E) * (UP ? 1 : p.ksplit_max);
     int64_t grid = cu_count();
     if (grid > items) grid = items;
     grid = ((grid + 7) / 8) * 8;
@@ -425,6 +471,8 @@ hipError_t launch_tiled_up(const UpArgs& a, hipStream_t stream)
     p.h_out = a.h;
     p.mlo = a.mlo;
     p.mhi = a.mhi;
+    p.ksplit_max = 1;
+    p.A = a.A;
     return run_q<true>(p, a.A, stream);
 }
 
@@ -442,6 +490,10 @@ hipError_t launch_tiled_down(const DownArgs& a, hipStream_t stream)
     p.perm = a.perm;
     p.mlo = a.mlo;
     p.mhi = a.mhi;
+    p.ksplit_max = a.ksplit_max > 1 ? a.ksplit_max : 1;
+    p.slice = a.A * a.d;
+    p.ksplit_out = a.ksplit_out;
+    p.A = a.A;
     return run_q<false>(p, a.A, stream);
 }
 

@@ -24,8 +24,14 @@ hipError_t launch_dispatch(const int32_t* topk_ids, int64_t A, int E, int32_t* o
 hipError_t launch_permute(const bf16_t* x, const int32_t* perm, int64_t A, int d, int k,
                           bf16_t* x_perm, hipStream_t stream);
 
+// nslices (device int, null = 1, clamped to [1, max_slices]): y holds that
+// many partial-sum slices of [T*k, d], summed per slot in ascending order
 hipError_t launch_combine(const float* y, const float* residual, int64_t T, int d, int k,
-                          bf16_t* out, float* out_f32, hipStream_t stream);
+                          bf16_t* out, float* out_f32, hipStream_t stream,
+                          const int* nslices = nullptr, int max_slices = 1);
+
+// *p = v, stream-ordered (a kernel, so it may be captured into a graph)
+hipError_t launch_fill_i32(int32_t* p, int32_t v, hipStream_t stream);
 
 hipError_t launch_rmsnorm(const float* h, const bf16_t* gamma, int64_t T, int d, float eps,
                           bf16_t* a, hipStream_t stream);
@@ -86,6 +92,11 @@ struct DownArgs {
     const float* s2 = nullptr;
     int mlo = 0, mhi = 0x7fffffff;
     int groups = 0;
+    // tiled kernel: y has room for ksplit_max slices [A,d]; the kernel picks
+    // how many reduction parts to use (1 = y only) and stores that count to
+    // *ksplit_out (device int, may be null)
+    int ksplit_max = 1;
+    int* ksplit_out = nullptr;
 };
 
 enum GemmVariant { VARIANT_AUTO = 0, VARIANT_STREAM = 1, VARIANT_TILED = 2 };

@@ -112,6 +112,40 @@ def test_route_and_stage_rejects(L):
     del p
 
 
+def test_parts_entry_points_reject(L):
+    """The cut down GEMM and its combine: the part count pointer and bound are
+    checked, and y's full extent (max_parts slices) may overlap nothing."""
+    T, d, ffn, E, k = 4, 128, 256, 8, 2
+    yb = T * k * d * 4  # one slice
+    w2 = 1 << 36
+    y, parts = 1 << 38, 1 << 39
+
+    def down(**kw):
+        a = dict(mp=4, y=y, parts=parts, w2=w2)
+        a.update(kw)
+        return L.moe_swiglu_down_parts(X, 0x700000, a["w2"], None, None, T, d, ffn, E, k,
+                                       a["mp"], a["y"], a["parts"], None)
+
+    assert down(mp=0) == B.MOE_ERR_INVALID_ARG and b"max_parts" in L.moe_last_error()
+    assert down(parts=None) == B.MOE_ERR_INVALID_ARG and b"parts is NULL" in L.moe_last_error()
+    assert down(parts=parts + 2) == B.MOE_ERR_INVALID_ARG and b"4-byte" in L.moe_last_error()
+    # the count inside the last slice; the last slice over w2
+    assert down(parts=y + 3 * yb + 64) == B.MOE_ERR_INVALID_ARG
+    assert b"parts overlaps y" in L.moe_last_error()
+    assert down(y=w2 - 3 * yb - 256) == B.MOE_ERR_INVALID_ARG
+    assert b"y overlaps w2" in L.moe_last_error()
+
+    def comb(**kw):
+        a = dict(mp=4, parts=parts, out=OUT)
+        a.update(kw)
+        return L.moe_combine_parts(y, a["parts"], a["mp"], None, T, d, k, a["out"], None, None)
+
+    assert comb(mp=0) == B.MOE_ERR_INVALID_ARG and b"max_parts" in L.moe_last_error()
+    assert comb(parts=None) == B.MOE_ERR_INVALID_ARG and b"parts is NULL" in L.moe_last_error()
+    assert comb(out=y + 3 * yb) == B.MOE_ERR_INVALID_ARG and b"overlaps y" in L.moe_last_error()
+    assert comb(out=parts - 64) == B.MOE_ERR_INVALID_ARG and b"overlaps parts" in L.moe_last_error()
+
+
 def test_forward_ex_workspace_checks(L):
     big = 1 << 40
     args = [X, RW, None, big, 2 * big, 3 * big, 4, 128, 256, 8, 2, None, 4 * big, None]

@@ -226,6 +226,54 @@ def test_forward_split_by_rows(shape):
     _forward_check(c, variant=0)
 
 
+@pytest.mark.parametrize("shape,parts", [
+    ((288, 256, 2048, 8, 2), 4),   # one token tile per expert, 4 parts of 8 steps
+    ((600, 512, 1024, 8, 2), 2),   # 2 weight blocks per expert, 2 parts of 8 steps
+])
+def test_forward_down_split(shape, parts):
+    """Prefill-regime sizes with few token tiles: the tiled down GEMM cuts its
+    reduction into parts written as separate f32 slices that the combine
+    sums.  Parity with the oracle; the part count the kernel chose (the int
+    in the last 256 bytes of the forward's workspace); and agreement with the
+    staged calls, which run the same GEMM uncut."""
+    say(f"[forward] down reduction split {shape}")
+    c = small_case(*shape, seed=29)
+    assert B.moe_gemm_variant_for(c.T, c.d, c.ffn, c.E, c.k) == 2
+    _forward_check(c, variant=0)
+    T, d, k = c.T, c.d, c.k
+    ws = torch.empty(B.moe_workspace_size(T, d, c.ffn, c.E, k), dtype=torch.uint8, device=DEV)
+    of = torch.empty(T, d, dtype=torch.float32, device=DEV)
+    B.moe_forward_ex(c.x, c.router_w, c.w1, c.w3, c.w2, k, out_f32=of, workspace=ws)
+    torch.cuda.synchronize()
+    assert int(ws[-256:].view(torch.int32)[0]) == parts
+    ids, gw, offs, perm, _ = gpu_route(c)
+    xp = torch.empty(T * k, d, dtype=torch.bfloat16, device=DEV)
+    B.moe_permute(c.x, perm, k, xp)
+    h = torch.empty(T * k, c.ffn, dtype=torch.bfloat16, device=DEV)
+    y = torch.empty(T * k, d, dtype=torch.float32, device=DEV)
+    B.moe_grouped_swiglu(xp, offs, c.w1, c.w3, c.w2, T, k, h, y, topk_w=gw, perm=perm)
+    staged = torch.empty(T, d, dtype=torch.float32, device=DEV)
+    B.moe_combine(y, T, d, k, out_f32=staged)
+    torch.cuda.synchronize()
+    err = rowwise_rel(of.double().cpu().numpy(), staged.double().cpu().numpy())
+    say(f"  forward (cut) vs staged (uncut): rowwise rel {err:.3e}")
+    assert err < 1e-5
+    # the staged pair that the forward runs gives the same bits
+    yp = torch.empty(4, T * k, d, dtype=torch.float32, device=DEV)
+    np_dev = torch.zeros(1, dtype=torch.int32, device=DEV)
+    B.moe_swiglu_down_parts(h, offs, c.w2, T, k, yp, np_dev, topk_w=gw, perm=perm)
+    st2 = torch.empty(T, d, dtype=torch.float32, device=DEV)
+    B.moe_combine_parts(yp, np_dev, T, d, k, out_f32=st2)
+    torch.cuda.synchronize()
+    assert int(np_dev.item()) == parts
+    assert torch.equal(st2, of)
+    # the same inputs give the same bits
+    of2 = torch.empty_like(of)
+    B.moe_forward_ex(c.x, c.router_w, c.w1, c.w3, c.w2, k, out_f32=of2, workspace=ws)
+    torch.cuda.synchronize()
+    assert torch.equal(of, of2)
+
+
 def test_forward_t0():
     c = small_case(3, 64, 64, 4, 2)
     out = torch.zeros(0, 64, dtype=torch.bfloat16, device=DEV)
