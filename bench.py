@@ -124,13 +124,15 @@ def main():
     offs = torch.empty(E + 1, dtype=torch.int32, device=dev)
     perm = torch.empty(A, dtype=torch.int32, device=dev)
     h = torch.empty(A, ffn, dtype=torch.bfloat16, device=dev)
-    # where the tiled kernels run, the down GEMM may cut its reduction into up
-    # to 4 parts written as separate slices (as moe_forward does)
+    # as in moe_forward, the down GEMM may cut its reduction into parts written
+    # as separate slices: up to 4 where the tiled kernels run, up to 8 for
+    # the heavy experts of a split streaming step
     variant = {1: "stream", 2: "tiled", 3: "split"}[B.moe_gemm_variant_for(T, d, ffn, E, k)]
     if w.fp8 and variant == "tiled":
         variant = "stream"  # 8-bit weights always stream
-    cut = variant == "tiled"
-    y = torch.empty(4 if cut else 1, A, d, dtype=torch.float32, device=dev)
+    cut = variant in ("tiled", "split") and not w.fp8
+    y = torch.empty({"tiled": 4, "split": 8}[variant] if cut else 1, A, d, dtype=torch.float32,
+                    device=dev)
     parts = torch.ones(1, dtype=torch.int32, device=dev)
     out = torch.empty(T, d, dtype=torch.bfloat16, device=dev)
     stream = torch.cuda.current_stream()

@@ -127,12 +127,16 @@ moe_status_t moe_swiglu_down(const moe_bf16_t* h, const int32_t* expert_offsets,
  * expert on average) and a few hundred output tiles would leave its last
  * round of workgroups mostly idle.  y is [max_parts, T*k, d] f32: slice s
  * receives the partial sum over the s-th part of ffn, gate-weighted and
- * scattered as in moe_swiglu_down.  The number of parts used (1, 2 or 4; at
- * most max_parts and at most ffn/512) is chosen on the device from the routed
- * row counts and stored to *parts (device int32, 4-byte aligned); where the
- * weight-streaming kernel runs the result is uncut and *parts = 1.  Slices at
- * or past *parts are not written.  moe_combine_parts sums the slices;
- * moe_forward runs this pair.  Errors as moe_swiglu_down, and
+ * scattered as in moe_swiglu_down.  The number of parts used (a power of two
+ * up to 16, at most max_parts, each part at least 512 elements of ffn) is
+ * chosen on the device from the routed row counts and stored to *parts
+ * (device int32, 4-byte aligned).  In the streaming regime (up to 64 rows per
+ * expert on average) with T > 64, the experts holding more than 64 rows take
+ * the cut tiled kernel and their slices are then added into slice 0 in
+ * ascending order, so *parts = 1 on return; the other experts stream uncut
+ * into slice 0.  Where only the streaming kernel runs, *parts = 1.  Slices at
+ * or past the count used are left as they were.  moe_combine_parts sums the
+ * slices; moe_forward runs this pair.  Errors as moe_swiglu_down, and
  * MOE_ERR_INVALID_ARG for max_parts < 1 or parts NULL.
  */
 moe_status_t moe_swiglu_down_parts(const moe_bf16_t* h, const int32_t* expert_offsets,
@@ -181,11 +185,13 @@ moe_status_t moe_combine_parts(const float* y, const int32_t* parts, int32_t max
  * any input.  Scratch is owned by the library, cached per device and grown on
  * demand (a growth is refused with MOE_ERR_NO_MEMORY while `stream` is being
  * captured into a graph; call once outside capture first).
- * At prefill sizes the down GEMM runs as moe_swiglu_down_parts with up to 4
- * parts (the count depends on the routed row counts and the GPU's compute
- * units) and the combine as moe_combine_parts, so the result can differ in
- * the last bits from the uncut staged calls moe_grouped_swiglu + moe_combine;
- * for the same inputs on the same GPU it is deterministic.
+ * At prefill sizes (up to 4 parts) and for the heavy experts of a streaming
+ * step with T > 64 (up to 8 parts) the down GEMM runs as
+ * moe_swiglu_down_parts and the combine as moe_combine_parts (the part count
+ * depends on the routed row counts and the GPU's compute units), so the
+ * result can differ in the last bits from the uncut staged calls
+ * moe_grouped_swiglu + moe_combine; for the same inputs on the same GPU it is
+ * deterministic.
  */
 moe_status_t moe_forward(const moe_bf16_t* x, const moe_bf16_t* router_w, const moe_bf16_t* w1,
                          const moe_bf16_t* w3, const moe_bf16_t* w2, int64_t T, int32_t d,

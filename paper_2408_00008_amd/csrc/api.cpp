@@ -22,6 +22,7 @@ hipError_t launch_stream_up(const UpArgs& a, int64_t rows_max, hipStream_t strea
 hipError_t launch_stream_down(const DownArgs& a, int64_t rows_max, hipStream_t stream);
 hipError_t launch_tiled_up(const UpArgs& a, hipStream_t stream);
 hipError_t launch_tiled_down(const DownArgs& a, hipStream_t stream);
+int tiled_down_grid(const DownArgs& a);
 bool tiled_supported(int d, int ffn);
 }  // namespace moe
 
@@ -147,17 +148,34 @@ size_t align256(size_t v) { return (v + 255) & ~size_t(255); }
 // device from the real tile count).  Only where the tiled kernel runs by
 // default and the tiles fill fewer than 16 rounds of 256 workgroups, where a
 // cut evens out the last round.
+// Largest power of two <= requested, <= 16 and leaving each part at least 8
+// reduction steps of 64.
 int parts_cap(int32_t ffn, int requested)
 {
     const int steps = ffn / 64;
-    const int cap = steps >= 32 ? 4 : steps >= 16 ? 2 : 1;
-    const int r = requested >= 4 ? 4 : requested >= 2 ? 2 : 1;
-    return r < cap ? r : cap;
+    int c = 1;
+    while (c * 2 <= requested && c * 2 <= 16 && steps / (c * 2) >= 8) c *= 2;
+    return c;
 }
 
-int down_split_max(int64_t A, int32_t d, int32_t ffn, int32_t E)
+// An expert with more rows than this takes its own launch in the streaming
+// regime (see run_up / run_down).
+constexpr int64_t kLightRows = 64;
+
+// Reduction parts moe_forward's down GEMM may use (the slices of y):
+//  * tiled regime (over 64 rows per expert on average): up to 4, where the
+//    tiles fill fewer than 16 rounds of 256 workgroups;
+//  * streaming regime with T > kLightRows, where an expert may be heavy: up to
+//    8 for the heavy experts' tiled launch (their few tiles spread over the
+//    whole GPU; the parts are folded back into slice 0 before the combine).
+//    Measured on MI355X, one expert of 194 rows and seven of 45: down +
+//    combine 253 us with the heavy expert streaming in 64-row passes, 318 /
+//    260 / 234 / 236 us with at most 2 / 4 / 8 / 16 parts.
+int down_split_max(int64_t T, int32_t d, int32_t ffn, int32_t E, int32_t k)
 {
-    if (A <= 64LL * E || !moe::tiled_supported(d, ffn)) return 1;
+    const int64_t A = T * k;
+    if (!moe::tiled_supported(d, ffn)) return 1;
+    if (A <= 64LL * E) return T > kLightRows ? parts_cap(ffn, 8) : 1;
     const int64_t items = (int64_t)(d / 256) * (A / 256 + E);
     if (items >= 16 * 256) return 1;
     return parts_cap(ffn, 4);
@@ -172,7 +190,7 @@ Layout layout(int64_t T, int32_t d, int32_t ffn, int32_t E, int32_t k)
 {
     const size_t A = static_cast<size_t>(T) * k;
     Layout L{};
-    L.nsplit = down_split_max(static_cast<int64_t>(A), d, ffn, E);
+    L.nsplit = down_split_max(T, d, ffn, E, k);
     size_t o = 0;
     L.ids = o;  o += align256(A * 4);
     L.w = o;    o += align256(A * 4);
@@ -307,8 +325,9 @@ moe_status_t no_overlap_v(const char* oname, Range o, const std::vector<std::pai
 // heavier ones take the tiled kernel (up, bf16) or the streaming kernel with
 // 128-row passes (down, and 8-bit weights).  Measured on MI355X with one
 // expert of 194 rows and seven of 45 (T = 256): up 426 -> 392 us, down
-// 261 -> 228 us.
-constexpr int64_t kLightRows = 64;
+// 261 -> 228 us.  Where the caller provides slices for reduction parts
+// (moe_forward, moe_swiglu_down_parts), the heavy down GEMM takes the tiled
+// kernel with its reduction cut into up to 16 parts, folded into slice 0.
 
 bool split_by_rows(int64_t rows_max, int64_t A, int E)
 {
@@ -337,29 +356,47 @@ hipError_t run_up(const moe::UpArgs& a, int64_t T, hipStream_t stream)
     return moe::launch_stream_up(a, rmax, stream);
 }
 
-// *sliced: whether y was written as the reduction-part slices of the tiled
-// kernel (their count at a.ksplit_out)
+// With a.ksplit_out set, y has room for a.ksplit_max slices [A,d] and on
+// return *a.ksplit_out (stream-ordered) holds how many of them the combine
+// must sum; *sliced tells whether that may exceed 1.
 hipError_t run_down(const moe::DownArgs& a, int64_t T, int32_t k, hipStream_t stream,
                     bool* sliced = nullptr)
 {
     if (sliced) *sliced = false;
+    const bool parts = a.ksplit_out != nullptr;
+    auto uncut = [&](hipError_t e) {
+        if (e != hipSuccess || !parts) return e;
+        return moe::launch_fill_i32(a.ksplit_out, 1, stream);
+    };
     const int64_t rmax = rows_bound(T, k);
     if (split_by_rows(rmax, a.A, a.E)) {
         moe::DownArgs light = a, heavy = a;
         light.mhi = kLightRows;
+        light.ksplit_out = nullptr;
         heavy.mlo = kLightRows + 1;
-        heavy.groups = 8;
         hipError_t e = moe::launch_stream_down(light, kLightRows, stream);
         if (e != hipSuccess) return e;
-        return moe::launch_stream_down(heavy, rmax, stream);
+        if (parts && a.ksplit_max > 1 && !a.q2 && moe::tiled_supported(a.d, a.ffn)) {
+            // the fold recomputes the part count and sets *ksplit_out = 1
+            heavy.ksplit_out = nullptr;
+            e = moe::launch_tiled_down(heavy, stream);
+            if (e != hipSuccess) return e;
+            return moe::launch_fold_parts(a.y, a.A, a.d, a.offsets, a.E, heavy.mlo,
+                                          a.topk_w ? a.perm : nullptr, a.ffn / 64,
+                                          moe::tiled_down_grid(heavy) / 8, a.ksplit_max,
+                                          a.ksplit_out, stream);
+        }
+        heavy.groups = 8;
+        heavy.ksplit_out = nullptr;
+        return uncut(moe::launch_stream_down(heavy, rmax, stream));
     }
-    if (a.q2) return moe::launch_stream_down(a, rmax, stream);
+    if (a.q2) return uncut(moe::launch_stream_down(a, rmax, stream));
     const int v = moe::resolve_variant(g_variant.load(), a.A, a.E);
     if (v == moe::VARIANT_TILED && moe::tiled_supported(a.d, a.ffn)) {
-        if (sliced) *sliced = a.ksplit_out != nullptr;
+        if (sliced) *sliced = parts;
         return moe::launch_tiled_down(a, stream);
     }
-    return moe::launch_stream_down(a, rmax, stream);
+    return uncut(moe::launch_stream_down(a, rmax, stream));
 }
 
 }  // namespace
@@ -448,13 +485,8 @@ moe_status_t swiglu_down_impl(const moe_bf16_t* h, const int32_t* expert_offsets
     a.q2 = w.q2, a.s2 = w.s2;
     a.ksplit_max = parts ? parts_cap(ffn, max_parts) : 1;
     a.ksplit_out = parts;
-    bool sliced = false;
-    hipError_t e = run_down(a, T, k, stream, &sliced);
+    hipError_t e = run_down(a, T, k, stream);
     if (e != hipSuccess) return hip_fail(e, "expert down kernel launch");
-    if (parts && !sliced) {
-        e = moe::launch_fill_i32(parts, 1, stream);
-        if (e != hipSuccess) return hip_fail(e, "fill kernel launch");
-    }
     return ok();
 }
 
@@ -525,7 +557,8 @@ moe_status_t forward_impl(const moe_bf16_t* x, const moe_bf16_t* router_w,
     moe::DownArgs da{h, offs, w.w2, gw, perm, y, A, d, ffn, E};
     da.q2 = w.q2, da.s2 = w.s2;
     da.ksplit_max = L.nsplit;
-    da.ksplit_out = reinterpret_cast<int*>(b + L.ns);
+    // the part count is only needed (and only written) where y has slices
+    da.ksplit_out = L.nsplit > 1 ? reinterpret_cast<int*>(b + L.ns) : nullptr;
     bool sliced = false;
     e = run_down(da, T, k, stream, &sliced);
     if (e != hipSuccess) return hip_fail(e, "expert down kernel launch");

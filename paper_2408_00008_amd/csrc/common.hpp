@@ -87,4 +87,33 @@ __device__ __forceinline__ T wave_shfl_xor(T v, int mask)
     return __shfl_xor(v, mask, 64);
 }
 
+// Parts of the tiled down GEMM's reduction (used by that kernel and by the
+// kernel that folds a heavy expert's parts back together).  The persistent
+// workgroups of an XCD take its items in rounds, so the layer costs
+// ceil(share / workgroups) rounds of one item; with a few hundred 256 x 256 tiles over 256 CUs the
+// last round is mostly idle (560 tiles: 3 rounds for 2.2 rounds of work).
+// Cutting every tile's reduction into S parts gives S times as many items of
+// 1/S of the steps, which evens out the rounds, at the price of a start-up
+// and an output store per item and S - 1 more f32 slices for the combine to
+// read.  Cost in thousandths of a reduction step (one step = 64 elements of
+// the reduction, ~1.5 us on the 4096 x 14336 shapes): per item 1000 nk / S +
+// 6000, per extra slice A * N / 1800 (its read at ~5 TB/s).  Integer
+// arithmetic, so every kernel that evaluates it gets the same answer.
+__device__ __forceinline__ int down_parts(int total, int per_xcd, int nk, int64_t A, int N, int smax)
+{
+    int best = 1;
+    int64_t best_cost = INT64_MAX;
+    const int64_t slice_cost = A * N / 1800;
+    for (int s = 1; s <= smax && s <= nk; s *= 2) {
+        const int64_t share = ((int64_t)total * s + 7) / 8;
+        const int64_t rounds = (share + per_xcd - 1) / per_xcd;
+        const int64_t cost = rounds * (1000LL * nk / s + 6000) + (s - 1) * slice_cost;
+        if (cost < best_cost) {
+            best_cost = cost;
+            best = s;
+        }
+    }
+    return best;
+}
+
 }  // namespace moe

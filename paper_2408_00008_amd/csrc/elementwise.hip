@@ -132,6 +132,71 @@ hipError_t launch_combine(const float* y, const float* residual, int64_t T, int 
     return hipGetLastError();
 }
 
+// After the tiled down GEMM over the experts with at least mlo rows ran with
+// its reduction cut: slice 0 of each of their rows += slices 1 .. n-1 in
+// ascending order (the order the combine uses).  n is recomputed here with the
+// cost model that kernel used (same tile count, grid, steps, sizes and cap),
+// so the count needs no device handoff; *parts_out (if not null) is set to 1
+// for the combine.  Permuted row r lives at y row perm[r] (perm null: r).
+// Blocks take (row, 1024-column chunk) units.
+__global__ __launch_bounds__(256) void fold_parts_kernel(float* __restrict__ y, int64_t A, int d,
+                                                         const int32_t* __restrict__ offsets,
+                                                         int E, int mlo,
+                                                         const int32_t* __restrict__ perm,
+                                                         int nk, int per_xcd, int smax,
+                                                         int* parts_out)
+{
+    if (parts_out && blockIdx.x == 0 && threadIdx.x == 0) *parts_out = 1;
+    int tiles = 0;
+    for (int e = 0; e < E; ++e) {
+        const int m = offsets[e + 1] - offsets[e];
+        if (m >= mlo) tiles += (m + 255) >> 8;
+    }
+    const int ns = down_parts((d >> 8) * tiles, per_xcd, nk, A, d, smax);
+    if (ns <= 1) return;
+    const int64_t slice = A * d;
+    const int cpr = d >> 2;                  // float4 per row
+    const int chunks = (cpr + 255) >> 8;     // 256 float4 per unit
+    for (int64_t u = blockIdx.x; u < A * chunks; u += gridDim.x) {
+        const int64_t r = u / chunks;
+        const int c = static_cast<int>(u - r * chunks) * 256 + threadIdx.x;
+        // the expert holding row r: offsets are non-decreasing with offsets[E] = A
+        int e = 0;
+        while (e + 1 < E && offsets[e + 1] <= r) ++e;
+        if (offsets[e + 1] - offsets[e] < mlo || c >= cpr) continue;
+        float4* y0 = reinterpret_cast<float4*>(y + (perm ? (int64_t)perm[r] : r) * d) + c;
+        float4 v = *y0;
+        // loads four slices at a time, adds them in order
+        for (int q = 1; q < ns; q += 4) {
+            float4 t[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                if (q + i < ns) t[i] = *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(y0) + (q + i) * slice);
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                if (q + i < ns) {
+                    v.x += t[i].x;
+                    v.y += t[i].y;
+                    v.z += t[i].z;
+                    v.w += t[i].w;
+                }
+        }
+        *y0 = v;
+    }
+}
+
+hipError_t launch_fold_parts(float* y, int64_t A, int d, const int32_t* offsets, int E, int mlo,
+                             const int32_t* perm, int nk, int per_xcd, int smax, int* parts_out,
+                             hipStream_t stream)
+{
+    if (A == 0) return hipSuccess;
+    const int64_t units = A * (((d >> 2) + 255) >> 8);
+    const unsigned grid = static_cast<unsigned>(units < 8192 ? units : 8192);
+    fold_parts_kernel<<<grid, 256, 0, stream>>>(y, A, d, offsets, E, mlo, perm, nk, per_xcd, smax,
+                                                parts_out);
+    return hipGetLastError();
+}
+
 __global__ void fill_i32_kernel(int32_t* p, int32_t v) { *p = v; }
 
 hipError_t launch_fill_i32(int32_t* p, int32_t v, hipStream_t stream)

@@ -112,32 +112,6 @@ __device__ __forceinline__ void wait_vmem()
 // s_waitcnt lgkmcnt(0) with vmcnt/expcnt at max
 __device__ __forceinline__ void wait_lds() { __builtin_amdgcn_s_waitcnt(0xC07F); }
 
-// Parts of the down GEMM's reduction.  The persistent workgroups of an XCD
-// take its items in rounds, so the layer costs ceil(share / workgroups)
-// rounds of one item; with a few hundred 256 x 256 tiles over 256 CUs the
-// last round is mostly idle (560 tiles: 3 rounds for 2.2 rounds of work).
-// Cutting every tile's reduction into S parts gives S times as many items of
-// 1/S of the steps, which evens out the rounds, at the price of a start-up
-// and an output store per item and S - 1 more f32 slices for the combine to
-// read.  Cost in reduction steps (one step = 64 elements of the reduction,
-// ~1.5 us on the 4096 x 14336 shapes): per item nk / S + 6, per extra slice
-// A * N / 1.8e6 (its read at ~5 TB/s).
-__device__ __forceinline__ int down_parts(int total, int per_xcd, int nk, int64_t A, int N, int smax)
-{
-    int best = 1;
-    float best_cost = 3.0e38f;
-    for (int s = 1; s <= smax && s <= nk; s *= 2) {
-        const int share = (total * s + 7) / 8;
-        const int rounds = (share + per_xcd - 1) / per_xcd;
-        const float cost = rounds * ((float)nk / s + 6.0f) + (s - 1) * ((float)A * N / 1.8e6f);
-        if (cost < best_cost) {
-            best_cost = cost;
-            best = s;
-        }
-    }
-    return best;
-}
-
 template <bool UP>
 __global__ __launch_bounds__(256) void q_kernel(TiledParams p)
 {
@@ -414,6 +388,19 @@ __global__ __launch_bounds__(256) void q_kernel(TiledParams p)
     }
 }
 
+// persistent grid: one workgroup per CU, fewer for fewer items (a bound:
+// the real tile counts are on the device), a multiple of the 8 XCDs
+template <bool UP>
+int q_grid(int N, int E, int64_t A, int ksplit_max)
+{
+    using C = QCfg<UP>;
+    const int64_t nbn = N / C::NOUT;
+    const int64_t items = nbn * (A / C::BM + E) * (UP ? 1 : ksplit_max);
+    int64_t grid = cu_count();
+    if (grid > items) grid = items;
+    return static_cast<int>(((grid + 7) / 8) * 8);
+}
+
 template <bool UP>
 hipError_t run_q(const TiledParams& p, int64_t A, hipStream_t stream)
 {
@@ -425,11 +412,7 @@ hipError_t run_q(const TiledParams& p, int64_t A, hipStream_t stream)
         if (e != hipSuccess) return e;
         attr_set = true;
     }
-    const int64_t nbn = p.N / C::NOUT;
-    const int64_t items = nbn * (A / C::BM + p.E) * (UP ? 1 : p.ksplit_max);
-    int64_t grid = cu_count();
-    if (grid > items) grid = items;
-    grid = ((grid + 7) / 8) * 8;
+    const int grid = q_grid<UP>(p.N, p.E, A, p.ksplit_max);
     q_kernel<UP><<<static_cast<unsigned>(grid), C::THREADS, C::LDS_BYTES, stream>>>(p);
     return hipGetLastError();
 }
@@ -474,6 +457,11 @@ hipError_t launch_tiled_up(const UpArgs& a, hipStream_t stream)
     p.ksplit_max = 1;
     p.A = a.A;
     return run_q<true>(p, a.A, stream);
+}
+
+int tiled_down_grid(const DownArgs& a)
+{
+    return q_grid<false>(a.d, a.E, a.A, a.ksplit_max > 1 ? a.ksplit_max : 1);
 }
 
 hipError_t launch_tiled_down(const DownArgs& a, hipStream_t stream)

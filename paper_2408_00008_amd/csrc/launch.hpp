@@ -30,6 +30,14 @@ hipError_t launch_combine(const float* y, const float* residual, int64_t T, int 
                           bf16_t* out, float* out_f32, hipStream_t stream,
                           const int* nslices = nullptr, int max_slices = 1);
 
+// Folds the reduction-part slices of the experts with at least mlo rows into
+// slice 0 (y [smax, A, d] f32) after launch_tiled_down(mlo, ksplit_max =
+// smax) ran with grid tiled_down_grid and nk = ffn / 64 reduction steps; the
+// part count is recomputed on the device.  *parts_out (may be null) = 1.
+hipError_t launch_fold_parts(float* y, int64_t A, int d, const int32_t* offsets, int E, int mlo,
+                             const int32_t* perm, int nk, int per_xcd, int smax, int* parts_out,
+                             hipStream_t stream);
+
 // *p = v, stream-ordered (a kernel, so it may be captured into a graph)
 hipError_t launch_fill_i32(int32_t* p, int32_t v, hipStream_t stream);
 

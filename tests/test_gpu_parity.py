@@ -274,6 +274,46 @@ def test_forward_down_split(shape, parts):
     assert torch.equal(of, of2)
 
 
+@pytest.mark.parametrize("shape", [
+    (256, 256, 2048, 8, 2),   # heavy expert: 4 parts of 8 steps
+    (256, 256, 8192, 8, 2),   # heavy expert: up to 8 parts of 16 steps
+])
+def test_forward_split_heavy_cut(shape):
+    """Streaming regime with a heavy expert: its down GEMM takes the tiled
+    kernel with the reduction cut (slices folded into slice 0 before the
+    combine).  Parity with the oracle; the forward equals the staged pair
+    moe_swiglu_down_parts + moe_combine_parts bitwise, whose count reads 1
+    after the fold; and the uncut staged calls agree to f32 rounding."""
+    say(f"[forward] heavy expert, cut down GEMM {shape}")
+    bias = [2.0] + [0.0] * (shape[3] - 1)
+    c = small_case(*shape, seed=31, bias=bias)
+    assert B.moe_gemm_variant_for(c.T, c.d, c.ffn, c.E, c.k) == 3
+    T, d, k = c.T, c.d, c.k
+    ids, gw, offs, perm, _ = gpu_route(c)
+    rows = np.diff(offs.cpu().numpy())
+    assert rows.max() > 64, rows
+    _forward_check(c, variant=0)
+    of = gpu_forward(c, out_f32=True)[1]
+    h = torch.empty(T * k, c.ffn, dtype=torch.bfloat16, device=DEV)
+    B.moe_swiglu_up(c.x, offs, c.w1, c.w3, T, k, h, perm=perm)
+    # 8 slices: the forward's cap in this regime
+    yp = torch.empty(8, T * k, d, dtype=torch.float32, device=DEV)
+    np_dev = torch.zeros(1, dtype=torch.int32, device=DEV)
+    B.moe_swiglu_down_parts(h, offs, c.w2, T, k, yp, np_dev, topk_w=gw, perm=perm)
+    st = torch.empty(T, d, dtype=torch.float32, device=DEV)
+    B.moe_combine_parts(yp, np_dev, T, d, k, out_f32=st)
+    y = torch.empty(T * k, d, dtype=torch.float32, device=DEV)
+    B.moe_swiglu_down(h, offs, c.w2, T, k, y, topk_w=gw, perm=perm)
+    unc = torch.empty(T, d, dtype=torch.float32, device=DEV)
+    B.moe_combine(y, T, d, k, out_f32=unc)
+    torch.cuda.synchronize()
+    assert int(np_dev.item()) == 1
+    assert torch.equal(st, of)
+    err = rowwise_rel(st.double().cpu().numpy(), unc.double().cpu().numpy())
+    say(f"  cut vs uncut: rowwise rel {err:.3e}")
+    assert err < 1e-5
+
+
 def test_forward_t0():
     c = small_case(3, 64, 64, 4, 2)
     out = torch.zeros(0, 64, dtype=torch.bfloat16, device=DEV)
