@@ -128,9 +128,7 @@ def main():
     # as separate slices: up to 4 where the tiled kernels run, up to 8 for
     # the heavy experts of a split streaming step
     variant = {1: "stream", 2: "tiled", 3: "split"}[B.moe_gemm_variant_for(T, d, ffn, E, k)]
-    if w.fp8 and variant == "tiled":
-        variant = "stream"  # 8-bit weights always stream
-    cut = variant in ("tiled", "split") and not w.fp8
+    cut = variant in ("tiled", "split")
     y = torch.empty({"tiled": 4, "split": 8}[variant] if cut else 1, A, d, dtype=torch.float32,
                     device=dev)
     parts = torch.ones(1, dtype=torch.int32, device=dev)
@@ -147,7 +145,10 @@ def main():
             B.moe_swiglu_up(x, offs, w1, w3, T, k, h, perm=perm, stream=stream)
         if ev1 is not None:
             ev1.record(stream)
-        if w.fp8:
+        if w.fp8 and cut:
+            B.moe_swiglu_down_parts_fp8(h, offs, q[4], q[5], T, k, y, parts, topk_w=gw, perm=perm,
+                                        stream=stream)
+        elif w.fp8:
             B.moe_swiglu_down_fp8(h, offs, q[4], q[5], T, k, y[0], topk_w=gw, perm=perm,
                                   stream=stream)
         elif cut:

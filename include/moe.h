@@ -227,7 +227,9 @@ moe_status_t moe_forward_ex(const moe_bf16_t* x, const moe_bf16_t* router_w,
  * rows, h, y, out, routing) is as in the bf16 calls of the same name, with
  * the same limits and alignment rules (byte arrays and scales 16-byte
  * aligned).  A NaN byte, or a non-finite scale, makes the rows it reaches
- * NaN.  These calls always use the weight-streaming kernels.
+ * NaN.  Kernel families as for bf16 weights (moe_set_gemm_variant): the
+ * tiled kernels stage the E4M3 bytes in LDS and widen them to bf16 operands
+ * there.
  */
 moe_status_t moe_swiglu_up_fp8(const moe_bf16_t* x, const int32_t* perm,
                                const int32_t* expert_offsets, const uint8_t* w1q,
@@ -239,6 +241,14 @@ moe_status_t moe_swiglu_down_fp8(const moe_bf16_t* h, const int32_t* expert_offs
                                  const uint8_t* w2q, const float* w2s, const float* topk_w,
                                  const int32_t* perm, int64_t T, int32_t d, int32_t ffn, int32_t E,
                                  int32_t k, float* y, hipStream_t stream);
+
+/* moe_swiglu_down_parts with the 8-bit weights above (same slices, count and
+ * errors). */
+moe_status_t moe_swiglu_down_parts_fp8(const moe_bf16_t* h, const int32_t* expert_offsets,
+                                       const uint8_t* w2q, const float* w2s, const float* topk_w,
+                                       const int32_t* perm, int64_t T, int32_t d, int32_t ffn,
+                                       int32_t E, int32_t k, int32_t max_parts, float* y,
+                                       int32_t* parts, hipStream_t stream);
 
 /* moe_forward_ex with the 8-bit expert weights above (the router stays bf16). */
 moe_status_t moe_forward_fp8_ex(const moe_bf16_t* x, const moe_bf16_t* router_w,
@@ -330,15 +340,15 @@ size_t moe_workspace_size(int64_t T, int32_t d, int32_t ffn, int32_t E, int32_t 
  *   shapes).  Automatic: streaming while T*k/E <= 64, tiled above; in the
  *   streaming regime with T > 64 (so an expert may hold more than 64 rows)
  *   each expert GEMM is two launches that split the experts on the device by
- *   their row count (<= 64: streaming; more: tiled for the bf16 up GEMM,
- *   streaming with 128-row passes otherwise).  Process-wide; returns the
- *   previous value, or -1 for an unknown value (nothing changed).  For
- *   testing and measurement.  The 8-bit weight calls never take the tiled
- *   kernel.
+ *   their row count (<= 64: streaming; more: tiled for the up GEMM, and for
+ *   the down GEMM where the caller provides reduction-part slices, streaming
+ *   with 128-row passes otherwise).  Process-wide; returns the previous
+ *   value, or -1 for an unknown value (nothing changed).  For testing and
+ *   measurement.  The same choice applies to the 8-bit weight calls.
  */
 int moe_set_gemm_variant(int variant);
 
-/* The kernel family the bf16 expert GEMMs use for these sizes under the
+/* The kernel family the expert GEMMs use for these sizes under the
  * current moe_set_gemm_variant setting: 1 = weight-streaming, 2 = tiled,
  * 3 = split by rows per expert (see moe_set_gemm_variant); 0 for invalid
  * sizes.  Host-only, enqueues nothing. */

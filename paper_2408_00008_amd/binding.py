@@ -24,7 +24,7 @@ VARIANT_AUTO, VARIANT_STREAM, VARIANT_TILED = 0, 1, 2
 EXPORTS = (
     "moe_route", "moe_permute", "moe_swiglu_up", "moe_swiglu_down", "moe_swiglu_down_parts",
     "moe_grouped_swiglu", "moe_combine", "moe_combine_parts", "moe_forward", "moe_forward_ex", "moe_rmsnorm", "moe_workspace_size",
-    "moe_swiglu_up_fp8", "moe_swiglu_down_fp8", "moe_forward_fp8_ex",
+    "moe_swiglu_up_fp8", "moe_swiglu_down_fp8", "moe_swiglu_down_parts_fp8", "moe_forward_fp8_ex",
     "moe_linear", "moe_rope_kv_append", "moe_attention_decode",
     "moe_set_gemm_variant", "moe_gemm_variant_for", "moe_status_string", "moe_last_error", "moe_version",
 )
@@ -67,6 +67,7 @@ def lib() -> ctypes.CDLL:
         "moe_rmsnorm": [p, p, i64, i32, f32, p, p],
         "moe_swiglu_up_fp8": [p, p, p, p, p, p, p, i64, i32, i32, i32, i32, p, p],
         "moe_swiglu_down_fp8": [p, p, p, p, p, p, i64, i32, i32, i32, i32, p, p],
+        "moe_swiglu_down_parts_fp8": [p, p, p, p, p, p, i64, i32, i32, i32, i32, i32, p, p, p],
         "moe_forward_fp8_ex": [p, p, p, p, p, p, p, p, p, i64, i32, i32, i32, i32, p, p, p, p,
                                sz, p],
         "moe_linear": [p, p, i64, i32, i32, p, p],
@@ -165,6 +166,17 @@ def moe_swiglu_down_parts(h, expert_offsets, w2, T, k, y, parts, topk_w=None, pe
         _ptr(h, bf16, "h"), _ptr(expert_offsets, i32, "offsets"), _ptr(w2, bf16, "w2"),
         _ptr(topk_w, f32, "topk_w"), _ptr(perm, i32, "perm"), T, d, ffn, E, k, max_parts,
         _ptr(y, f32, "y"), _ptr(parts, i32, "parts"), _stream(stream)), "moe_swiglu_down_parts")
+
+
+def moe_swiglu_down_parts_fp8(h, expert_offsets, w2q, w2s, T, k, y, parts, topk_w=None,
+                              perm=None, stream=None):
+    """8-bit weights: y [max_parts, T*k, d] f32 slices; parts one device int32."""
+    E, d, ffn = w2q.shape
+    _check(lib().moe_swiglu_down_parts_fp8(
+        _ptr(h, bf16, "h"), _ptr(expert_offsets, i32, "offsets"), _ptr(w2q, u8, "w2q"),
+        _ptr(w2s, f32, "w2s"), _ptr(topk_w, f32, "topk_w"), _ptr(perm, i32, "perm"), T, d, ffn,
+        E, k, y.shape[0], _ptr(y, f32, "y"), _ptr(parts, i32, "parts"), _stream(stream)),
+        "moe_swiglu_down_parts_fp8")
 
 
 def moe_grouped_swiglu(x_perm, expert_offsets, w1, w3, w2, T, k, h_ws, y, topk_w=None,

@@ -338,7 +338,7 @@ bool split_by_rows(int64_t rows_max, int64_t A, int E)
 hipError_t run_up(const moe::UpArgs& a, int64_t T, hipStream_t stream)
 {
     const int64_t rmax = rows_bound(T, a.kslots);
-    const bool tiled_ok = !a.q1 && moe::tiled_supported(a.d, a.ffn);
+    const bool tiled_ok = moe::tiled_supported(a.d, a.ffn);
     if (split_by_rows(rmax, a.A, a.E)) {
         moe::UpArgs light = a, heavy = a;
         light.mhi = kLightRows;
@@ -349,8 +349,6 @@ hipError_t run_up(const moe::UpArgs& a, int64_t T, hipStream_t stream)
         heavy.groups = 8;
         return moe::launch_stream_up(heavy, rmax, stream);
     }
-    // 8-bit weights run the weight-streaming kernels at every size
-    if (a.q1) return moe::launch_stream_up(a, rmax, stream);
     const int v = moe::resolve_variant(g_variant.load(), a.A, a.E);
     if (v == moe::VARIANT_TILED && tiled_ok) return moe::launch_tiled_up(a, stream);
     return moe::launch_stream_up(a, rmax, stream);
@@ -376,7 +374,7 @@ hipError_t run_down(const moe::DownArgs& a, int64_t T, int32_t k, hipStream_t st
         heavy.mlo = kLightRows + 1;
         hipError_t e = moe::launch_stream_down(light, kLightRows, stream);
         if (e != hipSuccess) return e;
-        if (parts && a.ksplit_max > 1 && !a.q2 && moe::tiled_supported(a.d, a.ffn)) {
+        if (parts && a.ksplit_max > 1 && moe::tiled_supported(a.d, a.ffn)) {
             // the fold recomputes the part count and sets *ksplit_out = 1
             heavy.ksplit_out = nullptr;
             e = moe::launch_tiled_down(heavy, stream);
@@ -390,7 +388,6 @@ hipError_t run_down(const moe::DownArgs& a, int64_t T, int32_t k, hipStream_t st
         heavy.ksplit_out = nullptr;
         return uncut(moe::launch_stream_down(heavy, rmax, stream));
     }
-    if (a.q2) return uncut(moe::launch_stream_down(a, rmax, stream));
     const int v = moe::resolve_variant(g_variant.load(), a.A, a.E);
     if (v == moe::VARIANT_TILED && moe::tiled_supported(a.d, a.ffn)) {
         if (sliced) *sliced = parts;
@@ -744,6 +741,21 @@ moe_status_t moe_swiglu_down_fp8(const moe_bf16_t* h, const int32_t* expert_offs
     return swiglu_down_impl(h, expert_offsets,
                             fp8_weights(nullptr, nullptr, nullptr, nullptr, w2q, w2s), topk_w,
                             perm, T, d, ffn, E, k, y, stream);
+}
+
+moe_status_t moe_swiglu_down_parts_fp8(const moe_bf16_t* h, const int32_t* expert_offsets,
+                                       const uint8_t* w2q, const float* w2s, const float* topk_w,
+                                       const int32_t* perm, int64_t T, int32_t d, int32_t ffn,
+                                       int32_t E, int32_t k, int32_t max_parts, float* y,
+                                       int32_t* parts, hipStream_t stream)
+{
+    if (max_parts < 1) return fail(MOE_ERR_INVALID_ARG, "max_parts=%d must be >= 1", max_parts);
+    if (!parts) return fail(MOE_ERR_INVALID_ARG, "parts is NULL");
+    if (reinterpret_cast<uintptr_t>(parts) & 3u)
+        return fail(MOE_ERR_INVALID_ARG, "parts is not 4-byte aligned");
+    return swiglu_down_impl(h, expert_offsets,
+                            fp8_weights(nullptr, nullptr, nullptr, nullptr, w2q, w2s), topk_w,
+                            perm, T, d, ffn, E, k, y, stream, max_parts, parts);
 }
 
 moe_status_t moe_grouped_swiglu(const moe_bf16_t* x_perm, const int32_t* expert_offsets,

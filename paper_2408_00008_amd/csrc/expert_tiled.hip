@@ -37,6 +37,12 @@ struct TiledParams {
     const int32_t* offsets;  // [E+1]
     const bf16_t* wa;        // UP: w1, DOWN: w2  [E, N, K]
     const bf16_t* wb;        // UP: w3            [E, N, K]
+    // 8-bit weights (then wa/wb are unused): E4M3 bytes [E, N, K] and per-row
+    // f32 scales [E, N], applied to the accumulators in the epilogue
+    const uint8_t* qa;
+    const uint8_t* qb;
+    const float* sa;
+    const float* sb;
     int N, K, E;             // N = weight rows per expert (UP: ffn, DOWN: d)
     bf16_t* h_out;           // UP   [A, N]
     float* y_out;            // DOWN [A, N]
@@ -84,19 +90,22 @@ int cu_count();
 //     consecutive rows, one chunk) hits 16 distinct bank groups;
 //   * loads past the last step re-load the last step into the free slot, so
 //     the wait counts are the same every step.
-template <bool UP>
+template <bool UP, bool F8>
 struct QCfg {
     static constexpr int THREADS = 256;
     static constexpr int BN = 256;                 // weight rows staged (UP: 128 w1 + 128 w3)
     static constexpr int BM = 256;                 // token rows
     static constexpr int NOUT = UP ? BN / 2 : BN;  // output columns per tile
     static constexpr int BK = 64;
-    static constexpr int ROWB = BK * 2;            // bytes per LDS row
-    static constexpr int SLOT = 256 * ROWB;        // 32 KB, one operand of one step
-    static constexpr int B_OFF = 3 * SLOT;
-    static constexpr int LDS_BYTES = 5 * SLOT;
+    static constexpr int ROWB = BK * 2;            // bytes per LDS token row
+    static constexpr int AROWB = F8 ? BK : BK * 2; // bytes per LDS weight row
+    static constexpr int SLOT = 256 * ROWB;        // 32 KB, the token tile of one step
+    static constexpr int ASLOT = 256 * AROWB;      // the weight tile of one step (32 or 16 KB)
+    static constexpr int B_OFF = 3 * ASLOT;
+    static constexpr int LDS_BYTES = 3 * ASLOT + 2 * SLOT;
     static constexpr int NT = 4, MT = 4;           // 32x32 tiles per wave: 128 weight rows x 128 tokens
-    static constexpr int LOADS = 8;                // 8-row loads per wave per operand per step
+    static constexpr int LOADS = 8;                // 1 KB token loads per wave per step
+    static constexpr int ALOADS = F8 ? 4 : 8;      // 1 KB weight loads per wave per step
 };
 
 __device__ __forceinline__ int q_swz(int r) { return (r >> 1) & 7; }
@@ -112,11 +121,11 @@ __device__ __forceinline__ void wait_vmem()
 // s_waitcnt lgkmcnt(0) with vmcnt/expcnt at max
 __device__ __forceinline__ void wait_lds() { __builtin_amdgcn_s_waitcnt(0xC07F); }
 
-template <bool UP>
+template <bool UP, bool F8>
 __global__ __launch_bounds__(256) void q_kernel(TiledParams p)
 {
-    using C = QCfg<UP>;
-    constexpr int NT = C::NT, MT = C::MT, L = C::LOADS;
+    using C = QCfg<UP, F8>;
+    constexpr int NT = C::NT, MT = C::MT, L = C::LOADS, LA = C::ALOADS;
     extern __shared__ __attribute__((aligned(16))) unsigned char ring[];
 
     const int tid = threadIdx.x, lane = tid & 63;
@@ -148,20 +157,35 @@ __global__ __launch_bounds__(256) void q_kernel(TiledParams p)
     const int beg = (int)((int64_t)total * xcd / 8);
     const int end = (int)((int64_t)total * (xcd + 1) / 8);
 
-    // a load covers 8 rows starting at a multiple of 8: lane l takes row l / 8
-    // and the global chunk stored at slot l % 8 (odd loads start at 8 mod 16)
+    // a token load covers 8 rows starting at a multiple of 8: lane l takes row
+    // l / 8 and the global chunk stored at slot l % 8 (odd loads start at 8
+    // mod 16); bf16 weight loads the same.  An 8-bit weight load covers 16
+    // rows of 64 bytes: lane l takes row l / 4 and the global chunk stored at
+    // slot l % 4 (chunk c of row r lives at slot c ^ ((r >> 2) & 3)).
     const int lrow = lane >> 3;
     const int lchunk[2] = {(lane & 7) ^ ((lrow >> 1) & 7), (lane & 7) ^ (((8 + lrow) >> 1) & 7)};
-    // fragment reads: row (tile base + lane % 32), chunk 2 ks + lane / 32; the
-    // tile bases are multiples of 32, so the swizzle depends on the lane only
+    const int lchunk8 = (lane & 3) ^ ((lane >> 4) & 3);
+    // Fragment reads: row (tile base + lane % 32); the tile bases are
+    // multiples of 32, so the swizzles depend on the lane only.  bf16: k-step
+    // ks of both operands is chunk 2 ks + lane / 32 of the row.  8-bit weights
+    // order a step's reduction differently, identically for both operands:
+    // k-step ks, lane half h = lane / 32 holds elements 32 h + 8 ks .. + 7,
+    // so one 16-byte read of a weight row (chunk 2 h + p) serves k-steps 2p
+    // and 2p + 1, and the token row's k-step ks is its chunk 4 h + ks.
     int xk[4];
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks)
-        xk[ks] = (lane & 31) * C::ROWB + (((2 * ks + (lane >> 5)) ^ (((lane & 31) >> 1) & 7)) << 4);
+    for (int ks = 0; ks < 4; ++ks) {
+        const int ch = F8 ? 4 * (lane >> 5) + ks : 2 * ks + (lane >> 5);
+        xk[ks] = (lane & 31) * C::ROWB + ((ch ^ (((lane & 31) >> 1) & 7)) << 4);
+    }
+    int xa[2];
+#pragma unroll
+    for (int q = 0; q < 2; ++q)
+        xa[q] = (lane & 31) * C::AROWB + (((2 * (lane >> 5) + q) ^ (((lane & 31) >> 2) & 3)) << 4);
     // byte offset of this wave's nt-th 32-row weight tile in an A slot (UP:
     // nt < 2 are w1 rows, nt + 2 the same rows of w3), and of its token tiles
-    const int a_wave = (UP ? wr * 64 : wr * 128) * C::ROWB;
-    auto atile = [](int nt) { return (UP ? (nt >> 1) * (C::BN / 2) + (nt & 1) * 32 : nt * 32) * C::ROWB; };
+    const int a_wave = (UP ? wr * 64 : wr * 128) * C::AROWB;
+    auto atile = [](int nt) { return (UP ? (nt >> 1) * (C::BN / 2) + (nt & 1) * 32 : nt * 32) * C::AROWB; };
 
     for (int w = beg + local; w < end; w += per_xcd) {
         // the expert of item w: the last one (with tiles) whose first item is <= w
@@ -183,18 +207,17 @@ __global__ __launch_bounds__(256) void q_kernel(TiledParams p)
 
         // wave w loads A rows [64w, 64w + 64) and B rows [64w, 64w + 64); the
         // 64 A rows are 64 consecutive rows of w1, w3 or w2
-        const bf16_t* abase;
-        {
-            const bf16_t* base = p.wa;
-            int wrow = nb * C::NOUT + 64 * wave;
-            if (UP && 64 * wave >= C::BN / 2) {
-                base = p.wb;
-                wrow -= C::BN / 2;
-            }
-            abase = base + ((int64_t)e * p.N + wrow) * p.K + k0 * C::BK;
+        const bool a_second = UP && 64 * wave >= C::BN / 2;
+        const int64_t wrow = (int64_t)e * p.N + nb * C::NOUT + 64 * wave - (a_second ? C::BN / 2 : 0);
+        const unsigned char* aptr[2];
+        if constexpr (F8) {
+            const uint8_t* base = (a_second ? p.qb : p.qa) + wrow * p.K + k0 * C::BK;
+            aptr[0] = aptr[1] = base + (int64_t)(lane >> 2) * p.K + lchunk8 * 16;
+        } else {
+            const bf16_t* base = (a_second ? p.wb : p.wa) + wrow * p.K + k0 * C::BK;
+            aptr[0] = reinterpret_cast<const unsigned char*>(base + (int64_t)lrow * p.K + lchunk[0] * 8);
+            aptr[1] = reinterpret_cast<const unsigned char*>(base + (int64_t)lrow * p.K + lchunk[1] * 8);
         }
-        const bf16_t* aptr[2] = {abase + (int64_t)lrow * p.K + lchunk[0] * 8,
-                                 abase + (int64_t)lrow * p.K + lchunk[1] * 8};
         const bf16_t* bptr[L];
 #pragma unroll
         for (int i = 0; i < L; ++i) {
@@ -203,13 +226,15 @@ __global__ __launch_bounds__(256) void q_kernel(TiledParams p)
             const int64_t src = (UP && p.gather) ? p.gather[rowm] / p.kslots : rowm;
             bptr[i] = p.act + src * p.K + k0 * C::BK + lchunk[i & 1] * 8;
         }
-        const int64_t astep = (int64_t)8 * p.K;  // elements between a wave's consecutive A loads
+        // bytes between a wave's consecutive weight loads (8 or 16 rows)
+        const int64_t astep = F8 ? (int64_t)16 * p.K : (int64_t)16 * p.K;
         auto load_a = [&](int s, int i) {
-            unsigned char* st = ring + (s % 3) * C::SLOT;
-            int64_t ko = (int64_t)(s < kn ? s : kn - 1) * C::BK + i * astep;
+            unsigned char* st = ring + (s % 3) * C::ASLOT;
+            const int64_t ko = (int64_t)(s < kn ? s : kn - 1) * C::BK * (F8 ? 1 : 2) + i * astep;
+            const int rows = F8 ? 16 : 8;
             __builtin_amdgcn_global_load_lds(
-                (const void __attribute__((address_space(1)))*)(aptr[i & 1] + ko),
-                (void __attribute__((address_space(3)))*)(st + (64 * wave + 8 * i) * C::ROWB), 16, 0, 0);
+                (const void __attribute__((address_space(1)))*)(aptr[F8 ? 0 : (i & 1)] + ko),
+                (void __attribute__((address_space(3)))*)(st + (64 * wave + rows * i) * C::AROWB), 16, 0, 0);
         };
         auto load_b = [&](int s, int i) {
             unsigned char* st = ring + C::B_OFF + (s & 1) * C::SLOT;
@@ -244,40 +269,83 @@ __global__ __launch_bounds__(256) void q_kernel(TiledParams p)
                     for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.0f;
 
             bf16x8 fa[2][NT], fb[2][NMT];
+            // 8-bit weights: raw 16-byte reads, k-steps (0,1) and (2,3).  A
+            // native vector type: an aggregate (HIP's uint4) load carries no
+            // memory operand the compiler can tell apart from the in-flight
+            // global->LDS loads, and it then waits for all of them (vmcnt(0))
+            // before each read.
+            u32x4 fq[NT][2];
             // fragment f (0-3: weight tiles, 4-7: token tiles) of k-step ks of step s
             auto fread1 = [&](int s, int ks, int slot, int f) {
                 if (f >= NT + NMT) return;  // token tile not multiplied in this variant
                 if (f < NT) {
-                    const unsigned char* sa = ring + (s % 3) * C::SLOT + a_wave + xk[ks];
+                    const unsigned char* sa = ring + (s % 3) * C::ASLOT + a_wave + xk[ks];
                     fa[slot][f] = *reinterpret_cast<const bf16x8*>(sa + atile(f));
                 } else {
                     const unsigned char* sb = ring + C::B_OFF + (s & 1) * C::SLOT + b_wave + xk[ks];
                     fb[slot][f - NT] = *reinterpret_cast<const bf16x8*>(sb + (f - NT) * 32 * C::ROWB);
                 }
             };
+            // 8-bit weights: token fragment m of k-step ks of step s, and the
+            // raw weight bytes of k-step pair q of step s for tile nt
+            auto fread_b = [&](int s, int ks, int slot, int m) {
+                if (m >= NMT) return;
+                const unsigned char* sb = ring + C::B_OFF + (s & 1) * C::SLOT + b_wave + xk[ks];
+                fb[slot][m] = *reinterpret_cast<const bf16x8*>(sb + m * 32 * C::ROWB);
+            };
+            auto fread_q = [&](int s, int q, int nt) {
+                const unsigned char* sa = ring + (s % 3) * C::ASLOT + a_wave + xa[q];
+                fq[nt][q] = *reinterpret_cast<const u32x4*>(sa + atile(nt));
+            };
             auto fence = [] { __builtin_amdgcn_sched_barrier(0); };
+
+            // 8-bit weights: the row scales of this lane's accumulator rows
+            // (UP: w1 then w3 rows of its two 32-row tiles; DOWN: its four
+            // tiles), loaded before the prologue's loads so that they are the
+            // oldest memory operations and the counter waits below stay exact
+            floatx4 sc[4][4];
+            if constexpr (F8) {
+                const int n0 = nb * C::NOUT + (UP ? wr * 64 : wr * 128) + 4 * (lane >> 5);
+    #pragma unroll
+                for (int t = 0; t < 4; ++t) {
+                    const float* sp = UP ? (t < 2 ? p.sa : p.sb) + (int64_t)e * p.N + n0 + (t & 1) * 32
+                                         : p.sa + (int64_t)e * p.N + n0 + t * 32;
+    #pragma unroll
+                    for (int q = 0; q < 4; ++q) sc[t][q] = *reinterpret_cast<const floatx4*>(sp + 8 * q);
+                }
+            }
 
             // prologue: A(0), B(0), A(1), as the steady state would have issued
             // them; A(0) and B(0) complete everywhere
     #pragma unroll
-            for (int i = 0; i < L; ++i) load_a(0, i);
+            for (int i = 0; i < LA; ++i) load_a(0, i);
             if (bload) {
     #pragma unroll
                 for (int i = 0; i < L; ++i) load_b(0, i);
             }
     #pragma unroll
-            for (int i = 0; i < L; ++i) load_a(1, i);
-            wait_vmem<L>();
+            for (int i = 0; i < LA; ++i) load_a(1, i);
+            wait_vmem<LA>();
             fence();
             __builtin_amdgcn_s_barrier();
             fence();
+            if constexpr (F8) {
     #pragma unroll
-            for (int f = 0; f < NT + NMT; ++f) fread1(0, 0, 0, f);
+                for (int nt = 0; nt < NT; ++nt) fread_q(0, 0, nt);
+    #pragma unroll
+                for (int m = 0; m < NMT; ++m) fread_b(0, 0, 0, m);
+            } else {
+    #pragma unroll
+                for (int f = 0; f < NT + NMT; ++f) fread1(0, 0, 0, f);
+            }
 
             // step j: k-step ks multiplies fragments slot ks & 1 while the other
             // slot receives the next k-step's fragments (in k-step 3: k-step 0 of
-            // step j+1).  Loads: B(j+1) in k-step 0, A(j+2) in k-steps 1 and 2.
-            // After k-step 2 every wave waits for its reads of step j's last
+            // step j+1).  Loads: B(j+1) in k-step 0, A(j+2) in k-steps 1 and 2
+            // (8-bit weights: k-step 1).  8-bit weight bytes are read a pair of
+            // k-steps at a time (k-step 0: pair 1 of step j; k-step 3: pair 0
+            // of step j+1) and widened to bf16 just before their MFMAs.  After
+            // k-step 2 every wave waits for its reads of step j's last
             // fragments and for its loads up to B(j+1), then one barrier makes
             // A(j+1), B(j+1) complete and frees the slots of A(j), B(j).
             for (int j = 0; j < kn; ++j) {
@@ -289,27 +357,42 @@ __global__ __launch_bounds__(256) void q_kernel(TiledParams p)
                     const int rs = ks < 3 ? j : j + 1, rk = ks < 3 ? ks + 1 : 0;
     #pragma unroll
                     for (int g = 0; g < NT; ++g) {
-                        acc[g][0] = mfma32x32x16(fa[cur][g], fb[cur][0], acc[g][0]);
-                        if constexpr (NMT > 1) acc[g][1] = mfma32x32x16(fa[cur][g], fb[cur][1], acc[g][1]);
+                        bf16x8 a;
+                        if constexpr (F8) {
+                            const u32x4 q = fq[g][ks >> 1];
+                            a = (ks & 1) ? e4m3x8_to_bf16(q[2], q[3]) : e4m3x8_to_bf16(q[0], q[1]);
+                        } else {
+                            a = fa[cur][g];
+                        }
+                        acc[g][0] = mfma32x32x16(a, fb[cur][0], acc[g][0]);
+                        if constexpr (NMT > 1) acc[g][1] = mfma32x32x16(a, fb[cur][1], acc[g][1]);
                         fence();
-                        fread1(rs, rk, cur ^ 1, 2 * g);
-                        fread1(rs, rk, cur ^ 1, 2 * g + 1);
+                        if constexpr (F8) {
+                            fread_b(rs, rk, cur ^ 1, g);
+                            if (ks == 0)
+                                fread_q(j, 1, g);
+                            else if (ks == 3)
+                                fread_q(j + 1, 0, g);
+                        } else {
+                            fread1(rs, rk, cur ^ 1, 2 * g);
+                            fread1(rs, rk, cur ^ 1, 2 * g + 1);
+                        }
                         if (ks == 0) {
                             if (bload) {
                                 load_b(j + 1, 2 * g);
                                 load_b(j + 1, 2 * g + 1);
                             }
-                        } else if (ks < 3) {
-                            load_a(j + 2, (ks - 1) * 4 + g);
+                        } else if (F8 ? ks == 1 : ks < 3) {
+                            load_a(j + 2, F8 ? g : (ks - 1) * 4 + g);
                         }
                         fence();
-                        if constexpr (NMT > 2) acc[g][2] = mfma32x32x16(fa[cur][g], fb[cur][2], acc[g][2]);
-                        if constexpr (NMT > 3) acc[g][3] = mfma32x32x16(fa[cur][g], fb[cur][3], acc[g][3]);
+                        if constexpr (NMT > 2) acc[g][2] = mfma32x32x16(a, fb[cur][2], acc[g][2]);
+                        if constexpr (NMT > 3) acc[g][3] = mfma32x32x16(a, fb[cur][3], acc[g][3]);
                         fence();
                     }
                     if (ks == 2) {
                         wait_lds();
-                        wait_vmem<L>();
+                        wait_vmem<LA>();
                         fence();
                         __builtin_amdgcn_s_barrier();
                         fence();
@@ -323,19 +406,30 @@ __global__ __launch_bounds__(256) void q_kernel(TiledParams p)
             // copy all accumulators out of their registers at once.  Token columns
             // past the expert's rows were loaded from its last row, so they hold
             // exactly that row's results and store the same bits to the same place.
+            // 8-bit weights: each weight row's scale multiplies its accumulators.
     #pragma unroll
             for (int mt = 0; mt < NMT; ++mt) {
                 const int mloc = (wm * NMT + mt) * 32 + (lane & 31);
                 const int64_t rrow = row0 + m0 + (mloc < Mp ? mloc : Mp - 1);
                 if (UP) {
-                    bf16_t* hrow = p.h_out + rrow * p.N + nb * C::NOUT + wr * 64 + 4 * (lane >> 5);
+                    const int n0 = nb * C::NOUT + wr * 64 + 4 * (lane >> 5);
+                    bf16_t* hrow = p.h_out + rrow * p.N + n0;
     #pragma unroll
                     for (int h = 0; h < 2; ++h) {
                         // the accumulators are redefined here (in their AGPRs), so
                         // their copies into VGPRs cannot move above this point
                         asm volatile("" : "+a"(acc[h][mt]), "+a"(acc[h + 2][mt]));
-                        const floatx16& u = acc[h][mt];
-                        const floatx16& v = acc[h + 2][mt];
+                        floatx16 u = acc[h][mt];
+                        floatx16 v = acc[h + 2][mt];
+                        if constexpr (F8) {
+    #pragma unroll
+                            for (int q = 0; q < 4; ++q)
+    #pragma unroll
+                                for (int i = 0; i < 4; ++i) {
+                                    u[4 * q + i] *= sc[h][q][i];
+                                    v[4 * q + i] *= sc[h + 2][q][i];
+                                }
+                        }
     #pragma unroll
                         for (int q = 0; q < 4; ++q) {
                             uint2 pk;
@@ -352,18 +446,20 @@ __global__ __launch_bounds__(256) void q_kernel(TiledParams p)
                         orow = p.perm[rrow];
                         gw = p.topk_w[orow];
                     }
-                    float* yrow = p.y_out + part * p.slice + orow * p.N + nb * C::NOUT + wr * 128 +
-                                  4 * (lane >> 5);
+                    const int n0 = nb * C::NOUT + wr * 128 + 4 * (lane >> 5);
+                    float* yrow = p.y_out + part * p.slice + orow * p.N + n0;
     #pragma unroll
                     for (int nt = 0; nt < NT; ++nt) {
                         asm volatile("" : "+a"(acc[nt][mt]));
     #pragma unroll
                         for (int q = 0; q < 4; ++q) {
+                            floatx4 g4 = {gw, gw, gw, gw};
+                            if constexpr (F8) g4 = g4 * sc[nt][q];
                             float4 v;
-                            v.x = gw * acc[nt][mt][4 * q + 0];
-                            v.y = gw * acc[nt][mt][4 * q + 1];
-                            v.z = gw * acc[nt][mt][4 * q + 2];
-                            v.w = gw * acc[nt][mt][4 * q + 3];
+                            v.x = g4[0] * acc[nt][mt][4 * q + 0];
+                            v.y = g4[1] * acc[nt][mt][4 * q + 1];
+                            v.z = g4[2] * acc[nt][mt][4 * q + 2];
+                            v.w = g4[3] * acc[nt][mt][4 * q + 3];
                             *reinterpret_cast<float4*>(yrow + nt * 32 + 8 * q) = v;
                         }
                         __builtin_amdgcn_sched_barrier(0);
@@ -393,7 +489,7 @@ __global__ __launch_bounds__(256) void q_kernel(TiledParams p)
 template <bool UP>
 int q_grid(int N, int E, int64_t A, int ksplit_max)
 {
-    using C = QCfg<UP>;
+    using C = QCfg<UP, false>;  // the item shape does not depend on the weight format
     const int64_t nbn = N / C::NOUT;
     const int64_t items = nbn * (A / C::BM + E) * (UP ? 1 : ksplit_max);
     int64_t grid = cu_count();
@@ -401,19 +497,19 @@ int q_grid(int N, int E, int64_t A, int ksplit_max)
     return static_cast<int>(((grid + 7) / 8) * 8);
 }
 
-template <bool UP>
+template <bool UP, bool F8>
 hipError_t run_q(const TiledParams& p, int64_t A, hipStream_t stream)
 {
-    using C = QCfg<UP>;
+    using C = QCfg<UP, F8>;
     static bool attr_set = false;
     if (!attr_set) {
-        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&q_kernel<UP>),
+        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&q_kernel<UP, F8>),
                                            hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS_BYTES);
         if (e != hipSuccess) return e;
         attr_set = true;
     }
     const int grid = q_grid<UP>(p.N, p.E, A, p.ksplit_max);
-    q_kernel<UP><<<static_cast<unsigned>(grid), C::THREADS, C::LDS_BYTES, stream>>>(p);
+    q_kernel<UP, F8><<<static_cast<unsigned>(grid), C::THREADS, C::LDS_BYTES, stream>>>(p);
     return hipGetLastError();
 }
 
@@ -435,8 +531,8 @@ int cu_count()
 
 bool tiled_supported(int d, int ffn)
 {
-    return ffn % QCfg<true>::NOUT == 0 && d % QCfg<false>::NOUT == 0 && d % QCfg<true>::BK == 0 &&
-           ffn % QCfg<false>::BK == 0;
+    return ffn % QCfg<true, false>::NOUT == 0 && d % QCfg<false, false>::NOUT == 0 &&
+           d % QCfg<true, false>::BK == 0 && ffn % QCfg<false, false>::BK == 0;
 }
 
 hipError_t launch_tiled_up(const UpArgs& a, hipStream_t stream)
@@ -448,6 +544,10 @@ hipError_t launch_tiled_up(const UpArgs& a, hipStream_t stream)
     p.offsets = a.offsets;
     p.wa = a.w1;
     p.wb = a.w3;
+    p.qa = a.q1;
+    p.qb = a.q3;
+    p.sa = a.s1;
+    p.sb = a.s3;
     p.N = a.ffn;
     p.K = a.d;
     p.E = a.E;
@@ -456,7 +556,7 @@ hipError_t launch_tiled_up(const UpArgs& a, hipStream_t stream)
     p.mhi = a.mhi;
     p.ksplit_max = 1;
     p.A = a.A;
-    return run_q<true>(p, a.A, stream);
+    return a.q1 ? run_q<true, true>(p, a.A, stream) : run_q<true, false>(p, a.A, stream);
 }
 
 int tiled_down_grid(const DownArgs& a)
@@ -470,6 +570,8 @@ hipError_t launch_tiled_down(const DownArgs& a, hipStream_t stream)
     p.act = a.h;
     p.offsets = a.offsets;
     p.wa = a.w2;
+    p.qa = a.q2;
+    p.sa = a.s2;
     p.N = a.d;
     p.K = a.ffn;
     p.E = a.E;
@@ -482,7 +584,7 @@ hipError_t launch_tiled_down(const DownArgs& a, hipStream_t stream)
     p.slice = a.A * a.d;
     p.ksplit_out = a.ksplit_out;
     p.A = a.A;
-    return run_q<false>(p, a.A, stream);
+    return a.q2 ? run_q<false, true>(p, a.A, stream) : run_q<false, false>(p, a.A, stream);
 }
 
 }  // namespace moe

@@ -106,6 +106,11 @@ WORKLOADS = {
     "decode_t256_skew_fp8": Workload("decode_t256_skew_fp8", 256, MIXTRAL_D, MIXTRAL_FFN,
                                      MIXTRAL_E, MIXTRAL_K, 1.0, 0.02, 0.02, 0.02, 0.02,
                                      bias0=2.0, fp8=True),
+    # the prefill chunk and the mixed step with 8-bit expert weights
+    "prefill_t4096_fp8": Workload("prefill_t4096_fp8", 4096, MIXTRAL_D, MIXTRAL_FFN, MIXTRAL_E,
+                                  MIXTRAL_K, 1.0, 1 / 64.0, 0.02, 0.02, 0.02, fp8=True),
+    "mixed_t576_fp8": Workload("mixed_t576_fp8", 576, MIXTRAL_D, MIXTRAL_FFN, MIXTRAL_E,
+                               MIXTRAL_K, 1.0, 0.02, 0.02, 0.02, 0.02, fp8=True),
     # one GPU's share of the decode step under 8-way tensor parallelism: every
     # expert with ffn / 8 hidden units (the partial outputs are then summed
     # across GPUs)

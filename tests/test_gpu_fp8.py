@@ -31,7 +31,8 @@ def _forward_check(c, rows=None):
     return out
 
 
-@pytest.mark.parametrize("shape", [(16, 256, 512, 8, 2), "decode_t64_fp8"])
+@pytest.mark.parametrize("shape", [(16, 256, 512, 8, 2), "decode_t64_fp8",
+                                   (600, 256, 512, 8, 2)])
 def test_fp8_stages_teacher_forced(shape):
     """up/down fed the oracle's routing; h and y compared slot by slot, with
     and without the fused gather and the fused gate-weighted scatter."""
@@ -92,6 +93,31 @@ def test_fp8_forward_skew_sampled():
 def test_fp8_forward_shapes(shape):
     say(f"[fp8 forward] shape {shape}")
     _forward_check(fp8_small_case(*shape, seed=13))
+
+
+@pytest.mark.parametrize("shape", [
+    (600, 512, 1024, 8, 2),   # tiled: 2 weight blocks, down cut in 2 parts
+    (1000, 512, 384, 8, 2),   # tiled: odd count of 128-column output blocks
+    (288, 256, 2048, 8, 2),   # tiled: one token tile per expert, down cut in 4 parts
+    (700, 256, 256, 4, 2),    # tiled: several ragged 256-row token tiles per expert
+])
+def test_fp8_forward_tiled_shapes(shape):
+    """Above 64 rows per expert the 8-bit weights take the tiled kernels (E4M3
+    bytes staged in LDS, widened to bf16 at the fragment reads, row scales in
+    the epilogue)."""
+    say(f"[fp8 forward] tiled shape {shape}")
+    c = fp8_small_case(*shape, seed=14)
+    assert B.moe_gemm_variant_for(c.T, c.d, c.ffn, c.E, c.k) == 2
+    _forward_check(c)
+
+
+@pytest.mark.parametrize("name", ["prefill_t4096_fp8", "mixed_t576_fp8"])
+def test_fp8_forward_tiled_sampled(name):
+    say(f"[fp8 forward] {name} (sampled tokens)")
+    c = fp8_workload_case(name)
+    rng = np.random.default_rng(13)
+    rows = np.unique(np.concatenate([[0, c.T - 1], rng.choice(c.T, 30, replace=False)]))
+    _forward_check(c, rows)
 
 
 def test_fp8_forward_heavy_expert():
