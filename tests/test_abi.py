@@ -140,6 +140,18 @@ def test_parts_entry_points_reject(L):
         a.update(kw)
         return L.moe_combine_parts(y, a["parts"], a["mp"], None, T, d, k, a["out"], None, None)
 
+    # the 8-bit weight form: same checks, and the scales are required
+    q2, s2 = 1 << 36, 1 << 37
+    st = L.moe_swiglu_down_parts_fp8(X, 0x700000, q2, s2, None, None, T, d, ffn, E, k, 0, y,
+                                      parts, None)
+    assert st == B.MOE_ERR_INVALID_ARG and b"max_parts" in L.moe_last_error()
+    st = L.moe_swiglu_down_parts_fp8(X, 0x700000, q2, None, None, None, T, d, ffn, E, k, 4, y,
+                                      parts, None)
+    assert st == B.MOE_ERR_INVALID_ARG and b"w2s is NULL" in L.moe_last_error()
+    st = L.moe_swiglu_down_parts_fp8(X, 0x700000, q2, s2, None, None, T, d, ffn, E, k, 4, y,
+                                      y + 3 * yb + 64, None)
+    assert st == B.MOE_ERR_INVALID_ARG and b"parts overlaps y" in L.moe_last_error()
+
     assert comb(mp=0) == B.MOE_ERR_INVALID_ARG and b"max_parts" in L.moe_last_error()
     assert comb(parts=None) == B.MOE_ERR_INVALID_ARG and b"parts is NULL" in L.moe_last_error()
     assert comb(out=y + 3 * yb) == B.MOE_ERR_INVALID_ARG and b"overlaps y" in L.moe_last_error()
