@@ -349,6 +349,20 @@ def test_forward_split_side_by_side_and_graph():
         assert torch.equal(outs[2], outs[0]), rep
 
 
+@pytest.mark.parametrize("variant", [0, 1])
+def test_forward_long_prefill_chunk(variant):
+    """32768 tokens at the Mixtral shapes (65536 assignments, ~8192 rows per
+    expert, 32 token tiles each): row and item indices well past the bench
+    sizes; sampled tokens against the oracle, including the first and last."""
+    say(f"[forward] 32768-token prefill chunk, variant {variant}")
+    c = workload_case("prefill_t4096", T=32768)
+    rng = np.random.default_rng(19)
+    rows = np.unique(np.concatenate([[0, c.T - 1], rng.choice(c.T, 30, replace=False)]))
+    _forward_check(c, rows, variant)
+    del c
+    torch.cuda.empty_cache()
+
+
 def test_forward_t0():
     c = small_case(3, 64, 64, 4, 2)
     out = torch.zeros(0, 64, dtype=torch.bfloat16, device=DEV)
