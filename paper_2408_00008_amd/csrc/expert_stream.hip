@@ -562,11 +562,17 @@ hipError_t launch_stream_down(const DownArgs& a, int64_t rows_max, hipStream_t s
     if (!a.offsets) {
         // dense projection (one matrix): several reduction shares per
         // workgroup, so that a single matrix still spreads over the CUs.
-        // Measured on MI355X at 64 tokens, K = 4096: up to 4096 output rows,
-        // 2 row waves x 4 shares with 32-token passes (2 workgroups per slab,
-        // the second re-reading it from L2; 4096 rows: 23 -> 14 us); more
-        // rows, 4 x 4 with 64-token passes (6144 rows: 24 us)
-        if (a.d <= 4096 && a.ffn % 512 == 0) return run<false, 2, 4, 2, 128>(p, rows_max, stream);
+        // Measured on MI355X, K = 4096: more than 4096 output rows, 2 row
+        // waves x 4 shares with 64-token passes (6144 rows: 23 -> 18 us at 64
+        // tokens, 19 -> 12 us at 8); up to 24 tokens, 16-row slabs (4096 rows
+        // at 8 tokens: 11.6 -> 8.3 us); otherwise 2 row waves x 4 shares
+        // with 32-token passes (2 workgroups per slab, the second re-reading
+        // it from L2; 4096 rows at 64 tokens: 23 -> 14 us)
+        if (a.ffn % 512 == 0) {
+            if (a.d > 4096) return run<false, 2, 4, 4, 128>(p, rows_max, stream);
+            if (G == 2) return run<false, 1, 4, 2, 128>(p, rows_max, stream);
+            return run<false, 2, 4, 2, 128>(p, rows_max, stream);
+        }
         if (a.ffn % 256 == 0) {
             if (G == 2) return run<false, 4, 4, 2, 64>(p, rows_max, stream);
             return run<false, 4, 4, 4, 64>(p, rows_max, stream);
