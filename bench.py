@@ -125,11 +125,11 @@ def main():
     perm = torch.empty(A, dtype=torch.int32, device=dev)
     h = torch.empty(A, ffn, dtype=torch.bfloat16, device=dev)
     # as in moe_forward, the down GEMM may cut its reduction into parts written
-    # as separate slices: up to 4 where the tiled kernels run, up to 8 for
+    # as separate slices: up to 4 where the tiled kernels run, up to 2 for
     # the heavy experts of a split streaming step
     variant = {1: "stream", 2: "tiled", 3: "split"}[B.moe_gemm_variant_for(T, d, ffn, E, k)]
     cut = variant in ("tiled", "split")
-    y = torch.empty({"tiled": 4, "split": 8}[variant] if cut else 1, A, d, dtype=torch.float32,
+    y = torch.empty({"tiled": 4, "split": 2}[variant] if cut else 1, A, d, dtype=torch.float32,
                     device=dev)
     parts = torch.ones(1, dtype=torch.int32, device=dev)
     out = torch.empty(T, d, dtype=torch.bfloat16, device=dev)

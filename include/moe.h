@@ -186,7 +186,7 @@ moe_status_t moe_combine_parts(const float* y, const int32_t* parts, int32_t max
  * demand (a growth is refused with MOE_ERR_NO_MEMORY while `stream` is being
  * captured into a graph; call once outside capture first).
  * At prefill sizes (up to 4 parts) and for the heavy experts of a streaming
- * step with T > 64 (up to 8 parts) the down GEMM runs as
+ * step with T > 64 (up to 2 parts) the down GEMM runs as
  * moe_swiglu_down_parts and the combine as moe_combine_parts (the part count
  * depends on the routed row counts and the GPU's compute units), so the
  * result can differ in the last bits from the uncut staged calls

@@ -166,16 +166,18 @@ constexpr int64_t kLightRows = 64;
 //  * tiled regime (over 64 rows per expert on average): up to 4, where the
 //    tiles fill fewer than 16 rounds of 256 workgroups;
 //  * streaming regime with T > kLightRows, where an expert may be heavy: up to
-//    8 for the heavy experts' tiled launch (their few tiles spread over the
-//    whole GPU; the parts are folded back into slice 0 before the combine).
-//    Measured on MI355X, one expert of 194 rows and seven of 45: down +
-//    combine 253 us with the heavy expert streaming in 64-row passes, 318 /
-//    260 / 234 / 236 us with at most 2 / 4 / 8 / 16 parts.
+//    2 for the heavy experts' tiled launch, which runs next to the light
+//    experts' streaming launch (the parts are folded back into slice 0
+//    before the combine).  Measured on MI355X, one expert of 194 rows and
+//    seven of 45, down + combine: 264 us with the heavy expert streaming in
+//    64-row passes after the light ones; side by side 224 / 233 / 242 / 242 us
+//    with at most 2 / 4 / 8 / 16 parts (in sequence 8 parts were best: the
+//    fewer the parts, the fewer CUs the heavy launch takes from the light).
 int down_split_max(int64_t T, int32_t d, int32_t ffn, int32_t E, int32_t k)
 {
     const int64_t A = T * k;
     if (!moe::tiled_supported(d, ffn)) return 1;
-    if (A <= 64LL * E) return T > kLightRows ? parts_cap(ffn, 8) : 1;
+    if (A <= 64LL * E) return T > kLightRows ? parts_cap(ffn, 2) : 1;
     const int64_t items = (int64_t)(d / 256) * (A / 256 + E);
     if (items >= 16 * 256) return 1;
     return parts_cap(ffn, 4);

@@ -275,8 +275,8 @@ def test_forward_down_split(shape, parts):
 
 
 @pytest.mark.parametrize("shape", [
-    (256, 256, 2048, 8, 2),   # heavy expert: 4 parts of 8 steps
-    (256, 256, 8192, 8, 2),   # heavy expert: up to 8 parts of 16 steps
+    (256, 256, 2048, 8, 2),   # heavy expert: 2 parts of 16 steps
+    (256, 256, 8192, 8, 2),   # heavy expert: 2 parts of 64 steps
 ])
 def test_forward_split_heavy_cut(shape):
     """Streaming regime with a heavy expert: its down GEMM takes the tiled
@@ -296,8 +296,8 @@ def test_forward_split_heavy_cut(shape):
     of = gpu_forward(c, out_f32=True)[1]
     h = torch.empty(T * k, c.ffn, dtype=torch.bfloat16, device=DEV)
     B.moe_swiglu_up(c.x, offs, c.w1, c.w3, T, k, h, perm=perm)
-    # 8 slices: the forward's cap in this regime
-    yp = torch.empty(8, T * k, d, dtype=torch.float32, device=DEV)
+    # 2 slices: the forward's cap in this regime
+    yp = torch.empty(2, T * k, d, dtype=torch.float32, device=DEV)
     np_dev = torch.zeros(1, dtype=torch.int32, device=DEV)
     B.moe_swiglu_down_parts(h, offs, c.w2, T, k, yp, np_dev, topk_w=gw, perm=perm)
     st = torch.empty(T, d, dtype=torch.float32, device=DEV)
