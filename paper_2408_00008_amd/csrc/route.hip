@@ -3,11 +3,12 @@
 // The router of a Mixtral MoE layer (the model of the paper's engine, Sec. 4.1)
 // scores every token against every expert, keeps the k best experts and
 // weights them with a softmax over the kept scores.  Here:
-//   * one workgroup (8 wave64) per token: each lane multiplies 16-byte chunks
-//     of x against the same chunk of every expert's router row, accumulating
-//     in f32; the per-expert partial sums are combined by a transposed wave
-//     butterfly and a fixed-order sum over the waves, so results are bitwise
-//     reproducible;
+//   * one workgroup (8 wave64) per token, or per 64 / E tokens for long
+//     inputs: each lane multiplies 16-byte chunks of x against the same chunk
+//     of every expert's router row, accumulating in f32; the per-(token,
+//     expert) partial sums are combined by a transposed wave butterfly and a
+//     fixed-order sum over the waves, so results are bitwise reproducible and
+//     the same for any tokens per workgroup;
 //   * the top k are then ranked on the key (logit, -expert) -- equal logits
 //     pick the lower expert -- by one lane for up to 16 experts, or by a
 //     wave-wide arg-max butterfly for more, and the softmax over the selected
@@ -36,56 +37,79 @@ __device__ __forceinline__ bool ahead(const Cand& a, const Cand& b)
     return a.v > b.v || (a.v == b.v && a.i < b.i);
 }
 
-template <int EMAX>
+// TPB tokens per workgroup pass (EMAX * TPB <= 64): every 16-byte chunk of the
+// router rows is loaded once and multiplied with the TPB tokens' chunks, and
+// the (token, expert) partial sums are reduced together.  A sum's order does
+// not depend on TPB or on the token's place in the pass (the same chunks per
+// lane in the same order, the same lane tree, the same wave order), so the
+// logits are bitwise those of one token per workgroup.
+template <int EMAX, int TPB>
 __global__ __launch_bounds__(ROUTE_THREADS) void router_topk_kernel(
     const bf16_t* __restrict__ x, const bf16_t* __restrict__ wr, const float* __restrict__ bias,
     int64_t T, int d, int E, int k, int32_t* __restrict__ topk_ids, float* __restrict__ topk_w,
     float* __restrict__ logits_out)
 {
-    __shared__ float red[ROUTE_THREADS / 64][EMAX];
-    __shared__ float lg[EMAX];
+    constexpr int NV = EMAX * TPB;  // (token, expert) sums per lane, index j * EMAX + e
+    static_assert(NV <= 64 && (NV & (NV - 1)) == 0, "at most 64 sums, a power of two");
+    __shared__ float red[ROUTE_THREADS / 64][NV];
+    __shared__ float lg[TPB][EMAX];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int nchunk = d >> 3;  // 16-byte chunks per row
+    const int64_t npass = (T + TPB - 1) / TPB;
 
-    for (int64_t t = blockIdx.x; t < T; t += gridDim.x) {
-        float acc[EMAX];
+    for (int64_t pass = blockIdx.x; pass < npass; pass += gridDim.x) {
+        const int64_t t0 = pass * TPB;
+        const int nt = static_cast<int>(T - t0 < TPB ? T - t0 : TPB);
+        float acc[NV];
 #pragma unroll
-        for (int e = 0; e < EMAX; ++e) acc[e] = 0.0f;
-        const bf16_t* xr = x + t * (int64_t)d;
+        for (int i = 0; i < NV; ++i) acc[i] = 0.0f;
         for (int c = tid; c < nchunk; c += ROUTE_THREADS) {
-            uint4 xv = ldg16(xr + c * 8);
-            float xf[8];
-            const uint32_t xw[4] = {xv.x, xv.y, xv.z, xv.w};
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                xf[2 * q] = __uint_as_float(xw[q] << 16);
-                xf[2 * q + 1] = __uint_as_float(xw[q] & 0xffff0000u);
-            }
+            float wf[EMAX][8];
 #pragma unroll
             for (int e = 0; e < EMAX; ++e) {
                 if (e < E) {
-                    uint4 wv = ldg16(wr + (int64_t)e * d + c * 8);
+                    const uint4 wv = ldg16(wr + (int64_t)e * d + c * 8);
                     const uint32_t ww[4] = {wv.x, wv.y, wv.z, wv.w};
-                    float s = acc[e];
 #pragma unroll
                     for (int q = 0; q < 4; ++q) {
-                        s = fmaf(xf[2 * q], __uint_as_float(ww[q] << 16), s);
-                        s = fmaf(xf[2 * q + 1], __uint_as_float(ww[q] & 0xffff0000u), s);
+                        wf[e][2 * q] = __uint_as_float(ww[q] << 16);
+                        wf[e][2 * q + 1] = __uint_as_float(ww[q] & 0xffff0000u);
                     }
-                    acc[e] = s;
+                }
+            }
+#pragma unroll
+            for (int j = 0; j < TPB; ++j) {
+                if (j < nt) {
+                    const uint4 xv = ldg16(x + (t0 + j) * (int64_t)d + c * 8);
+                    float xf[8];
+                    const uint32_t xw[4] = {xv.x, xv.y, xv.z, xv.w};
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        xf[2 * q] = __uint_as_float(xw[q] << 16);
+                        xf[2 * q + 1] = __uint_as_float(xw[q] & 0xffff0000u);
+                    }
+#pragma unroll
+                    for (int e = 0; e < EMAX; ++e) {
+                        if (e < E) {
+                            float s = acc[j * EMAX + e];
+#pragma unroll
+                            for (int q = 0; q < 8; ++q) s = fmaf(xf[q], wf[e][q], s);
+                            acc[j * EMAX + e] = s;
+                        }
+                    }
                 }
             }
         }
         // Transposed butterfly: at each exchange a lane keeps half of its
-        // per-expert partial sums and ships the other half to its partner, so
-        // after log2(EMAX) exchanges lane l holds expert (l / (64/EMAX)) summed
-        // over 2^log2(EMAX) lanes; the remaining lane bits are then folded.
-        // EMAX-1 + log2(64/EMAX) shuffles instead of EMAX * 6.
-        float v[EMAX];
+        // partial sums and ships the other half to its partner, so after
+        // log2(NV) exchanges lane l holds sum l / (64/NV) over 2^log2(NV)
+        // lanes; the remaining lane bits are then folded.  Every sum is
+        // reduced over the same lane tree (bit 5 first, then 4, ... 0).
+        float v[NV];
 #pragma unroll
-        for (int e = 0; e < EMAX; ++e) v[e] = acc[e];
+        for (int i = 0; i < NV; ++i) v[i] = acc[i];
 #pragma unroll
-        for (int half = EMAX / 2, m = 32; half >= 1; half >>= 1, m >>= 1) {
+        for (int half = NV / 2, m = 32; half >= 1; half >>= 1, m >>= 1) {
             const bool hi = (lane & m) != 0;
 #pragma unroll
             for (int i = 0; i < half; ++i) {
@@ -94,25 +118,28 @@ __global__ __launch_bounds__(ROUTE_THREADS) void router_topk_kernel(
                 v[i] = keep + wave_shfl_xor(send, m);
             }
         }
-        constexpr int LANES_PER_E = 64 / EMAX;
+        constexpr int LANES_PER_V = 64 / NV;
         float tot = v[0];
 #pragma unroll
-        for (int m = LANES_PER_E / 2; m >= 1; m >>= 1) tot += wave_shfl_xor(tot, m);
-        const int my_e = lane / LANES_PER_E;
-        if ((lane % LANES_PER_E) == 0 && my_e < E) red[wave][my_e] = tot;
+        for (int m = LANES_PER_V / 2; m >= 1; m >>= 1) tot += wave_shfl_xor(tot, m);
+        if ((lane % LANES_PER_V) == 0) red[wave][lane / LANES_PER_V] = tot;
         __syncthreads();
-        if (tid < E) {
-            float s = red[0][tid];
+        if (tid < NV) {
+            const int j = tid / EMAX, e = tid - j * EMAX;
+            if (j < nt && e < E) {
+                float s = red[0][tid];
 #pragma unroll
-            for (int w = 1; w < ROUTE_THREADS / 64; ++w) s += red[w][tid];
-            if (bias) s += bias[tid];
-            lg[tid] = s;
-            if (logits_out) logits_out[t * E + tid] = s;
+                for (int w = 1; w < ROUTE_THREADS / 64; ++w) s += red[w][tid];
+                if (bias) s += bias[e];
+                lg[j][e] = s;
+                if (logits_out) logits_out[(t0 + j) * E + e] = s;
+            }
         }
         __syncthreads();
         if (EMAX <= 16) {
-            // few experts: one lane ranks them directly
-            if (tid == 0) {
+            // few experts: one lane per token ranks them directly
+            if (tid < nt) {
+                const int64_t t = t0 + tid;
                 int seli[8];
                 float selv[8];
                 uint32_t taken = 0;
@@ -124,7 +151,7 @@ __global__ __launch_bounds__(ROUTE_THREADS) void router_topk_kernel(
 #pragma unroll
                         for (int e = 0; e < EMAX; ++e) {
                             if (e < E && !(taken & (1u << e))) {
-                                const float le = lg[e];
+                                const float le = lg[tid][e];
                                 // strict: an equal logit keeps the lower index
                                 if (best < 0 || le > bv) {
                                     best = e;
@@ -156,9 +183,11 @@ __global__ __launch_bounds__(ROUTE_THREADS) void router_topk_kernel(
             __syncthreads();
             continue;
         }
-        if (wave == 0) {
+        // more experts: wave j ranks token j with a wave-wide arg-max
+        if (wave < nt) {
+            const int64_t t = t0 + wave;
             Cand me;
-            me.v = lane < E ? lg[lane] : -INFINITY;
+            me.v = lane < E ? lg[wave][lane] : -INFINITY;
             me.i = lane < E ? lane : 0x7fffffff;
             float selv[8];
             int seli[8];
@@ -274,19 +303,29 @@ hipError_t launch_router_topk(const bf16_t* x, const bf16_t* router_w, const flo
                               float* logits, hipStream_t stream)
 {
     if (T == 0) return hipSuccess;
-    const unsigned grid = static_cast<unsigned>(T < 16384 ? T : 16384);
-    if (E <= 8)
-        router_topk_kernel<8><<<grid, ROUTE_THREADS, 0, stream>>>(x, router_w, bias, T, d, E, k,
-                                                                  topk_ids, topk_w, logits);
-    else if (E <= 16)
-        router_topk_kernel<16><<<grid, ROUTE_THREADS, 0, stream>>>(x, router_w, bias, T, d, E, k,
-                                                                   topk_ids, topk_w, logits);
-    else if (E <= 32)
-        router_topk_kernel<32><<<grid, ROUTE_THREADS, 0, stream>>>(x, router_w, bias, T, d, E, k,
-                                                                   topk_ids, topk_w, logits);
-    else
-        router_topk_kernel<64><<<grid, ROUTE_THREADS, 0, stream>>>(x, router_w, bias, T, d, E, k,
-                                                                   topk_ids, topk_w, logits);
+    // 64 / EMAX tokens per workgroup pass where that still makes 256
+    // workgroups; fewer tokens, one per workgroup.  Measured on MI355X (route
+    // + dispatch, E = 8): 4096 tokens 62 -> 42 us; 64 tokens 11.5 us with one
+    // per workgroup, 16.8 us with eight.
+    const int tpb = E <= 8 ? 8 : (E <= 16 ? 4 : (E <= 32 ? 2 : 1));
+    const bool multi = T >= 256LL * tpb;
+#define MOE_ROUTE(EMAX_, TPB_)                                                                    \
+    {                                                                                             \
+        const int64_t npass = (T + (TPB_) - 1) / (TPB_);                                          \
+        const unsigned grid = static_cast<unsigned>(npass < 16384 ? npass : 16384);               \
+        router_topk_kernel<EMAX_, TPB_><<<grid, ROUTE_THREADS, 0, stream>>>(                      \
+            x, router_w, bias, T, d, E, k, topk_ids, topk_w, logits);                             \
+    }
+    if (E <= 8) {
+        if (multi) MOE_ROUTE(8, 8) else MOE_ROUTE(8, 1)
+    } else if (E <= 16) {
+        if (multi) MOE_ROUTE(16, 4) else MOE_ROUTE(16, 1)
+    } else if (E <= 32) {
+        if (multi) MOE_ROUTE(32, 2) else MOE_ROUTE(32, 1)
+    } else {
+        MOE_ROUTE(64, 1)
+    }
+#undef MOE_ROUTE
     return hipGetLastError();
 }
 

@@ -53,11 +53,28 @@ def test_route(name):
 
 
 @pytest.mark.parametrize("shape", [(1, 64, 64, 1, 1), (37, 192, 320, 8, 2), (5, 128, 128, 4, 4),
-                                   (300, 64, 128, 64, 8), (129, 256, 64, 3, 2)])
+                                   (300, 64, 128, 64, 8), (129, 256, 64, 3, 2),
+                                   # several tokens per router workgroup (T >= 256 * 64 / E),
+                                   # with a partial last pass
+                                   (2053, 256, 64, 8, 2), (1029, 512, 64, 16, 4),
+                                   (515, 4096, 64, 32, 8), (2051, 128, 64, 5, 3)])
 def test_route_shapes(shape):
     say(f"[route] shape {shape}")
     c = small_case(*shape, seed=5)
     _route_checks(c)
+
+
+def test_route_tokens_per_workgroup_bitwise():
+    """Long inputs put several tokens in one router workgroup; the logits,
+    ids and gates of a token do not depend on that: routing the first 300
+    tokens alone (one per workgroup) gives the same bits."""
+    say("[route] tokens per workgroup")
+    c = small_case(2053, 512, 64, 8, 2, seed=6)
+    ids, gw, _, _, logits = gpu_route(c)
+    c2 = c.with_x(c.x[:300].contiguous())
+    ids2, gw2, _, _, logits2 = gpu_route(c2)
+    assert torch.equal(logits[:300], logits2) and torch.equal(ids[:300], ids2)
+    assert torch.equal(gw[:300], gw2)
 
 
 def test_route_ties_lower_index():
