@@ -181,6 +181,27 @@ def test_workspace_size(L):
     assert ws >= A * f * 2 + A * d * 4 + 3 * A * 4
 
 
+def _ws_bytes(T, d, ffn, E, k, slices):
+    """moe_forward's scratch for these sizes: routing arrays, h, y with
+    `slices` f32 partial-sum slices, the part count; each 256-byte aligned."""
+    a = lambda v: (v + 255) // 256 * 256
+    A = T * k
+    return (a(A * 4) * 3 + a((E + 1) * 4) + a(A * ffn * 2) + a(A * d * 4 * slices) + 256)
+
+
+@pytest.mark.parametrize("T,d,ffn,E,k,slices", [
+    (4096, 4096, 14336, 8, 2, 4),   # prefill: tiled, down cut in up to 4 parts
+    (256, 4096, 14336, 8, 2, 2),    # streaming with T > 64: heavy experts cut in up to 2
+    (64, 4096, 14336, 8, 2, 1),     # decode: no heavy expert possible, one slice
+    (1000, 512, 384, 8, 2, 1),      # tiled, but 6 reduction steps: too short to cut
+    (1000, 512, 1024, 8, 2, 2),     # 16 steps: 2 parts of 8
+    (600, 192, 320, 8, 2, 1),       # no tiled shape
+    (40000, 4096, 14336, 8, 2, 1),  # 80000 rows: the grid is full anyway
+])
+def test_workspace_holds_part_slices(L, T, d, ffn, E, k, slices):
+    assert L.moe_workspace_size(T, d, ffn, E, k) == _ws_bytes(T, d, ffn, E, k, slices)
+
+
 def test_variant_switch(L):
     assert L.moe_gemm_variant_for(64, 4096, 14336, 8, 2) == 1
     assert L.moe_gemm_variant_for(64, 4096, 14336, 8, 9) == 0
