@@ -109,7 +109,7 @@ def main():
     A = T * k
     x = inputs.make_x(w, dev)
     if w.fp8:
-        # E4M3 expert weights with per-row f32 scales (always the streaming kernels)
+        # E4M3 expert weights with per-row f32 scales
         lay = inputs.make_layer_fp8(w, 0, dev)
         q = [lay[n] for n in ("w1q", "w1s", "w3q", "w3s", "w2q", "w2s")]
         wbytes_per_elem = 1
