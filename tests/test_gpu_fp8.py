@@ -120,6 +120,32 @@ def test_fp8_forward_tiled_sampled(name):
     _forward_check(c, rows)
 
 
+@pytest.mark.parametrize("shape,bias0", [
+    ((288, 256, 2048, 8, 2), None),   # tiled: down cut in 4 parts, summed by the combine
+    ((256, 256, 2048, 8, 2), 2.0),    # split step: heavy expert cut in 2 parts, folded
+])
+def test_fp8_down_parts_pair_equals_forward(shape, bias0):
+    """moe_swiglu_down_parts_fp8 + moe_combine_parts, fed the forward's own
+    routing and h, reproduce moe_forward_fp8_ex bitwise."""
+    say(f"[fp8] parts pair {shape}")
+    bias = None if bias0 is None else [bias0] + [0.0] * (shape[3] - 1)
+    c = fp8_small_case(*shape, seed=15, bias=bias)
+    T, d, k = c.T, c.d, c.k
+    _, of = gpu_forward_fp8(c, out_f32=True)
+    ids, gw, offs, perm, _ = gpu_route(c)
+    h = torch.empty(T * k, c.ffn, dtype=torch.bfloat16, device=DEV)
+    B.moe_swiglu_up_fp8(c.x, offs, c.w1q, c.w1s, c.w3q, c.w3s, T, k, h, perm=perm)
+    slices = 4 if bias0 is None else 2  # the forward's caps in the two regimes
+    y = torch.empty(slices, T * k, d, dtype=torch.float32, device=DEV)
+    parts = torch.zeros(1, dtype=torch.int32, device=DEV)
+    B.moe_swiglu_down_parts_fp8(h, offs, c.w2q, c.w2s, T, k, y, parts, topk_w=gw, perm=perm)
+    st = torch.empty(T, d, dtype=torch.float32, device=DEV)
+    B.moe_combine_parts(y, parts, T, d, k, out_f32=st)
+    torch.cuda.synchronize()
+    assert int(parts.item()) == (4 if bias0 is None else 1)
+    assert torch.equal(st, of)
+
+
 def test_fp8_forward_heavy_expert():
     """Every token on expert 0: more passes than a slab has pass slots."""
     say("[fp8 forward] heavy expert")
