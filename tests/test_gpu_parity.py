@@ -329,6 +329,18 @@ def test_forward_split_heavy_cut(shape):
     err = rowwise_rel(st.double().cpu().numpy(), unc.double().cpu().numpy())
     say(f"  cut vs uncut: rowwise rel {err:.3e}")
     assert err < 1e-5
+    # plain mode (no gate weights, rows in permuted order): the fold works on
+    # row r itself; slice 0 then matches the uncut plain down GEMM
+    yp.fill_(0.0)
+    np_dev.fill_(0)
+    B.moe_swiglu_down_parts(h, offs, c.w2, T, k, yp, np_dev)
+    yplain = torch.empty(T * k, d, dtype=torch.float32, device=DEV)
+    B.moe_swiglu_down(h, offs, c.w2, T, k, yplain)
+    torch.cuda.synchronize()
+    assert int(np_dev.item()) == 1
+    err = rowwise_rel(yp[0].double().cpu().numpy(), yplain.double().cpu().numpy())
+    say(f"  plain rows, cut vs uncut: rowwise rel {err:.3e}")
+    assert err < 1e-5
 
 
 def test_forward_split_side_by_side_and_graph():
