@@ -71,6 +71,7 @@ constexpr int DPL = HD / LPP;
 constexpr int PPB = 64 / LPP;  // positions per wave block
 constexpr int NWAVE = 4;  // waves per workgroup
 constexpr int MAXP = 4096;  // page-table entries per request held in LDS
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
 __device__ __forceinline__ void widen16(const uint4& lo, const uint4& hi, float* f)
 {
@@ -103,10 +104,14 @@ __device__ __forceinline__ float sum8(float v)
 // One workgroup per (token t, KV head g); the GROUP query heads of g share
 // every key/value read.  A wave takes blocks of 8 positions (8 lanes per
 // position, 16 dims per lane) and keeps, per lane group, its own running max,
-// sum and weighted value sum (online softmax in base 2: the query is
-// pre-scaled by scale * log2(e)).  The wave's blocks are loaded through a
-// ring of NB register sets, NB - 1 blocks ahead of the one being multiplied.
-// The lane groups are merged by shuffles, the waves through LDS.
+// sum and weighted value sum (online softmax in base 2: each score is
+// multiplied by scale * log2(e)).  Query and key stay bf16 pairs: the dot
+// products run as 2-wide bf16 dot instructions accumulating in f32 (half the
+// instructions of widening both and multiplying in f32, and no registers for
+// widened keys; measured 62-74 -> 60-68 us for 268 MB of cache).  The wave's
+// blocks are loaded through a ring of NB register sets, NB - 1 blocks ahead
+// of the one being multiplied.  The lane groups are merged by shuffles, the
+// waves through LDS.
 //
 // With nsplit > 1 (few tokens, long contexts) the request's position blocks
 // are cut into nsplit contiguous ranges, one workgroup each (workgroup
@@ -142,14 +147,13 @@ __global__ __launch_bounds__(NWAVE * 64) void attn_decode_kernel(
     __syncthreads();
     const float qs = scale * 1.44269504088896340736f;  // scores in base 2
 
-    float qv[GROUP][DPL];
+    uint32_t qb[GROUP][DPL / 2];  // the query's bf16 pairs (exact; the scale goes on the score)
 #pragma unroll
     for (int h = 0; h < GROUP; ++h) {
         const bf16_t* qr = q + ((int64_t)t * Hq + g * GROUP + h) * HD + DPL * sub;
-        float f[DPL];
-        widen16(ldg16(qr), ldg16(qr + 8), f);
-#pragma unroll
-        for (int i = 0; i < DPL; ++i) qv[h][i] = f[i] * qs;
+        const uint4 lo = ldg16(qr), hi = ldg16(qr + 8);
+        qb[h][0] = lo.x; qb[h][1] = lo.y; qb[h][2] = lo.z; qb[h][3] = lo.w;
+        qb[h][4] = hi.x; qb[h][5] = hi.y; qb[h][6] = hi.z; qb[h][7] = hi.w;
     }
     float m[GROUP], l[GROUP], acc[GROUP][DPL];
 #pragma unroll
@@ -173,16 +177,19 @@ __global__ __launch_bounds__(NWAVE * 64) void attn_decode_kernel(
     };
     auto update = [&](int b, const uint4* kv) {
         if (PPB * b + pp >= L) return;  // uniform over the lane group
-        float kf[DPL], vf[DPL];
-        widen16(kv[0], kv[1], kf);
+        float vf[DPL];
         widen16(kv[2], kv[3], vf);
+        const uint32_t kw[DPL / 2] = {kv[0].x, kv[0].y, kv[0].z, kv[0].w,
+                                      kv[1].x, kv[1].y, kv[1].z, kv[1].w};
         float sd[GROUP];
 #pragma unroll
         for (int h = 0; h < GROUP; ++h) {
             float d = 0.0f;
 #pragma unroll
-            for (int i = 0; i < DPL; ++i) d = fmaf(qv[h][i], kf[i], d);
-            sd[h] = d;
+            for (int i = 0; i < DPL / 2; ++i)
+                d = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, qb[h][i]),
+                                                    __builtin_bit_cast(bf16x2, kw[i]), d, false);
+            sd[h] = d * qs;
         }
 #pragma unroll
         for (int h = 0; h < GROUP; ++h) sd[h] = sum8(sd[h]);
