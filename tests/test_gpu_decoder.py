@@ -164,12 +164,14 @@ def _layer(w):
     return attn, moe, kv
 
 
-def _check_layer(w, rows):
+def _check_layer(w, rows, kv=None):
     """The GPU layer against the oracle, block by block on the GPU's own
     block inputs: the attention block (h -> h1) on the layer input, the MoE
     block on the GPU's h1 (a routing decision near a tie is judged by the
-    margin rule, as for the MoE layer)."""
-    attn, moe, kv = _layer(w)
+    margin rule, as for the MoE layer).  kv: a cache, page table, positions
+    and contexts to use instead of the workload's one-token-per-request ones."""
+    attn, moe, kv0 = _layer(w)
+    kv = kv0 if kv is None else kv
     h0 = inputs.make_h(w, DEV)
     kc0, vc0 = bits(kv["k_cache"]), bits(kv["v_cache"])
     kc, vc = kv["k_cache"].clone(), kv["v_cache"].clone()  # for the whole-layer run
@@ -229,6 +231,34 @@ def test_decoder_layer_small():
     say("[decoder] layer, ragged contexts")
     w = small_workload(24, 512, 4, 2, ctx=90, page=16, ffn=512, seed=11)
     _check_layer(w, np.arange(w.T))
+
+
+def test_decoder_layer_prefill_chunks():
+    """Prefill through the same layer: two requests' prompt chunks (37 and 27
+    tokens) at consecutive positions after 21 and 0 cached ones, every token
+    of a request on that request's page-table row.  The keys and values of
+    the whole chunk go into the cache before attention, so each token
+    attends to its request's earlier positions and the chunk tokens up to
+    itself (causal).  All tokens against the oracle."""
+    say("[decoder] layer, prefill chunks")
+    w = small_workload(64, 512, 4, 2, ctx=64, page=16, ffn=512, seed=19)
+    chunks = [(21, 37), (0, 27)]  # (cached positions, chunk tokens) per request
+    page, maxp = w.page, 8
+    g = torch.Generator().manual_seed(23)
+    npages = len(chunks) * maxp
+    pages = torch.randperm(npages, generator=g).to(torch.int32).reshape(len(chunks), maxp)
+    rows, pos = [], []
+    for r, (c0, n) in enumerate(chunks):
+        rows += [pages[r]] * n
+        pos += list(range(c0, c0 + n))
+    shape = (npages, w.hkv, page, w.hd)
+    kv = {"k_cache": torch.randn(shape, generator=g).to(torch.bfloat16).to(DEV),
+          "v_cache": torch.randn(shape, generator=g).to(torch.bfloat16).to(DEV),
+          "page_table": torch.stack(rows).contiguous().to(DEV),
+          "pos": torch.tensor(pos, dtype=torch.int32, device=DEV)}
+    kv["ctx"] = kv["pos"] + 1
+    assert kv["page_table"].shape == (w.T, maxp)
+    _check_layer(w, np.arange(w.T), kv)
 
 
 def test_decoder_layer_mixtral_decode():
