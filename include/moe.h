@@ -291,7 +291,8 @@ moe_status_t moe_rmsnorm(const float* h, const moe_bf16_t* gamma, int64_t T, int
  * Dense projection y[t, n] = sum_i x[t, i] w[n, i] (bf16 operands, f32
  * accumulate and output): x [T, K] bf16, w [N, K] bf16 (nn.Linear layout),
  * y [T, N] f32.  K, N multiples of 64 (<= 65536).  The weight-streaming GEMM
- * with one matrix.
+ * with one matrix, or, from 128 output tiles of 256 x 256 on (N a multiple of
+ * 256, K of 128; e.g. N = 6144 from 1281 tokens), the tiled MFMA GEMM.
  */
 moe_status_t moe_linear(const moe_bf16_t* x, const moe_bf16_t* w, int64_t T, int32_t K, int32_t N,
                         float* y, hipStream_t stream);

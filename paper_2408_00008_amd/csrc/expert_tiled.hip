@@ -34,7 +34,7 @@ struct TiledParams {
     const bf16_t* act;       // token rows (UP: x, DOWN: h)
     const int32_t* gather;   // UP: source row = gather[r] / kslots (null = r)
     int kslots;
-    const int32_t* offsets;  // [E+1]
+    const int32_t* offsets;  // [E+1]; null: one matrix (E = 1) of all A rows
     const bf16_t* wa;        // UP: w1, DOWN: w2  [E, N, K]
     const bf16_t* wb;        // UP: w3            [E, N, K]
     // 8-bit weights (then wa/wb are unused): E4M3 bytes [E, N, K] and per-row
@@ -136,7 +136,8 @@ __global__ __launch_bounds__(256) void q_kernel(TiledParams p)
 
     // per-expert token tiles and their prefix, one expert per lane:
     // items before expert e = nbn * (token tiles of experts < e)
-    const int my_rows = lane < p.E ? p.offsets[lane + 1] - p.offsets[lane] : 0;
+    // (offsets null: one matrix, E = 1, of all A rows -- a dense projection)
+    const int my_rows = lane < p.E ? (p.offsets ? p.offsets[lane + 1] - p.offsets[lane] : (int)p.A) : 0;
     const int my_tiles = (my_rows >= p.mlo && my_rows <= p.mhi) ? (my_rows + C::BM - 1) / C::BM : 0;
     int in_tiles = my_tiles;
 #pragma unroll
@@ -200,8 +201,8 @@ __global__ __launch_bounds__(256) void q_kernel(TiledParams p)
         // this item's reduction steps [k0, k0 + kn)
         const int k0 = (int)((int64_t)nk * part / nparts);
         const int kn = (int)((int64_t)nk * (part + 1) / nparts) - k0;
-        const int row0 = p.offsets[e];
-        const int M = p.offsets[e + 1] - row0;
+        const int row0 = p.offsets ? p.offsets[e] : 0;
+        const int M = p.offsets ? p.offsets[e + 1] - row0 : (int)p.A;
         const int m0 = mtile * C::BM;
         const int Mp = min(C::BM, M - m0);
 

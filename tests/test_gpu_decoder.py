@@ -41,7 +41,9 @@ def small_workload(T, d, hq, hkv, ctx, page=16, ffn=256, E=8, k=2, ragged=True, 
 
 @pytest.mark.parametrize("T,K,N", [(1, 64, 64), (37, 512, 320), (64, 4096, 6144), (130, 256, 512),
                                    (64, 448, 192), (8, 4096, 4096), (20, 1024, 448),
-                                   (8, 4096, 6144), (64, 4096, 4096)])
+                                   (8, 4096, 6144), (64, 4096, 4096),
+                                   # 128+ output tiles: the tiled kernel, ragged last tile
+                                   (1300, 512, 8192), (2100, 2048, 4096)])
 def test_linear(T, K, N):
     say(f"[decoder] linear T={T} K={K} N={N}")
     g = torch.Generator(device=DEV).manual_seed(T + K + N)
