@@ -246,6 +246,7 @@ def test_forward_split_by_rows(shape):
 @pytest.mark.parametrize("shape,parts", [
     ((288, 256, 2048, 8, 2), 4),   # one token tile per expert, 4 parts of 8 steps
     ((600, 512, 1024, 8, 2), 2),   # 2 weight blocks per expert, 2 parts of 8 steps
+    ((600, 256, 2048, 64, 8), None),  # E = 64, k = 8: 64 ragged tiles (count not pinned)
 ])
 def test_forward_down_split(shape, parts):
     """Prefill-regime sizes with few token tiles: the tiled down GEMM cuts its
@@ -262,7 +263,8 @@ def test_forward_down_split(shape, parts):
     of = torch.empty(T, d, dtype=torch.float32, device=DEV)
     B.moe_forward_ex(c.x, c.router_w, c.w1, c.w3, c.w2, k, out_f32=of, workspace=ws)
     torch.cuda.synchronize()
-    assert int(ws[-256:].view(torch.int32)[0]) == parts
+    used = int(ws[-256:].view(torch.int32)[0])
+    assert used in (1, 2, 4) if parts is None else used == parts
     ids, gw, offs, perm, _ = gpu_route(c)
     xp = torch.empty(T * k, d, dtype=torch.bfloat16, device=DEV)
     B.moe_permute(c.x, perm, k, xp)
@@ -282,7 +284,7 @@ def test_forward_down_split(shape, parts):
     st2 = torch.empty(T, d, dtype=torch.float32, device=DEV)
     B.moe_combine_parts(yp, np_dev, T, d, k, out_f32=st2)
     torch.cuda.synchronize()
-    assert int(np_dev.item()) == parts
+    assert int(np_dev.item()) == used
     assert torch.equal(st2, of)
     # the same inputs give the same bits
     of2 = torch.empty_like(of)
