@@ -324,12 +324,12 @@ moe_status_t no_overlap_v(const char* oname, Range o, const std::vector<std::pai
 // sizes (more than kLightRows tokens, e.g. a skewed decode step), each expert
 // GEMM becomes two launches that each keep the experts of their size class:
 // experts with at most kLightRows rows stream their weights in one pass;
-// heavier ones take the tiled kernel (up, bf16) or the streaming kernel with
-// 128-row passes (down, and 8-bit weights).  Measured on MI355X with one
-// expert of 194 rows and seven of 45 (T = 256): up 426 -> 392 us, down
-// 261 -> 228 us.  Where the caller provides slices for reduction parts
+// heavier ones take the tiled kernel (up, bf16 or 8-bit weights) or, for the
+// down GEMM, the streaming kernel with 128-row passes.  Measured on MI355X
+// with one expert of 194 rows and seven of 45 (T = 256): up 426 -> 392 us,
+// down 261 -> 228 us.  Where the caller provides slices for reduction parts
 // (moe_forward, moe_swiglu_down_parts), the heavy down GEMM takes the tiled
-// kernel with its reduction cut into up to 16 parts, folded into slice 0.
+// kernel too, its reduction cut into up to 16 parts, folded into slice 0.
 
 // ---- expert groups side by side -------------------------------------------
 //
@@ -382,10 +382,13 @@ hipError_t run_side_by_side(hipStream_t stream, Light light, Heavy heavy)
     std::lock_guard<std::mutex> lk(ss->mu);
     if ((e = hipEventRecord(ss->fork, stream)) != hipSuccess) return e;
     if ((e = hipStreamWaitEvent(ss->s, ss->fork, 0)) != hipSuccess) return e;
-    if ((e = light(stream)) != hipSuccess) return e;
-    if ((e = heavy(ss->s)) != hipSuccess) return e;
-    if ((e = hipEventRecord(ss->join, ss->s)) != hipSuccess) return e;
-    return hipStreamWaitEvent(stream, ss->join, 0);
+    const hipError_t el = light(stream);
+    const hipError_t eh = el == hipSuccess ? heavy(ss->s) : hipSuccess;
+    // join after a failed launch too: whatever the side stream took on stays
+    // ordered before the caller's later work
+    e = hipEventRecord(ss->join, ss->s);
+    if (e == hipSuccess) e = hipStreamWaitEvent(stream, ss->join, 0);
+    return el != hipSuccess ? el : (eh != hipSuccess ? eh : e);
 }
 
 bool split_by_rows(int64_t rows_max, int64_t A, int E)
