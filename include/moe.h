@@ -184,7 +184,10 @@ moe_status_t moe_combine_parts(const float* y, const int32_t* parts, int32_t max
  * into the first expert GEMM) -> combine.  out [T,d] bf16, must not overlap
  * any input.  Scratch is owned by the library, cached per device and grown on
  * demand (a growth is refused with MOE_ERR_NO_MEMORY while `stream` is being
- * captured into a graph; call once outside capture first).
+ * captured into a graph; call once outside capture first).  Every call on one
+ * device shares that scratch, so calls on different streams of one device
+ * must not overlap in time; give each stream its own caller workspace
+ * (moe_forward_ex) to run them concurrently.
  * At prefill sizes (up to 4 parts) and for the heavy experts of a streaming
  * step with T > 64 (up to 2 parts) the down GEMM runs as
  * moe_swiglu_down_parts and the combine as moe_combine_parts (the part count
