@@ -199,6 +199,32 @@ def test_forward_shapes(shape, variant):
     _forward_check(small_case(*shape, seed=13), variant=variant)
 
 
+def _random_shapes(n=16, seed=2408):
+    """Seeded draws over the supported space: E in 1..64, k in 1..min(E, 8),
+    d and ffn multiples of 64 up to 768 (every other draw multiples of 256,
+    which the tiled kernel takes), T from 1 to 699 in three bands."""
+    rng = np.random.default_rng(seed)
+    out = []
+    while len(out) < n:
+        E = int(rng.choice([1, 2, 3, 4, 6, 8, 12, 16, 32, 64]))
+        k = int(rng.integers(1, min(E, 8) + 1))
+        unit = 256 if len(out) % 2 else 64
+        d = unit * int(rng.integers(1, 768 // unit + 1))
+        ffn = unit * int(rng.integers(1, 768 // unit + 1))
+        T = int(rng.choice([int(rng.integers(1, 65)), int(rng.integers(65, 300)),
+                            int(rng.integers(300, 700))]))
+        out.append((T, d, ffn, E, k))
+    return out
+
+
+@pytest.mark.parametrize("shape", _random_shapes(), ids=lambda s: "x".join(map(str, s)))
+def test_forward_random_shapes(shape):
+    """The automatic kernel choice (streaming, split by rows, tiled with a
+    cut reduction) on seeded random shapes, every token against the oracle."""
+    say(f"[forward] random shape {shape} (auto: {B.moe_gemm_variant_for(*shape)})")
+    _forward_check(small_case(*shape, seed=31), variant=0)
+
+
 def test_forward_empty_experts():
     """A bias that sends every token to experts 2 and 5 leaves the rest idle."""
     say("[forward] empty experts")
