@@ -197,3 +197,21 @@ def oracle_out_fp8(c: Fp8Case, rows, gpu_ids_rows=None):
         gates = o.gates_for_ids(logits, ids)
     out = o.moe_apply_fp8(x, *c.weights(), ids, gates)
     return out, logits, ids, gates
+
+
+def random_shapes(n=16, seed=2408):
+    """Seeded draws over the supported space: E in 1..64, k in 1..min(E, 8),
+    d and ffn multiples of 64 up to 768 (every other draw multiples of 256,
+    which the tiled kernel takes), T from 1 to 699 in three bands."""
+    rng = np.random.default_rng(seed)
+    out = []
+    while len(out) < n:
+        E = int(rng.choice([1, 2, 3, 4, 6, 8, 12, 16, 32, 64]))
+        k = int(rng.integers(1, min(E, 8) + 1))
+        unit = 256 if len(out) % 2 else 64
+        d = unit * int(rng.integers(1, 768 // unit + 1))
+        ffn = unit * int(rng.integers(1, 768 // unit + 1))
+        T = int(rng.choice([int(rng.integers(1, 65)), int(rng.integers(65, 300)),
+                            int(rng.integers(300, 700))]))
+        out.append((T, d, ffn, E, k))
+    return out

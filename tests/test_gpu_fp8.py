@@ -11,7 +11,7 @@ import pytest
 import torch
 
 from gpu_common import (DEV, bf16_to_f64, fp8_small_case, fp8_workload_case, gpu_forward_fp8,
-                        gpu_route, orc, oracle_out_fp8, say)
+                        gpu_route, orc, oracle_out_fp8, random_shapes, say)
 from parity import OUT_TOL, check_routing, rowwise_rel
 from paper_2408_00008_amd import binding as B
 
@@ -109,6 +109,14 @@ def test_fp8_forward_tiled_shapes(shape):
     c = fp8_small_case(*shape, seed=14)
     assert B.moe_gemm_variant_for(c.T, c.d, c.ffn, c.E, c.k) == 2
     _forward_check(c)
+
+
+@pytest.mark.parametrize("shape", random_shapes(10, seed=2409), ids=lambda s: "x".join(map(str, s)))
+def test_fp8_forward_random_shapes(shape):
+    """The automatic kernel choice with 8-bit weights on seeded random shapes,
+    every token against the oracle."""
+    say(f"[fp8 forward] random shape {shape} (auto: {B.moe_gemm_variant_for(*shape)})")
+    _forward_check(fp8_small_case(*shape, seed=32))
 
 
 @pytest.mark.parametrize("name", ["prefill_t4096_fp8", "mixed_t576_fp8"])

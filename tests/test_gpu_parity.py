@@ -5,7 +5,7 @@ import pytest
 import torch
 
 from gpu_common import (DEV, bf16_to_f64, gpu_forward, gpu_route, oracle_logits, oracle_out, orc,
-                        say, small_case, workload_case)
+                        random_shapes, say, small_case, workload_case)
 from parity import OUT_TOL, check_routing, rowwise_rel
 from paper_2408_00008_amd import binding as B
 from paper_2408_00008_amd import inputs
@@ -199,25 +199,7 @@ def test_forward_shapes(shape, variant):
     _forward_check(small_case(*shape, seed=13), variant=variant)
 
 
-def _random_shapes(n=16, seed=2408):
-    """Seeded draws over the supported space: E in 1..64, k in 1..min(E, 8),
-    d and ffn multiples of 64 up to 768 (every other draw multiples of 256,
-    which the tiled kernel takes), T from 1 to 699 in three bands."""
-    rng = np.random.default_rng(seed)
-    out = []
-    while len(out) < n:
-        E = int(rng.choice([1, 2, 3, 4, 6, 8, 12, 16, 32, 64]))
-        k = int(rng.integers(1, min(E, 8) + 1))
-        unit = 256 if len(out) % 2 else 64
-        d = unit * int(rng.integers(1, 768 // unit + 1))
-        ffn = unit * int(rng.integers(1, 768 // unit + 1))
-        T = int(rng.choice([int(rng.integers(1, 65)), int(rng.integers(65, 300)),
-                            int(rng.integers(300, 700))]))
-        out.append((T, d, ffn, E, k))
-    return out
-
-
-@pytest.mark.parametrize("shape", _random_shapes(), ids=lambda s: "x".join(map(str, s)))
+@pytest.mark.parametrize("shape", random_shapes(), ids=lambda s: "x".join(map(str, s)))
 def test_forward_random_shapes(shape):
     """The automatic kernel choice (streaming, split by rows, tiled with a
     cut reduction) on seeded random shapes, every token against the oracle."""
