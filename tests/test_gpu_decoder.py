@@ -58,6 +58,22 @@ def test_linear(T, K, N):
     assert err < 1e-5
 
 
+def _linear_shapes(n=10, seed=2410):
+    """Seeded (T, K, N): K and N multiples of 64 up to 2048, T from 1 to 1599;
+    the last two draws make 128+ output tiles of 256 x 256 (the tiled path)."""
+    rng = np.random.default_rng(seed)
+    out = [(int(rng.integers(1, 700)), 64 * int(rng.integers(1, 33)), 64 * int(rng.integers(1, 33)))
+           for _ in range(n - 2)]
+    out += [(int(rng.integers(1100, 1600)), 256 * int(rng.integers(1, 9)), 256 * int(rng.integers(28, 33)))
+            for _ in range(2)]
+    return out
+
+
+@pytest.mark.parametrize("T,K,N", _linear_shapes())
+def test_linear_random_shapes(T, K, N):
+    test_linear(T, K, N)
+
+
 @pytest.mark.parametrize("hq,hkv,page", [(4, 1, 16), (8, 2, 8), (32, 8, 16)])
 def test_rope_append(hq, hkv, page):
     say(f"[decoder] rope+append hq={hq} hkv={hkv} page={page}")
