@@ -86,8 +86,8 @@ def main():
     if args.copy_calibration_mib:
         return copy_calibration(args.copy_calibration_mib)
     if args.gpus != 1:
-        print(f"bench.py: this build runs on exactly one GPU (asked for --gpus {args.gpus}); "
-              "the MoE layer is measured at N=1 only", file=sys.stderr)
+        print(f"bench.py: the MoE layer is measured on exactly one GPU (asked for --gpus "
+              f"{args.gpus}); runs over several GPUs are not supported", file=sys.stderr)
         sys.exit(2)
 
     import numpy as np
