@@ -12,15 +12,22 @@
 //     through the dispatch permutation while loading (no separate permute);
 //   * DOWN scales each output row by its gate weight and scatters it to the
 //     row's (token, slot) position;
-//   * workgroups are persistent: one per CU, each walking a contiguous share
-//     of the (expert, weight block, token tile) items of its XCD.  Items are
-//     ordered expert, weight block, token tile, so the workgroups of one XCD
-//     work on the token tiles of a few weight blocks at a time and share both
-//     operands through that XCD's L2.  Per-expert tile counts are read from
-//     the device-side offsets: ragged row counts need no host synchronisation;
-//   * DOWN may cut each tile's reduction into 2 or 4 parts (items then ordered
-//     expert, part, weight block, token tile), chosen on the device from the
-//     tile count, when that evens out the rounds of the persistent grid.
+//   * workgroups are persistent: one per CU.  The items, ordered expert,
+//     weight block, token tile, are cut into 8 contiguous ranges, one per
+//     XCD, and the P workgroups of an XCD take the items of its range in
+//     turn (workgroup j: items j, j + P, j + 2P, ...), so at any time they
+//     work on the token tiles of a few weight blocks and share both operands
+//     through that XCD's L2.  Per-expert tile counts are read from the
+//     device-side offsets: ragged row counts need no host synchronisation;
+//   * DOWN may cut each tile's reduction into parts (a power of two up to
+//     the caller's limit; items then ordered expert, part, weight block,
+//     token tile), chosen on the device from the tile count by a cost model,
+//     where that evens out the rounds of the persistent grid;
+//   * 8-bit weights (E4M3 bytes, one f32 scale per weight row) are staged in
+//     LDS as bytes, widened to bf16 at the fragment reads, and their scales
+//     multiply the accumulators in the epilogue;
+//   * with null offsets the kernel takes one matrix of all rows (a dense
+//     projection).
 #include <type_traits>
 
 #include "common.hpp"
