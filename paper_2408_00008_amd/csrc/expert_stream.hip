@@ -11,7 +11,10 @@
 //     reduction dimension;
 //   * weights go straight from HBM into registers as the A operand of a
 //     16x16x32 bf16 MFMA (lane l reads 16 contiguous bytes of row l%16), one
-//     chunk of KC reduction elements ahead of the MFMAs that consume them;
+//     or two chunks of KC reduction elements ahead of the MFMAs that consume
+//     them (two or three register sets); 8-bit weights (E4M3 bytes, one f32
+//     scale per row) are widened to bf16 in registers and scaled in the
+//     epilogue;
 //   * the expert's token rows (<= 16*G per pass) are staged through LDS once
 //     per chunk and shared by the NS waves of a reduction share (B operand);
 //   * UP pairs waves: one streams 16 rows of w1, its partner the same rows of
@@ -25,7 +28,8 @@
 // Per-expert row counts come from the device-side offsets; experts with no
 // rows exit at once and no host synchronisation is needed.  An expert with
 // more than 16*G rows is cut into several passes over its slab, which run as
-// separate workgroups placed to share the slab's weights through L2.
+// separate workgroups placed to share the slab's weights through L2.  With
+// null offsets the kernels take one matrix of all rows (a dense projection).
 #include "common.hpp"
 #include "launch.hpp"
 
