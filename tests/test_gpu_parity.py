@@ -363,6 +363,21 @@ def test_forward_split_side_by_side_and_graph():
     c = small_case(256, 256, 2048, 8, 2, seed=37, bias=[2.0] + [0.0] * 7)
     assert B.moe_gemm_variant_for(c.T, c.d, c.ffn, c.E, c.k) == 3
     _forward_check(c, variant=0)
+    _graph_replays_match_eager(c)
+
+
+def test_forward_tiled_parts_graph():
+    """A prefill-regime step whose down GEMM is cut into 4 parts (the count
+    chosen and stored on the device, read by the combine): graph replays give
+    the bits of the eager runs, which match the oracle."""
+    say("[forward] tiled step with reduction parts: graph capture")
+    c = small_case(288, 256, 2048, 8, 2, seed=38)
+    assert B.moe_gemm_variant_for(c.T, c.d, c.ffn, c.E, c.k) == 2
+    _forward_check(c, variant=0)
+    _graph_replays_match_eager(c)
+
+
+def _graph_replays_match_eager(c):
     T, d, k = c.T, c.d, c.k
     ws = torch.empty(B.moe_workspace_size(T, d, c.ffn, c.E, k), dtype=torch.uint8, device=DEV)
     outs = [torch.empty(T, d, dtype=torch.float32, device=DEV) for _ in range(3)]
