@@ -119,6 +119,44 @@ def test_fp8_forward_random_shapes(shape):
     _forward_check(fp8_small_case(*shape, seed=32))
 
 
+@pytest.mark.parametrize("shape,bias", [
+    ((288, 256, 2048, 8, 2), None),                 # tiled, down cut into 4 parts
+    ((256, 256, 2048, 8, 2), [2.0] + [0.0] * 7),    # split: heavy expert tiled beside the rest
+])
+def test_fp8_forward_graph_replays(shape, bias):
+    """8-bit weights: graph replays of the step (with the workspace cleared in
+    between) give the bits of the eager runs, which match the oracle."""
+    say(f"[fp8 forward] graph capture {shape}")
+    c = fp8_small_case(*shape, seed=39, bias=bias)
+    _forward_check(c)
+    T, d, k = c.T, c.d, c.k
+    ws = torch.empty(B.moe_workspace_size(T, d, c.ffn, c.E, k), dtype=torch.uint8, device=DEV)
+    outs = [torch.empty(T, d, dtype=torch.float32, device=DEV) for _ in range(3)]
+
+    def step(o, s):
+        B.moe_forward_fp8_ex(c.x, c.router_w, c.w1q, c.w1s, c.w3q, c.w3s, c.w2q, c.w2s, k,
+                             out_f32=o, router_bias=c.router_bias, workspace=ws, stream=s)
+
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        step(outs[0], s)
+        step(outs[1], s)
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    assert torch.equal(outs[0], outs[1])
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=s):
+        step(outs[2], s)
+    for rep in range(3):
+        outs[2].fill_(7.0)
+        ws.zero_()
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(outs[2], outs[0]), rep
+
+
 @pytest.mark.parametrize("name", ["prefill_t4096_fp8", "mixed_t576_fp8"])
 def test_fp8_forward_tiled_sampled(name):
     say(f"[fp8 forward] {name} (sampled tokens)")
