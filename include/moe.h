@@ -108,7 +108,9 @@ moe_status_t moe_swiglu_up(const moe_bf16_t* x, const int32_t* perm,
                            int32_t k, moe_bf16_t* h, hipStream_t stream);
 
 /*
- * Second half of the expert FFN with the gate-weighted scatter fused in:
+ * Second half of the expert FFN with the gate-weighted scatter fused in
+ * (Sec. 4.1, the Mixtral experts of the served model: the W2 projection of
+ * each SwiGLU expert, then the gate-weighted sum of the k expert outputs):
  * for every expert e and row r of e, with a = perm[r]:
  *   y[a,i] = topk_w[a] * sum_n w2[e,i,n] h[r,n]        (f32, assignment order)
  * If topk_w or perm is NULL the plain result is written in row order instead:
@@ -121,7 +123,8 @@ moe_status_t moe_swiglu_down(const moe_bf16_t* h, const int32_t* expert_offsets,
                              hipStream_t stream);
 
 /*
- * moe_swiglu_down with its reduction over ffn cut into parts (the same sums:
+ * The W2 projection of the experts (Sec. 4.1, Mixtral's SwiGLU experts, as
+ * in moe_swiglu_down) with its reduction over ffn cut into parts (the same sums:
  * y of moe_swiglu_down = the sum of the slices written here), for prefill
  * sizes where the persistent tiled kernel runs (more than 64 rows per
  * expert on average) and a few hundred output tiles would leave its last
@@ -146,9 +149,10 @@ moe_status_t moe_swiglu_down_parts(const moe_bf16_t* h, const int32_t* expert_of
                                    hipStream_t stream);
 
 /*
- * The grouped SwiGLU expert FFN on permuted rows: moe_swiglu_up(x_perm,
- * perm = NULL) into h_ws, then moe_swiglu_down into y (same meaning of
- * topk_w / perm as there).
+ * The grouped SwiGLU expert FFN on permuted rows (Sec. 4.1, the experts of
+ * the Mixtral MoE layer the engine serves; Sec. 5, Mixtral-8x7B):
+ * moe_swiglu_up(x_perm, perm = NULL) into h_ws, then moe_swiglu_down into y
+ * (same meaning of topk_w / perm as there).
  * h_ws is caller scratch of T*k*ffn bf16.
  */
 moe_status_t moe_grouped_swiglu(const moe_bf16_t* x_perm, const int32_t* expert_offsets,
@@ -158,8 +162,10 @@ moe_status_t moe_grouped_swiglu(const moe_bf16_t* x_perm, const int32_t* expert_
                                 moe_bf16_t* h_ws, float* y, hipStream_t stream);
 
 /*
- * Gate-weighted un-permute/combine: slots of a token are summed in ascending j
- * in f32, after the optional residual:
+ * Gate-weighted un-permute/combine (Sec. 4.1, the Mixtral MoE layer: a
+ * token's output is the gate-weighted sum of its k experts' outputs; the
+ * residual add is the pre-norm block around the layer): slots of a token are
+ * summed in ascending j in f32, after the optional residual:
  *   s = (residual ? residual[t,i] : 0) + y[t*k+0,i] + ... + y[t*k+k-1,i]
  *   out[t,i] = bf16(s) (if out), out_f32[t,i] = s (if out_f32).
  * y [T*k,d] f32 in assignment order (already gate-weighted), residual/out_f32
@@ -170,7 +176,8 @@ moe_status_t moe_combine(const float* y, const float* residual, int64_t T, int32
                          moe_bf16_t* out, float* out_f32, hipStream_t stream);
 
 /*
- * moe_combine over the slices of moe_swiglu_down_parts: y [max_parts,T*k,d]
+ * The gate-weighted combine (Sec. 4.1, as in moe_combine) over the slices of
+ * moe_swiglu_down_parts: y [max_parts,T*k,d]
  * f32; each slot first sums its slices 0 .. n-1 in ascending order, with n =
  * *parts (device int32, read by the kernel, clamped to [1, max_parts]), then
  * the slots are summed as in moe_combine.
@@ -180,11 +187,20 @@ moe_status_t moe_combine_parts(const float* y, const int32_t* parts, int32_t max
                                moe_bf16_t* out, float* out_f32, hipStream_t stream);
 
 /*
- * The whole layer: route -> SwiGLU experts (the gather of token rows is fused
+ * The whole MoE FFN layer of the served model (Sec. 4.1, "Optimize Inference
+ * Engine": the engine work targets Mixture-of-Experts models; Sec. 5:
+ * Mixtral-8x7B, up to 256 concurrent requests per step under continuous
+ * batching): route -> SwiGLU experts (the gather of token rows is fused
  * into the first expert GEMM) -> combine.  out [T,d] bf16, must not overlap
  * any input.  Scratch is owned by the library, cached per device and grown on
  * demand (a growth is refused with MOE_ERR_NO_MEMORY while `stream` is being
- * captured into a graph; call once outside capture first).  Every call on one
+ * captured into a graph; call once outside capture first).  A buffer that was
+ * handed to a call under capture is kept alive when a later call grows the
+ * scratch, so graphs captured earlier stay valid (until
+ * moe_release_workspace).  The environment variable MOE_WORKSPACE_LIMIT_BYTES
+ * (a decimal byte count, read on every call) caps each library-owned scratch
+ * buffer: a call that needs more returns MOE_ERR_NO_MEMORY before any HIP
+ * call (an unparsable value gives MOE_ERR_INVALID_ARG).  Every call on one
  * device shares that scratch, so calls on different streams of one device
  * must not overlap in time; give each stream its own caller workspace
  * (moe_forward_ex) to run them concurrently.
@@ -201,7 +217,9 @@ moe_status_t moe_forward(const moe_bf16_t* x, const moe_bf16_t* router_w, const 
                          int32_t ffn, int32_t E, int32_t k, moe_bf16_t* out, hipStream_t stream);
 
 /*
- * moe_forward with the options of a residual block:
+ * moe_forward with the options of a residual block (Sec. 4.1 and Sec. 5: the
+ * MoE layer inside Mixtral's pre-norm decoder layer, whose residual stream
+ * the caller keeps in f32):
  *   router_bias  [E] f32 or NULL;
  *   residual     [T,d] f32 or NULL, added before rounding (see moe_combine);
  *   out          [T,d] bf16 or NULL; out_f32 [T,d] f32 or NULL (at least one;
@@ -334,6 +352,15 @@ moe_status_t moe_attention_decode(const moe_bf16_t* q, const moe_bf16_t* k_cache
                                   const int32_t* ctx, int64_t T, int32_t Hq, int32_t Hkv,
                                   int32_t hd, int32_t page, int32_t maxp, int64_t npages,
                                   float scale, moe_bf16_t* out, hipStream_t stream);
+
+/*
+ * Frees the library-owned scratch of the current device (moe_forward's and
+ * moe_attention_decode's, and buffers kept alive for captured graphs) after
+ * waiting for all work on the device.  Graphs captured earlier whose calls
+ * used the library scratch must not be replayed afterwards; the next call
+ * allocates again.  Not while a stream of the device is being captured.
+ */
+moe_status_t moe_release_workspace(void);
 
 /* Bytes of scratch moe_forward_ex needs for these sizes (0 for invalid sizes). */
 size_t moe_workspace_size(int64_t T, int32_t d, int32_t ffn, int32_t E, int32_t k);

@@ -27,6 +27,7 @@ EXPORTS = (
     "moe_swiglu_up_fp8", "moe_swiglu_down_fp8", "moe_swiglu_down_parts_fp8", "moe_forward_fp8_ex",
     "moe_linear", "moe_rope_kv_append", "moe_attention_decode",
     "moe_set_gemm_variant", "moe_gemm_variant_for", "moe_status_string", "moe_last_error", "moe_version",
+    "moe_release_workspace",
 )
 
 
@@ -91,6 +92,8 @@ def lib() -> ctypes.CDLL:
     L.moe_last_error.restype = ctypes.c_char_p
     L.moe_version.argtypes = []
     L.moe_version.restype = ctypes.c_int
+    L.moe_release_workspace.argtypes = []
+    L.moe_release_workspace.restype = ctypes.c_int
     _lib = L
     return L
 
@@ -302,3 +305,8 @@ def moe_gemm_variant_for(T, d, ffn, E, k) -> int:
 
 def moe_set_gemm_variant(v: int) -> int:
     return int(lib().moe_set_gemm_variant(v))
+
+
+def moe_release_workspace():
+    """Frees the library-owned scratch of the current device (after a device sync)."""
+    _check(lib().moe_release_workspace(), "moe_release_workspace")

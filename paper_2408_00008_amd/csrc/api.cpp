@@ -6,6 +6,9 @@
 #include <hip/hip_runtime.h>
 
 #include <atomic>
+#include <cerrno>
+#include <cstdint>
+#include <cstdlib>
 #include <cstdarg>
 #include <cstdio>
 #include <cmath>
@@ -208,37 +211,74 @@ Layout layout(int64_t T, int32_t d, int32_t ffn, int32_t E, int32_t k)
 struct DeviceScratch {
     void* ptr = nullptr;
     size_t bytes = 0;
+    // the buffer was handed to a call made while its stream was being
+    // captured: a graph may still replay with it, so a growth keeps it alive
+    // (retired) instead of freeing it
+    bool captured = false;
 };
 std::mutex g_ws_mu;
 // per device: slot 0 serves moe_forward / moe_forward_ex, slot 1 the
 // partial states of moe_attention_decode
 std::unordered_map<int, DeviceScratch> g_ws[2];
+// per device: buffers replaced while a captured graph may still use them;
+// freed by moe_release_workspace only
+std::unordered_map<int, std::vector<void*>> g_retired;
+
+// Cap on each library-owned scratch buffer, in bytes, from the environment
+// variable MOE_WORKSPACE_LIMIT_BYTES (read on every call; unset or empty = no
+// cap).  A call that needs more returns MOE_ERR_NO_MEMORY before any HIP call.
+moe_status_t workspace_limit(size_t* limit)
+{
+    *limit = SIZE_MAX;
+    const char* s = std::getenv("MOE_WORKSPACE_LIMIT_BYTES");
+    if (!s || !*s) return MOE_OK;
+    char* end = nullptr;
+    errno = 0;
+    const unsigned long long v = std::strtoull(s, &end, 10);
+    if (end == s || *end != '\0' || errno == ERANGE || s[0] == '-')
+        return fail(MOE_ERR_INVALID_ARG, "MOE_WORKSPACE_LIMIT_BYTES='%s' is not a byte count", s);
+    *limit = static_cast<size_t>(v);
+    return MOE_OK;
+}
 
 moe_status_t library_workspace(size_t need_bytes, hipStream_t stream, void** out, int slot = 0)
 {
+    size_t limit = SIZE_MAX;
+    TRY(workspace_limit(&limit));
+    if (need_bytes > limit)
+        return fail(MOE_ERR_NO_MEMORY,
+                    "library scratch of %zu bytes needed, above MOE_WORKSPACE_LIMIT_BYTES=%zu "
+                    "(pass a caller workspace to moe_forward_ex instead)",
+                    need_bytes, limit);
     int dev = 0;
     hipError_t e = hipGetDevice(&dev);
     if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+    e = hipStreamIsCapturing(stream, &cs);
+    if (e != hipSuccess) return hip_fail(e, "hipStreamIsCapturing");
     std::lock_guard<std::mutex> lk(g_ws_mu);
     DeviceScratch& s = g_ws[slot][dev];
     if (s.bytes < need_bytes) {
-        hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
-        e = hipStreamIsCapturing(stream, &cs);
-        if (e != hipSuccess) return hip_fail(e, "hipStreamIsCapturing");
         if (cs != hipStreamCaptureStatusNone)
             return fail(MOE_ERR_NO_MEMORY,
                         "library scratch must grow to %zu bytes while the stream is being "
                         "captured; call once outside capture first",
                         need_bytes);
         if (s.ptr) {
-            // earlier work on any stream may still use the old buffer
-            e = hipDeviceSynchronize();
-            if (e != hipSuccess) return hip_fail(e, "hipDeviceSynchronize");
-            (void)hipFree(s.ptr);
+            if (s.captured) {
+                g_retired[dev].push_back(s.ptr);
+            } else {
+                // earlier work on any stream may still use the old buffer
+                e = hipDeviceSynchronize();
+                if (e != hipSuccess) return hip_fail(e, "hipDeviceSynchronize");
+                (void)hipFree(s.ptr);
+            }
             s.ptr = nullptr;
             s.bytes = 0;
+            s.captured = false;
         }
-        const size_t grow = need_bytes + need_bytes / 4;
+        size_t grow = need_bytes + need_bytes / 4;
+        if (grow > limit) grow = limit;
         e = hipMalloc(&s.ptr, grow);
         if (e != hipSuccess) {
             s.ptr = nullptr;
@@ -246,6 +286,7 @@ moe_status_t library_workspace(size_t need_bytes, hipStream_t stream, void** out
         }
         s.bytes = grow;
     }
+    if (cs != hipStreamCaptureStatusNone) s.captured = true;
     *out = s.ptr;
     return MOE_OK;
 }
@@ -1013,6 +1054,28 @@ moe_status_t moe_attention_decode(const moe_bf16_t* q, const moe_bf16_t* k_cache
                                                 scale, nsplit, static_cast<float*>(part), out,
                                                 stream);
     return e == hipSuccess ? ok() : hip_fail(e, "attention kernel launch");
+}
+
+moe_status_t moe_release_workspace(void)
+{
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    std::lock_guard<std::mutex> lk(g_ws_mu);
+    e = hipDeviceSynchronize();
+    if (e != hipSuccess) return hip_fail(e, "hipDeviceSynchronize");
+    for (auto& slot : g_ws) {
+        auto it = slot.find(dev);
+        if (it == slot.end()) continue;
+        if (it->second.ptr) (void)hipFree(it->second.ptr);
+        slot.erase(it);
+    }
+    auto rt = g_retired.find(dev);
+    if (rt != g_retired.end()) {
+        for (void* p : rt->second) (void)hipFree(p);
+        g_retired.erase(rt);
+    }
+    return ok();
 }
 
 int moe_gemm_variant_for(int64_t T, int32_t d, int32_t ffn, int32_t E, int32_t k)

@@ -28,6 +28,8 @@
 //     multiply the accumulators in the epilogue;
 //   * with null offsets the kernel takes one matrix of all rows (a dense
 //     projection).
+#include <atomic>
+#include <mutex>
 #include <type_traits>
 
 #include "common.hpp"
@@ -66,6 +68,8 @@ struct TiledParams {
 };
 
 int cu_count();
+
+constexpr int kMaxDevices = 64;
 
 // ---- four-wave schedule ------------------------------------------------------
 //
@@ -509,12 +513,22 @@ template <bool UP, bool F8>
 hipError_t run_q(const TiledParams& p, int64_t A, hipStream_t stream)
 {
     using C = QCfg<UP, F8>;
-    static bool attr_set = false;
-    if (!attr_set) {
-        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&q_kernel<UP, F8>),
-                                           hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS_BYTES);
-        if (e != hipSuccess) return e;
-        attr_set = true;
+    // the dynamic-LDS limit is set once per device and kernel instance; the
+    // flags are per device and set under a lock, so concurrent first calls
+    // from several threads or on several devices are safe
+    static std::atomic<bool> attr_set[kMaxDevices];
+    static std::mutex attr_mu;
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices || !attr_set[dev].load(std::memory_order_acquire)) {
+        std::lock_guard<std::mutex> lk(attr_mu);
+        if (dev < 0 || dev >= kMaxDevices || !attr_set[dev].load(std::memory_order_relaxed)) {
+            e = hipFuncSetAttribute(reinterpret_cast<const void*>(&q_kernel<UP, F8>),
+                                    hipFuncAttributeMaxDynamicSharedMemorySize, C::LDS_BYTES);
+            if (e != hipSuccess) return e;
+            if (dev >= 0 && dev < kMaxDevices) attr_set[dev].store(true, std::memory_order_release);
+        }
     }
     const int grid = q_grid<UP>(p.N, p.E, A, p.ksplit_max);
     q_kernel<UP, F8><<<static_cast<unsigned>(grid), C::THREADS, C::LDS_BYTES, stream>>>(p);
@@ -523,16 +537,16 @@ hipError_t run_q(const TiledParams& p, int64_t A, hipStream_t stream)
 
 int cu_count()
 {
-    static int cached[64] = {0};
+    static std::atomic<int> cached[kMaxDevices];
     int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
-    if (!cached[dev]) {
-        int n = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return 256;
+    int n = cached[dev].load(std::memory_order_relaxed);
+    if (!n) {
         if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
             n = 256;
-        cached[dev] = n;
+        cached[dev].store(n, std::memory_order_relaxed);
     }
-    return cached[dev];
+    return n;
 }
 
 }  // namespace

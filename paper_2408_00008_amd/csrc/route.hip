@@ -37,6 +37,12 @@ __device__ __forceinline__ bool ahead(const Cand& a, const Cand& b)
     return a.v > b.v || (a.v == b.v && a.i < b.i);
 }
 
+// The ranking key of a logit: a NaN (non-finite input, outside the defined
+// domain) ranks as -inf, so the order stays total, every selected id is a
+// real expert of this token, and the token's gates come out NaN instead of
+// its routing reaching other tokens' rows.
+__device__ __forceinline__ float rank_key(float v) { return v != v ? -INFINITY : v; }
+
 // TPB tokens per workgroup pass (EMAX * TPB <= 64): every 16-byte chunk of the
 // router rows is loaded once and multiplied with the TPB tokens' chunks, and
 // the (token, expert) partial sums are reduced together.  A sum's order does
@@ -151,7 +157,7 @@ __global__ __launch_bounds__(ROUTE_THREADS) void router_topk_kernel(
 #pragma unroll
                         for (int e = 0; e < EMAX; ++e) {
                             if (e < E && !(taken & (1u << e))) {
-                                const float le = lg[tid][e];
+                                const float le = rank_key(lg[tid][e]);
                                 // strict: an equal logit keeps the lower index
                                 if (best < 0 || le > bv) {
                                     best = e;
@@ -187,7 +193,7 @@ __global__ __launch_bounds__(ROUTE_THREADS) void router_topk_kernel(
         if (wave < nt) {
             const int64_t t = t0 + wave;
             Cand me;
-            me.v = lane < E ? lg[wave][lane] : -INFINITY;
+            me.v = lane < E ? rank_key(lg[wave][lane]) : -INFINITY;
             me.i = lane < E ? lane : 0x7fffffff;
             float selv[8];
             int seli[8];
@@ -247,7 +253,10 @@ __global__ __launch_bounds__(DISPATCH_THREADS) void dispatch_kernel(
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     if (tid < 64) cnt[tid] = 0;
     __syncthreads();
-    for (int64_t a = tid; a < A; a += DISPATCH_THREADS) atomicAdd(&cnt[ids[a]], 1);
+    // ids come from the router kernel and lie in [0, E); the clamp keeps a
+    // corrupted id from indexing past the histogram
+    auto expert_of = [&](int64_t a) { return min(max(ids[a], 0), E - 1); };
+    for (int64_t a = tid; a < A; a += DISPATCH_THREADS) atomicAdd(&cnt[expert_of(a)], 1);
     __syncthreads();
     if (wave == 0) {
         int c = lane < E ? cnt[lane] : 0;
@@ -267,7 +276,7 @@ __global__ __launch_bounds__(DISPATCH_THREADS) void dispatch_kernel(
     const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
     for (int64_t b0 = 0; b0 < A; b0 += DISPATCH_THREADS) {
         const int64_t a = b0 + tid;
-        const int e = a < A ? ids[a] : -1;
+        const int e = a < A ? expert_of(a) : -1;
         if (lane < 64) wcnt[wave][lane] = 0;
         // rank among lanes of this wave with the same expert
         int rank = 0;

@@ -287,3 +287,47 @@ def test_decoder_entry_points_reject(L):
     assert attn(scale=0.0) == B.MOE_ERR_INVALID_ARG
     assert attn(out=q + 16) == B.MOE_ERR_INVALID_ARG and b"overlaps q" in L.moe_last_error()
     assert attn(T=0) == B.MOE_OK
+
+
+@pytest.fixture
+def ws_limit():
+    """Sets MOE_WORKSPACE_LIMIT_BYTES for one test (the library reads it on
+    every call) and removes it afterwards."""
+    old = os.environ.get("MOE_WORKSPACE_LIMIT_BYTES")
+
+    def set_(v):
+        os.environ["MOE_WORKSPACE_LIMIT_BYTES"] = v
+
+    yield set_
+    if old is None:
+        os.environ.pop("MOE_WORKSPACE_LIMIT_BYTES", None)
+    else:
+        os.environ["MOE_WORKSPACE_LIMIT_BYTES"] = old
+
+
+def test_workspace_limit_forces_no_memory(L, ws_limit):
+    """A cap below what moe_forward needs returns MOE_ERR_NO_MEMORY after
+    validation and before any HIP call (so it runs here without a GPU); an
+    unparsable cap is an argument error."""
+    need = L.moe_workspace_size(4, 128, 256, 8, 2)
+    ws_limit(str(need - 1))
+    assert fwd(L) == B.MOE_ERR_NO_MEMORY
+    msg = L.moe_last_error().decode()
+    assert "MOE_WORKSPACE_LIMIT_BYTES" in msg and str(need) in msg
+    # the 8-bit forward shares the scratch and the cap
+    big = 1 << 40
+    st = L.moe_forward_fp8_ex(X, RW, None, big, 2 * big, 3 * big, 4 * big, 5 * big, 6 * big,
+                              4, 128, 256, 8, 2, None, 7 * big, None, None, 0, None)
+    assert st == B.MOE_ERR_NO_MEMORY
+    # a caller workspace is not capped (rejected here only for its size)
+    st = L.moe_forward_ex(X, RW, None, big, 2 * big, 3 * big, 4, 128, 256, 8, 2, None, 4 * big,
+                          None, 5 * big, need - 1, None)
+    assert st == B.MOE_ERR_NO_MEMORY and b"smaller than" in L.moe_last_error()
+    for bad in ("abc", "-5", "12kb", "99999999999999999999999"):
+        ws_limit(bad)
+        assert fwd(L) == B.MOE_ERR_INVALID_ARG, bad
+        assert b"not a byte count" in L.moe_last_error()
+    # validation still comes first
+    ws_limit("0")
+    assert fwd(L, E=65) == B.MOE_ERR_UNSUPPORTED
+    assert fwd(L, T=0) == B.MOE_OK
