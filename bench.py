@@ -41,9 +41,13 @@ def parse():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="decode_t64")
     ap.add_argument("--seed", type=int, default=0)
-    ap.add_argument("--cpu-seconds", type=float, default=12.0,
+    ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="target wall time of the oracle baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-prefill", action="store_true",
+                    help="decode_t64 only: skip the prefill_t4096 sub-record")
+    ap.add_argument("--prefill-steps", type=int, default=20,
+                    help="timed steps of the prefill_t4096 sub-record")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="only run a plain device copy of this many MiB (3 times), for "
                          "scaling rocprofv3 FETCH_SIZE/WRITE_SIZE counters")
@@ -90,21 +94,52 @@ def main():
               f"{args.gpus}); runs over several GPUs are not supported", file=sys.stderr)
         sys.exit(2)
 
+    import torch
+
+    from paper_2408_00008_amd import inputs
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    w = inputs.WORKLOADS[args.workload].replace(seed=args.seed)
+    if w.hq:
+        from paper_2408_00008_amd import decoder
+        rec, state = decoder.bench_decoder(args, w)
+        rec["cpu_baseline"] = None if args.no_cpu_baseline else cpu_baseline_decoder(args, w, *state)
+        print(json.dumps(rec), flush=True)
+        return
+    if w.layers != 1:
+        from paper_2408_00008_amd import stack
+        rec, st, x = stack.bench_stack(args, w)
+        rec["cpu_baseline"] = None if args.no_cpu_baseline else cpu_baseline_stack(args, w, st, x)
+        print(json.dumps(rec), flush=True)
+        return
+    rec, state = measure_layer(args, w, args.steps, args.warmup)
+    rec["cpu_baseline"] = None if args.no_cpu_baseline else cpu_baseline(args, w, *state)
+    del state
+    if args.workload == "decode_t64" and not args.no_prefill:
+        # the metric's second half: the 4096-token prefill chunk against the
+        # bf16 MFMA peak, measured in the same run
+        pw = inputs.WORKLOADS["prefill_t4096"].replace(seed=args.seed)
+        sub, pstate = measure_layer(args, pw, args.prefill_steps, args.warmup)
+        sub["cpu_baseline"] = None if args.no_cpu_baseline else cpu_baseline(args, pw, *pstate)
+        del pstate
+        for key in ("metric", "n_gpus", "higher_is_better", "scaling", "vs_baseline", "dtype",
+                    "data"):
+            sub.pop(key, None)
+        rec["prefill_t4096"] = sub
+    print(json.dumps(rec), flush=True)
+
+
+def measure_layer(args, w, steps, warmup):
+    """Times `steps` whole-layer steps of workload w (after `warmup`) and
+    returns the bench record (without the CPU baseline) and the inputs the
+    baseline reuses."""
     import numpy as np
     import torch
 
     from paper_2408_00008_amd import binding as B
     from paper_2408_00008_amd import inputs
 
-    assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = "cuda:0"
-    w = inputs.WORKLOADS[args.workload].replace(seed=args.seed)
-    if w.hq:
-        from paper_2408_00008_amd import decoder
-        return decoder.bench_decoder(args, w)
-    if w.layers != 1:
-        from paper_2408_00008_amd import stack
-        return stack.bench_stack(args, w)
     T, d, ffn, E, k = w.T, w.d, w.ffn, w.E, w.k
     A = T * k
     x = inputs.make_x(w, dev)
@@ -161,71 +196,74 @@ def main():
         else:
             B.moe_combine(y[0], T, d, k, out=out, stream=stream)
 
-    for _ in range(args.warmup):
+    for _ in range(warmup):
         step()
     torch.cuda.synchronize()
 
     evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-           for _ in range(args.steps)]
+           for _ in range(steps)]
     # one event at every step boundary: the first and last bracket the timed
     # region, the ones between give the per-step spread
-    bounds = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    bounds = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
     torch.cuda.synchronize()
     wall0 = time.perf_counter()
     bounds[0].record(stream)
-    for i in range(args.steps):
+    for i in range(steps):
         step(*evs[i])
         bounds[i + 1].record(stream)
     torch.cuda.synchronize()
     wall1 = time.perf_counter()
     ms_total = bounds[0].elapsed_time(bounds[-1])
-    step_ms = np.array([bounds[i].elapsed_time(bounds[i + 1]) for i in range(args.steps)])
-    ms_per_step = ms_total / args.steps
+    step_ms = np.array([bounds[i].elapsed_time(bounds[i + 1]) for i in range(steps)])
+    ms_per_step = ms_total / steps
     up_ms = sorted(e0.elapsed_time(e1) for e0, e1 in evs)
     up_avg_ms = sum(up_ms) / len(up_ms)
 
     counts = np.diff(offs.cpu().numpy())
     active = int((counts > 0).sum())
     # algorithmic work of the up kernel: each active expert's w1 and w3 once
-    # (bf16, or E4M3 bytes plus one f32 scale per row), the routed token rows
-    # read once, h written once; 4*d*ffn FLOP per row
+    # (bf16, or E4M3 bytes plus one f32 scale per row) and the routed token
+    # rows read once; 4*d*ffn FLOP per row.  h is an intermediate and not
+    # counted.
     scale_bytes = 4 if w.fp8 else 0
-    up_bytes = (active * 2 * ffn * (d * wbytes_per_elem + scale_bytes) + A * d * 2
-                + A * ffn * 2)
+    up_bytes = active * 2 * ffn * (d * wbytes_per_elem + scale_bytes) + A * d * 2
     up_flops = 4.0 * A * d * ffn
     kernel = "expert_up_" + variant
+    layer_flops = 2.0 * T * d * E + 6.0 * A * d * ffn
+    layer_bytes = (active * (3 * ffn * d * wbytes_per_elem + (2 * ffn + d) * scale_bytes)
+                   + E * d * 2 + T * d * 2 * 2)
+    layer_s = ms_per_step * 1e-3
     if variant in ("stream", "split"):
-        # split: experts of up to 64 rows stream, heavier ones take a second
-        # launch; both sit between the same two events
+        # HBM-bound (split: experts of up to 64 rows stream, heavier ones take
+        # a second launch; both sit between the same two events)
         achieved = up_bytes / (up_avg_ms * 1e-3) / 1e9
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                 "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4)}
+        lach = layer_bytes / layer_s / 1e9
+        layer_roof = {"bound": "hbm", "achieved": round(lach, 1), "peak": HBM_PEAK_GBS,
+                      "unit": "GB/s", "frac": round(lach / HBM_PEAK_GBS, 4)}
     else:
         achieved = up_flops / (up_avg_ms * 1e-3) / 1e12
         roof = {"bound": "mfma", "achieved": round(achieved, 1), "peak": BF16_PEAK_TFLOPS,
                 "unit": "TFLOP/s", "frac": round(achieved / BF16_PEAK_TFLOPS, 4)}
-    roof["traffic"] = load_traffic(args.workload, kernel, variant)
+        lach = layer_flops / layer_s / 1e12
+        layer_roof = {"bound": "mfma", "achieved": round(lach, 1), "peak": BF16_PEAK_TFLOPS,
+                      "unit": "TFLOP/s", "frac": round(lach / BF16_PEAK_TFLOPS, 4)}
+    roof["traffic"] = load_traffic(w.name, kernel, variant)
     roof["kernel"] = kernel
     roof["avg_launch_us"] = round(up_avg_ms * 1e3, 2)
     roof["algorithmic_bytes_per_launch"] = up_bytes
     roof["algorithmic_flop_per_launch"] = up_flops
-
-    layer_flops = 2.0 * T * d * E + 6.0 * A * d * ffn
-    layer_bytes = (active * (3 * ffn * d * wbytes_per_elem + (2 * ffn + d) * scale_bytes)
-                   + E * d * 2 + T * d * 2 * 2)
-    tok_s = T * args.steps / (ms_total * 1e-3)
-
-    cpu = None
-    if not args.no_cpu_baseline:
-        cpu = cpu_baseline(args, w, x, lay, T)
+    layer_roof["scope"] = "whole layer step (route, up, down, combine)"
+    tok_s = T * steps / (ms_total * 1e-3)
 
     rec = {
         "metric": "MoE-layer tokens/s",
         "value": round(tok_s, 1),
         "unit": "tokens/s",
         "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
+        "steps": steps,
+        "warmup": warmup,
         "ms_per_step": round(ms_per_step, 4),
         "step_ms_p10_p50_p90": [round(float(np.percentile(step_ms, q)), 4) for q in (10, 50, 90)],
         "higher_is_better": True,
@@ -233,36 +271,73 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16",  # MFMA operands; E4M3 weights are widened exactly to bf16
         "data": "synthetic (seeded normals of the Mixtral-8x7B layer shapes; no dataset, random weights)",
-        "config": {"workload": args.workload, "T": T, "d": d, "ffn": ffn, "E": E, "k": k,
+        "config": {"workload": w.name, "T": T, "d": d, "ffn": ffn, "E": E, "k": k,
                    "expert_weights": "e4m3 + f32 row scale" if w.fp8 else "bf16",
                    "router_bias0": w.bias0, "seed": args.seed, "active_experts": active,
                    "rows_per_expert": counts.tolist(),
                    "down_reduction_parts": int(parts.item()) if cut else 1},
-        "layer": {"tflops": round(layer_flops / (ms_per_step * 1e-3) / 1e12, 2),
-                  "gbs": round(layer_bytes / (ms_per_step * 1e-3) / 1e9, 1),
-                  "hbm_frac": round(layer_bytes / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
-                  "mfma_frac": round(layer_flops / (ms_per_step * 1e-3) / 1e12 / BF16_PEAK_TFLOPS, 4),
+        "layer": {"tflops": round(layer_flops / layer_s / 1e12, 2),
+                  "gbs": round(layer_bytes / layer_s / 1e9, 1),
+                  "hbm_frac": round(layer_bytes / layer_s / 1e9 / HBM_PEAK_GBS, 4),
+                  "mfma_frac": round(layer_flops / layer_s / 1e12 / BF16_PEAK_TFLOPS, 4),
                   "algorithmic_bytes": layer_bytes, "algorithmic_flop": layer_flops},
         "roofline": roof,
-        "cpu_baseline": cpu,
+        "layer_roofline": layer_roof,
+        "cpu_baseline": None,
         "wall_s_timed": round(wall1 - wall0, 3),
     }
-    print(json.dumps(rec), flush=True)
+    return rec, (x, lay, T)
+
+
+def _oracle():
+    """The fp64 oracle with one OpenMP thread per host core this process may use."""
+    from oracle import oracle as oracle_mod
+
+    o = oracle_mod.get()
+    cores = len(os.sched_getaffinity(0))
+    cores = min(cores, int(os.environ.get("OMP_NUM_THREADS", cores)))
+    o.threads(cores)
+    return o
+
+
+def _cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for ln in f:
+                if ln.startswith("model name"):
+                    return ln.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return ""
+
+
+def _sample_rate(fn, T, seconds):
+    """Runs fn(n) on the first n tokens, n = T when a whole pass fits the
+    time budget, else the count a probe on 8 tokens says fits; repeats until
+    about `seconds` of wall time.  Returns (tokens, seconds, passes, n)."""
+    S = T
+    t0 = time.perf_counter()
+    fn(min(T, 8))
+    probe = time.perf_counter() - t0
+    if T > 8 and probe * T / 8 > 3 * seconds:
+        S = max(8, int(8 * seconds / probe))
+    tokens, el, reps = 0, 0.0, 0
+    while el < seconds and reps < 1000:
+        t0 = time.perf_counter()
+        fn(S)
+        el += time.perf_counter() - t0
+        tokens += S
+        reps += 1
+    return tokens, el, reps, S
 
 
 def cpu_baseline(args, w, x, lay, T):
     """The fp64 oracle, as it is, on this host: whole layers of the same
     workload (all T tokens when that fits the time budget, else the first
     tokens), repeated until about --cpu-seconds of wall time."""
-    import numpy as np
-
-    from oracle import oracle as oracle_mod
     from paper_2408_00008_amd import inputs
 
-    o = oracle_mod.get()
-    cores = len(os.sched_getaffinity(0))
-    cores = min(cores, int(os.environ.get("OMP_NUM_THREADS", cores)))
-    o.threads(cores)
+    o = _oracle()
     xb = inputs.bf16_bits(x)
     rwb = inputs.bf16_bits(lay["router_w"])
     bias = None if lay["router_bias"] is None else lay["router_bias"].cpu().numpy()
@@ -276,35 +351,76 @@ def cpu_baseline(args, w, x, lay, T):
 
         def layer(n):
             o.moe_layer(xb[:n], rwb, *ws, w.k, bias)
-    S = T
-    # probe with a small slice, then size the sample
-    t0 = time.perf_counter()
-    layer(min(T, 8))
-    probe = time.perf_counter() - t0
-    if T > 8 and probe * T / 8 > 3 * args.cpu_seconds:
-        S = max(8, int(8 * args.cpu_seconds / probe))
-    tokens, el, reps = 0, 0.0, 0
-    while el < args.cpu_seconds and reps < 1000:
-        t0 = time.perf_counter()
-        layer(S)
-        el += time.perf_counter() - t0
-        tokens += S
-        reps += 1
-    model = ""
-    try:
-        with open("/proc/cpuinfo") as f:
-            for ln in f:
-                if ln.startswith("model name"):
-                    model = ln.split(":", 1)[1].strip()
-                    break
-    except OSError:
-        pass
-    del np
+    tokens, el, reps, S = _sample_rate(layer, T, args.cpu_seconds)
     return {"value": round(tokens / el, 3), "unit": "tokens/s", "cores": o.threads(),
             "kind": "oracle",
             "sample": f"{reps} x full fp64 layer over the first {S} of {T} tokens of "
-                      f"{args.workload} ({el:.1f} s wall)",
-            "cpu_model": model}
+                      f"{w.name} ({el:.1f} s wall)",
+            "cpu_model": _cpu_model()}
+
+
+def cpu_baseline_stack(args, w, st, x):
+    """The oracle on the stack workload: layer 0 of the stack (RMSNorm of the
+    residual stream, rounding to bf16, the fp64 MoE layer) on this host;
+    every layer does the same work, so the 32-layer step's rate is the
+    layer's divided by the layer count."""
+    from paper_2408_00008_amd import inputs
+
+    o = _oracle()
+    lay = st.layers[0]
+    h = x.float().cpu().numpy()
+    gamma = inputs.bf16_bits(lay["gamma"])
+    wb = [inputs.bf16_bits(lay[n]) for n in ("router_w", "w1", "w3", "w2")]
+
+    def layer(n):
+        a = o.round_bf16(o.rmsnorm(h[:n], gamma, w.eps))
+        o.moe_layer(a, *wb, w.k)
+
+    tokens, el, reps, S = _sample_rate(layer, w.T, args.cpu_seconds)
+    return {"value": round(tokens / el / st.L, 4), "unit": "tokens/s", "cores": o.threads(),
+            "kind": "oracle",
+            "sample": f"{reps} x layer 0 of {st.L} (RMSNorm + fp64 MoE layer) over the first {S} "
+                      f"of {w.T} tokens of {w.name} ({el:.1f} s wall); rate divided by {st.L} "
+                      f"layers",
+            "cpu_model": _cpu_model()}
+
+
+def cpu_baseline_decoder(args, w, layer, cache, page_table, pos, h):
+    """The oracle on a decoder workload: one decoder layer (RMSNorm, the
+    projections, RoPE, paged attention over the request's cached positions,
+    the output projection, RMSNorm and the fp64 MoE layer) on this host; for
+    a stack of layers the rate is divided by the layer count."""
+    from paper_2408_00008_amd import inputs
+
+    o = _oracle()
+    hq, hkv, hd = w.hq, w.hkv, w.hd
+    wqkv = inputs.bf16_bits(layer.wqkv)
+    wq, wk, wv = wqkv[:hq * hd], wqkv[hq * hd:(hq + hkv) * hd], wqkv[(hq + hkv) * hd:]
+    wo = inputs.bf16_bits(layer.wo)
+    ga, gm = inputs.bf16_bits(layer.gamma_attn), inputs.bf16_bits(layer.gamma_moe)
+    rw = inputs.bf16_bits(layer.router_w)
+    kc, vc = inputs.bf16_bits(cache[0]), inputs.bf16_bits(cache[1])
+    pt, ps = page_table.cpu().numpy(), pos.cpu().numpy()
+    hn = h.cpu().numpy()
+    if layer.fp8:
+        ex = {"fp8_experts": [t.cpu().numpy() for t in layer.q]}
+        w1 = w3 = w2 = None
+    else:
+        ex = {}
+        w1, w3, w2 = (inputs.bf16_bits(t) for t in (layer.w1, layer.w3, layer.w2))
+
+    def one(n):
+        o.decoder_layer(hn[:n], ga, wq, wk, wv, wo, kc, vc, pt[:n], ps[:n], gm, rw, w1, w3, w2,
+                        w.k, hq, hkv, w.theta, w.eps, **ex)
+
+    tokens, el, reps, S = _sample_rate(one, w.T, args.cpu_seconds)
+    L = max(1, w.layers)
+    return {"value": round(tokens / el / L, 4), "unit": "tokens/s", "cores": o.threads(),
+            "kind": "oracle",
+            "sample": f"{reps} x one fp64 decoder layer over the first {S} of {w.T} requests of "
+                      f"{w.name} ({el:.1f} s wall)"
+                      + (f"; rate divided by {L} layers" if L > 1 else ""),
+            "cpu_model": _cpu_model()}
 
 
 if __name__ == "__main__":

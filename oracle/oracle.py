@@ -274,14 +274,16 @@ class Oracle:
         return out
 
     def decoder_layer(self, h, gamma_attn, wq, wk, wv, wo, k_cache, v_cache, page_table, pos,
-                      gamma_moe, wr, w1, w3, w2, k, hq, hkv, theta, eps):
+                      gamma_moe, wr, w1, w3, w2, k, hq, hkv, theta, eps, fp8_experts=None):
         """One decode step of a decoder layer for T tokens (one per request):
         h [T, d] float32 residual stream; projections bf16 bits (nn.Linear
         layout: wq [hq*hd, d], wk, wv [hkv*hd, d], wo [d, hq*hd]); the new
         token of request t sits at position pos[t] (pos[t] earlier positions
         are in the cache).  Returns the intermediates and the layer output
         h2 (float64); the caches passed in are not modified (copies with the
-        new entries are returned)."""
+        new entries are returned).  fp8_experts: (w1q, w1s, w3q, w3s, w2q, w2s)
+        to run the MoE block on 8-bit expert weights (then w1, w3, w2 are
+        unused)."""
         h = np.ascontiguousarray(h, dtype=np.float32)
         T, d = h.shape
         hd = wq.shape[0] // hq
@@ -309,7 +311,10 @@ class Oracle:
         # the residual stream is kept in float32 between the two blocks
         h1f = h1.astype(np.float32)
         a2 = self.round_bf16(self.rmsnorm(h1f, gamma_moe, eps))
-        moe = self.moe_layer(a2, wr, w1, w3, w2, k)
+        if fp8_experts is not None:
+            moe = self.moe_layer_fp8(a2, wr, *fp8_experts, k)
+        else:
+            moe = self.moe_layer(a2, wr, w1, w3, w2, k)
         h2 = h1f.astype(np.float64) + moe["out"]
         return {"a": a, "q": q, "k_new": kn, "v_new": vn, "k_cache": kc, "v_cache": vc,
                 "attn": o, "h1": h1, "a2": a2, "moe": moe, "h2": h2}

@@ -131,8 +131,9 @@ class DecoderStack:
 
 def bench_decoder_stack(args, w):
     """bench.py for a stack of decoder layers: one decode step of the whole
-    model (graph replays); prints one JSON line."""
-    import json
+    model (graph replays).  Returns the JSON record (its CPU baseline left
+    for bench.py) and what that baseline needs: the first layer, its cache,
+    the page table, positions and the residual stream."""
     import time
 
     import numpy as np
@@ -190,16 +191,17 @@ def bench_decoder_stack(args, w):
         "cpu_baseline": None,
         "wall_s_timed": round(wall, 3),
     }
-    print(json.dumps(rec), flush=True)
+    return rec, (st.layers[0], st.caches[0], st.page_table, st.pos, h)
 
 
 def bench_decoder(args, w):
     """bench.py for a decoder-layer workload: one decode step of the layer
-    for w.T requests; prints one JSON line.  Each step rewrites the same
-    cache slot and advances h, so every step does the same work."""
+    for w.T requests.  Each step rewrites the same cache slot and advances
+    h, so every step does the same work.  Returns the JSON record (its CPU
+    baseline left for bench.py) and the layer, cache, page table, positions
+    and residual stream that baseline needs."""
     if w.layers > 1:
         return bench_decoder_stack(args, w)
-    import json
     import time
 
     import numpy as np
@@ -293,4 +295,4 @@ def bench_decoder(args, w):
         "cpu_baseline": None,
         "wall_s_timed": round(wall, 3),
     }
-    print(json.dumps(rec), flush=True)
+    return rec, (layer, (kv["k_cache"], kv["v_cache"]), kv["page_table"], kv["pos"], h)

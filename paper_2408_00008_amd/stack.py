@@ -14,7 +14,6 @@ torch.cuda.CUDAGraph) so a 32-layer step is a single launch.
 
 from __future__ import annotations
 
-import json
 import time
 from typing import List, Optional
 
@@ -94,7 +93,9 @@ class MoeStack:
 
 
 def bench_stack(args, w: inputs.Workload):
-    """bench.py entry for the stack workload: graph-captured steps."""
+    """bench.py entry for the stack workload: graph-captured steps.  Returns
+    the JSON record (its CPU baseline left for bench.py to fill in), the
+    stack and its input."""
     HBM_PEAK_GBS = 8000.0
     dev = "cuda:0"
     st = MoeStack(w, dev)
@@ -152,4 +153,4 @@ def bench_stack(args, w: inputs.Workload):
         "cpu_baseline": None,
         "wall_s_timed": round(wall, 3),
     }
-    print(json.dumps(rec), flush=True)
+    return rec, st, x

@@ -10,8 +10,9 @@ import numpy as np
 import pytest
 import torch
 
-from gpu_common import (DEV, bf16_to_f64, fp8_small_case, fp8_workload_case, gpu_forward_fp8,
-                        gpu_route, orc, oracle_out_fp8, random_shapes, say)
+from gpu_common import (DEV, bf16_to_f64, fp8_small_case, fp8_workload_case, full_logits,
+                        full_reference, gpu_forward_fp8, gpu_route, orc, oracle_out_fp8,
+                        random_shapes, say)
 from parity import OUT_TOL, check_routing, rowwise_rel
 from paper_2408_00008_amd import binding as B
 
@@ -21,10 +22,16 @@ pytestmark = pytest.mark.gpu
 def _forward_check(c, rows=None):
     out = gpu_forward_fp8(c)
     ids, *_ = gpu_route(c)
-    rows = np.arange(c.T) if rows is None else np.asarray(rows)
     g_ids = ids.cpu().numpy()
-    ref, logits, *_ = oracle_out_fp8(c, rows, g_ids[rows])
-    check_routing(g_ids[rows], logits, c.k)
+    if rows is None:
+        rows = np.arange(c.T)
+        logits = full_logits(c, fp8=True)
+        check_routing(g_ids, logits, c.k)
+        ref, _ = full_reference(c, g_ids, fp8=True)
+    else:
+        rows = np.asarray(rows)
+        ref, logits, *_ = oracle_out_fp8(c, rows, g_ids[rows])
+        check_routing(g_ids[rows], logits, c.k)
     err = rowwise_rel(bf16_to_f64(out)[rows], ref)
     say(f"  {c.name} T={c.T}: rowwise rel {err:.3e} over {len(rows)} tokens")
     assert err < OUT_TOL
@@ -68,17 +75,15 @@ def test_fp8_stages_teacher_forced(shape):
     assert e_h < OUT_TOL and e_y < OUT_TOL and e_yp < OUT_TOL
 
 
-def test_fp8_forward_full():
-    say("[fp8 forward] decode_t64_fp8 (every token)")
-    _forward_check(fp8_workload_case("decode_t64_fp8"))
-
-
-def test_fp8_forward_skew_sampled():
-    say("[fp8 forward] decode_t256_skew_fp8 (sampled tokens)")
-    c = fp8_workload_case("decode_t256_skew_fp8")
-    rng = np.random.default_rng(12)
-    rows = np.unique(np.concatenate([[0, c.T - 1], rng.choice(c.T, 30, replace=False)]))
-    _forward_check(c, rows)
+@pytest.mark.parametrize("name", ["decode_t64_fp8", "decode_t256_skew_fp8", "prefill_t4096_fp8",
+                                  "mixed_t576_fp8"])
+def test_fp8_forward_full(name):
+    """Every token of each 8-bit workload the benchmark runs."""
+    say(f"[fp8 forward] {name} (every token)")
+    c = fp8_workload_case(name)
+    _forward_check(c)
+    del c
+    torch.cuda.empty_cache()
 
 
 @pytest.mark.parametrize("shape", [
@@ -155,15 +160,6 @@ def test_fp8_forward_graph_replays(shape, bias):
         g.replay()
         torch.cuda.synchronize()
         assert torch.equal(outs[2], outs[0]), rep
-
-
-@pytest.mark.parametrize("name", ["prefill_t4096_fp8", "mixed_t576_fp8"])
-def test_fp8_forward_tiled_sampled(name):
-    say(f"[fp8 forward] {name} (sampled tokens)")
-    c = fp8_workload_case(name)
-    rng = np.random.default_rng(13)
-    rows = np.unique(np.concatenate([[0, c.T - 1], rng.choice(c.T, 30, replace=False)]))
-    _forward_check(c, rows)
 
 
 @pytest.mark.parametrize("shape,bias0", [

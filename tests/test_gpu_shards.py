@@ -87,8 +87,8 @@ def test_tp_forward_share_equals_partial():
 
 def test_ep2_tp4_mixtral_decode():
     """EP2-TP4, the paper's best hybrid, on the Mixtral decode step: 8 shards
-    of 4 experts x 3584 hidden units at their real shape; sampled tokens."""
+    of 4 experts x 3584 hidden units at their real shape; every token."""
     say("[shards] EP2-TP4 decode_t64")
     c = workload_case("decode_t64")
     total, route = sharded_sum(c, 2, 4)
-    check_sum(c, total, route, rows=np.arange(0, c.T, 4))
+    check_sum(c, total, route)
