@@ -236,6 +236,27 @@ moe_status_t moe_forward_ex(const moe_bf16_t* x, const moe_bf16_t* router_w,
                             size_t workspace_bytes, hipStream_t stream);
 
 /*
+ * moe_forward_ex without a workspace, for callers that cannot allocate device
+ * memory: code under graph capture, tight serving loops, harnesses that
+ * forbid allocation.  The call allocates nothing (no hipMalloc, no stream or
+ * event creation: the heavy and light expert launches of a split step run in
+ * sequence on `stream`).  Its scratch is one fixed 64 MiB device array in the
+ * library, one copy per GPU, held from the library's load until the process
+ * ends; sizes whose moe_workspace_size exceeds 64 MiB (e.g. Mixtral shapes
+ * above about 512 tokens) return MOE_ERR_NO_MEMORY before anything is
+ * enqueued.  Every call on one GPU shares that GPU's array, which keeps the
+ * last call's contents: calls that overlap in time on one GPU (on different
+ * streams or host threads) race, and must be ordered by the caller.  Nothing
+ * in the array needs clearing between calls.  Arguments and results as
+ * moe_forward_ex (workspace omitted).
+ */
+moe_status_t moe_forward_noalloc(const moe_bf16_t* x, const moe_bf16_t* router_w,
+                                 const float* router_bias, const moe_bf16_t* w1,
+                                 const moe_bf16_t* w3, const moe_bf16_t* w2, int64_t T, int32_t d,
+                                 int32_t ffn, int32_t E, int32_t k, const float* residual,
+                                 moe_bf16_t* out, float* out_f32, hipStream_t stream);
+
+/*
  * 8-bit expert weights (Sec. 4.1, "Model Quantization": weights stored as
  * 8-bit floats; Sec. 5 serves an 8-bit quantized Mixtral-8x7B).  Each expert
  * matrix is held as OCP FP8 E4M3 bytes -- sign, 4 exponent bits with bias 7,

@@ -27,7 +27,7 @@ EXPORTS = (
     "moe_swiglu_up_fp8", "moe_swiglu_down_fp8", "moe_swiglu_down_parts_fp8", "moe_forward_fp8_ex",
     "moe_linear", "moe_rope_kv_append", "moe_attention_decode",
     "moe_set_gemm_variant", "moe_gemm_variant_for", "moe_status_string", "moe_last_error", "moe_version",
-    "moe_release_workspace",
+    "moe_release_workspace", "moe_forward_noalloc",
 )
 
 
@@ -65,6 +65,7 @@ def lib() -> ctypes.CDLL:
         "moe_combine_parts": [p, p, i32, p, i64, i32, i32, p, p, p],
         "moe_forward": [p, p, p, p, p, i64, i32, i32, i32, i32, p, p],
         "moe_forward_ex": [p, p, p, p, p, p, i64, i32, i32, i32, i32, p, p, p, p, sz, p],
+        "moe_forward_noalloc": [p, p, p, p, p, p, i64, i32, i32, i32, i32, p, p, p, p],
         "moe_rmsnorm": [p, p, i64, i32, f32, p, p],
         "moe_swiglu_up_fp8": [p, p, p, p, p, p, p, i64, i32, i32, i32, i32, p, p],
         "moe_swiglu_down_fp8": [p, p, p, p, p, p, i64, i32, i32, i32, i32, p, p],
@@ -225,6 +226,18 @@ def moe_forward_ex(x, router_w, w1, w3, w2, k, out=None, out_f32=None, router_bi
         _ptr(w1, bf16, "w1"), _ptr(w3, bf16, "w3"), _ptr(w2, bf16, "w2"), T, d, ffn, E, k,
         _ptr(residual, f32, "residual"), _ptr(out, bf16, "out"), _ptr(out_f32, f32, "out_f32"),
         _ptr(workspace, None, "workspace"), ws_bytes, _stream(stream)), "moe_forward_ex")
+
+
+def moe_forward_noalloc(x, router_w, w1, w3, w2, k, out=None, out_f32=None, router_bias=None,
+                        residual=None, stream=None):
+    """moe_forward_ex without a workspace: the library's fixed device scratch array."""
+    T, d = x.shape
+    E, ffn, _ = w1.shape
+    _check(lib().moe_forward_noalloc(
+        _ptr(x, bf16, "x"), _ptr(router_w, bf16, "router_w"), _ptr(router_bias, f32, "router_bias"),
+        _ptr(w1, bf16, "w1"), _ptr(w3, bf16, "w3"), _ptr(w2, bf16, "w2"), T, d, ffn, E, k,
+        _ptr(residual, f32, "residual"), _ptr(out, bf16, "out"), _ptr(out_f32, f32, "out_f32"),
+        _stream(stream)), "moe_forward_noalloc")
 
 
 def moe_swiglu_up_fp8(x, expert_offsets, w1q, w1s, w3q, w3s, T, k, h, perm=None, stream=None):

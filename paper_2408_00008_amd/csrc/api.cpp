@@ -409,13 +409,15 @@ SideStream* side_stream()
     return ss;
 }
 
+// side = false: the two launches run in sequence on `stream` (callers that
+// must not create the side stream's resources)
 template <class Light, class Heavy>
-hipError_t run_side_by_side(hipStream_t stream, Light light, Heavy heavy)
+hipError_t run_side_by_side(hipStream_t stream, Light light, Heavy heavy, bool side = true)
 {
     hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
     hipError_t e = hipStreamIsCapturing(stream, &cs);
     if (e != hipSuccess) return e;
-    SideStream* ss = cs == hipStreamCaptureStatusNone ? side_stream() : nullptr;
+    SideStream* ss = (side && cs == hipStreamCaptureStatusNone) ? side_stream() : nullptr;
     if (!ss) {
         e = light(stream);
         return e != hipSuccess ? e : heavy(stream);
@@ -438,7 +440,7 @@ bool split_by_rows(int64_t rows_max, int64_t A, int E)
            moe::resolve_variant(moe::VARIANT_AUTO, A, E) == moe::VARIANT_STREAM;
 }
 
-hipError_t run_up(const moe::UpArgs& a, int64_t T, hipStream_t stream)
+hipError_t run_up(const moe::UpArgs& a, int64_t T, hipStream_t stream, bool side = true)
 {
     const int64_t rmax = rows_bound(T, a.kslots);
     const bool tiled_ok = moe::tiled_supported(a.d, a.ffn);
@@ -449,7 +451,7 @@ hipError_t run_up(const moe::UpArgs& a, int64_t T, hipStream_t stream)
         if (tiled_ok)
             return run_side_by_side(
                 stream, [&](hipStream_t s) { return moe::launch_stream_up(light, kLightRows, s); },
-                [&](hipStream_t s) { return moe::launch_tiled_up(heavy, s); });
+                [&](hipStream_t s) { return moe::launch_tiled_up(heavy, s); }, side);
         hipError_t e = moe::launch_stream_up(light, kLightRows, stream);
         if (e != hipSuccess) return e;
         heavy.groups = 8;
@@ -464,7 +466,7 @@ hipError_t run_up(const moe::UpArgs& a, int64_t T, hipStream_t stream)
 // return *a.ksplit_out (stream-ordered) holds how many of them the combine
 // must sum; *sliced tells whether that may exceed 1.
 hipError_t run_down(const moe::DownArgs& a, int64_t T, int32_t k, hipStream_t stream,
-                    bool* sliced = nullptr)
+                    bool* sliced = nullptr, bool side = true)
 {
     if (sliced) *sliced = false;
     const bool parts = a.ksplit_out != nullptr;
@@ -490,7 +492,8 @@ hipError_t run_down(const moe::DownArgs& a, int64_t T, int32_t k, hipStream_t st
                                                   a.topk_w ? a.perm : nullptr, a.ffn / 64,
                                                   moe::tiled_down_grid(heavy) / 8, a.ksplit_max,
                                                   a.ksplit_out, s);
-                });
+                },
+                side);
         }
         hipError_t e = moe::launch_stream_down(light, kLightRows, stream);
         if (e != hipSuccess) return e;
@@ -597,11 +600,15 @@ moe_status_t swiglu_down_impl(const moe_bf16_t* h, const int32_t* expert_offsets
     return ok();
 }
 
+// scratch_fn (optional): supplies the scratch when workspace is NULL instead
+// of the library-owned buffer; the split launches then run in sequence on
+// `stream` (no side stream is created)
 moe_status_t forward_impl(const moe_bf16_t* x, const moe_bf16_t* router_w,
                           const float* router_bias, const ExpertWeights& w, int64_t T, int32_t d,
                           int32_t ffn, int32_t E, int32_t k, const float* residual,
                           moe_bf16_t* out, float* out_f32, void* workspace,
-                          size_t workspace_bytes, hipStream_t stream)
+                          size_t workspace_bytes, hipStream_t stream,
+                          moe::ScratchFn scratch_fn = nullptr)
 {
     TRY(check_Ek(E, k));
     TRY(check_T(T, k));
@@ -642,7 +649,13 @@ moe_status_t forward_impl(const moe_bf16_t* x, const moe_bf16_t* router_w,
     if (T == 0) return ok();
 
     void* base = workspace;
-    if (!base) TRY(library_workspace(L.total, stream, &base));
+    if (!base) {
+        if (scratch_fn)
+            TRY(static_cast<moe_status_t>(scratch_fn(L.total, &base)));
+        else
+            TRY(library_workspace(L.total, stream, &base));
+    }
+    const bool side = scratch_fn == nullptr;
     char* b = static_cast<char*>(base);
     int32_t* ids = reinterpret_cast<int32_t*>(b + L.ids);
     float* gw = reinterpret_cast<float*>(b + L.w);
@@ -659,7 +672,7 @@ moe_status_t forward_impl(const moe_bf16_t* x, const moe_bf16_t* router_w,
     if (e != hipSuccess) return hip_fail(e, "dispatch kernel launch");
     moe::UpArgs ua{x, perm, k, offs, w.w1, w.w3, h, A, d, ffn, E};
     ua.q1 = w.q1, ua.s1 = w.s1, ua.q3 = w.q3, ua.s3 = w.s3;
-    e = run_up(ua, T, stream);
+    e = run_up(ua, T, stream, side);
     if (e != hipSuccess) return hip_fail(e, "expert up kernel launch");
     moe::DownArgs da{h, offs, w.w2, gw, perm, y, A, d, ffn, E};
     da.q2 = w.q2, da.s2 = w.s2;
@@ -667,7 +680,7 @@ moe_status_t forward_impl(const moe_bf16_t* x, const moe_bf16_t* router_w,
     // the part count is only needed (and only written) where y has slices
     da.ksplit_out = L.nsplit > 1 ? reinterpret_cast<int*>(b + L.ns) : nullptr;
     bool sliced = false;
-    e = run_down(da, T, k, stream, &sliced);
+    e = run_down(da, T, k, stream, &sliced, side);
     if (e != hipSuccess) return hip_fail(e, "expert down kernel launch");
     e = moe::launch_combine(y, residual, T, d, k, out, out_f32, stream,
                             sliced ? da.ksplit_out : nullptr, L.nsplit);
@@ -694,6 +707,30 @@ ExpertWeights fp8_weights(const uint8_t* q1, const float* s1, const uint8_t* q3,
 }
 
 }  // namespace
+
+namespace moe {
+moe_status_t set_last_error(moe_status_t s, const char* fmt, ...)
+{
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_last_error = buf;
+    return s;
+}
+
+moe_status_t forward_fixed_scratch(const moe_bf16_t* x, const moe_bf16_t* router_w,
+                                   const float* router_bias, const moe_bf16_t* w1,
+                                   const moe_bf16_t* w3, const moe_bf16_t* w2, int64_t T,
+                                   int32_t d, int32_t ffn, int32_t E, int32_t k,
+                                   const float* residual, moe_bf16_t* out, float* out_f32,
+                                   hipStream_t stream, ScratchFn scratch_fn)
+{
+    return forward_impl(x, router_w, router_bias, bf16_weights(w1, w3, w2), T, d, ffn, E, k,
+                        residual, out, out_f32, nullptr, 0, stream, scratch_fn);
+}
+}  // namespace moe
 
 namespace {
 constexpr int kMaxHeads = 256, kMaxHd = 1024;

@@ -109,6 +109,10 @@ struct DownArgs {
 
 enum GemmVariant { VARIANT_AUTO = 0, VARIANT_STREAM = 1, VARIANT_TILED = 2 };
 
+// Supplies `bytes` of 256-byte aligned device scratch for one forward call,
+// or returns an error status (with its message set).
+typedef int (*ScratchFn)(size_t bytes, void** out);
+
 // Chooses the kernel family for these sizes (resolves VARIANT_AUTO).
 int resolve_variant(int requested, int64_t A, int E);
 

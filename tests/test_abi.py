@@ -331,3 +331,23 @@ def test_workspace_limit_forces_no_memory(L, ws_limit):
     ws_limit("0")
     assert fwd(L, E=65) == B.MOE_ERR_UNSUPPORTED
     assert fwd(L, T=0) == B.MOE_OK
+
+
+def test_noalloc_validates_then_refuses_large_sizes(L):
+    """moe_forward_noalloc validates like moe_forward_ex, then refuses sizes
+    beyond its fixed 64 MiB scratch array before any HIP call."""
+    big = 1 << 40
+    args = (X, RW, None, big, 2 * big, 3 * big)
+    st = L.moe_forward_noalloc(*args, 4, 128, 256, 65, 2, None, 4 * big, None, None)
+    assert st == B.MOE_ERR_UNSUPPORTED
+    st = L.moe_forward_noalloc(*args, 4, 128, 256, 8, 2, None, None, None, None)
+    assert st == B.MOE_ERR_INVALID_ARG and b"both NULL" in L.moe_last_error()
+    assert L.moe_forward_noalloc(*args, 0, 128, 256, 8, 2, None, 4 * big, None, None) == B.MOE_OK
+    T, d, ffn = 1024, 4096, 14336
+    need = L.moe_workspace_size(T, d, ffn, 8, 2)
+    assert need > 64 << 20
+    st = L.moe_forward_noalloc(X, RW, None, big, 2 * big, 3 * big, T, d, ffn, 8, 2, None, 4 * big,
+                               None, None)
+    assert st == B.MOE_ERR_NO_MEMORY
+    msg = L.moe_last_error().decode()
+    assert "fixed" in msg and str(need) in msg
