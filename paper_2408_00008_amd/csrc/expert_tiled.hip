@@ -132,6 +132,21 @@ __device__ __forceinline__ void wait_vmem()
 // s_waitcnt lgkmcnt(0) with vmcnt/expcnt at max
 __device__ __forceinline__ void wait_lds() { __builtin_amdgcn_s_waitcnt(0xC07F); }
 
+// f(integral_constant<int, i>) for i = 0 .. N-1, unrolled at compile time
+template <int I, int N, class F>
+__device__ __forceinline__ void static_for_from(F&& f)
+{
+    if constexpr (I < N) {
+        f(std::integral_constant<int, I>{});
+        static_for_from<I + 1, N>(f);
+    }
+}
+template <int N, class F>
+__device__ __forceinline__ void static_for(F&& f)
+{
+    static_for_from<0, N>(f);
+}
+
 template <bool UP, bool F8>
 __global__ __launch_bounds__(256) void q_kernel(TiledParams p)
 {
@@ -239,21 +254,24 @@ __global__ __launch_bounds__(256) void q_kernel(TiledParams p)
             bptr[i] = p.act + src * p.K + k0 * C::BK + lchunk[i & 1] * 8;
         }
         // bytes between a wave's consecutive weight loads (8 or 16 rows)
-        const int64_t astep = F8 ? (int64_t)16 * p.K : (int64_t)16 * p.K;
-        auto load_a = [&](int s, int i) {
-            unsigned char* st = ring + (s % 3) * C::ASLOT;
+        const int64_t astep = (int64_t)16 * p.K;
+        // the loads of step s into the ring slot at byte offset `slot`; steps
+        // past the last re-load the last step, so that the number of loads in
+        // flight, and with it every counter wait, is the same in every step
+        auto load_a = [&](int slot, int s, int i) {
             const int64_t ko = (int64_t)(s < kn ? s : kn - 1) * C::BK * (F8 ? 1 : 2) + i * astep;
             const int rows = F8 ? 16 : 8;
             __builtin_amdgcn_global_load_lds(
                 (const void __attribute__((address_space(1)))*)(aptr[F8 ? 0 : (i & 1)] + ko),
-                (void __attribute__((address_space(3)))*)(st + (64 * wave + rows * i) * C::AROWB), 16, 0, 0);
+                (void __attribute__((address_space(3)))*)(ring + slot + (64 * wave + rows * i) * C::AROWB),
+                16, 0, 0);
         };
-        auto load_b = [&](int s, int i) {
-            unsigned char* st = ring + C::B_OFF + (s & 1) * C::SLOT;
+        auto load_b = [&](int slot, int s, int i) {
             const int ko = (s < kn ? s : kn - 1) * C::BK;
             __builtin_amdgcn_global_load_lds(
                 (const void __attribute__((address_space(1)))*)(bptr[i] + ko),
-                (void __attribute__((address_space(3)))*)(st + (64 * wave + 8 * i) * C::ROWB), 16, 0, 0);
+                (void __attribute__((address_space(3)))*)(ring + C::B_OFF + slot + (64 * wave + 8 * i) * C::ROWB),
+                16, 0, 0);
         };
 
         // The tile body for NMT multiplied 32-token column blocks per wave
@@ -268,10 +286,11 @@ __global__ __launch_bounds__(256) void q_kernel(TiledParams p)
             constexpr int NMT = decltype(nmt_tag)::value;
             const int b_wave = wm * NMT * 32 * C::ROWB;
             // token rows [0, 64 NMT) are multiplied: wave w loads rows
-            // [64w, 64w + 64), so waves w >= NMT skip their token loads.  Their
-            // memory-counter waits stay exact: the A loads they still issue
-            // are the ones each wait leaves in flight.
-            const bool bload = wave < NMT;
+            // [64w, 64w + 64), so waves w >= NMT skip their token loads (in a
+            // full tile every wave loads, with no branch).  The counter waits
+            // stay exact for them: the loads younger than the ones a wait is
+            // for are A loads, which every wave issues.
+            const bool bload = NMT == 4 || wave < NMT;
             floatx16 acc[NT][NMT];
     #pragma unroll
             for (int i = 0; i < NT; ++i)
@@ -287,27 +306,28 @@ __global__ __launch_bounds__(256) void q_kernel(TiledParams p)
             // global->LDS loads, and it then waits for all of them (vmcnt(0))
             // before each read.
             u32x4 fq[NT][2];
-            // fragment f (0-3: weight tiles, 4-7: token tiles) of k-step ks of step s
-            auto fread1 = [&](int s, int ks, int slot, int f) {
-                if (f >= NT + NMT) return;  // token tile not multiplied in this variant
+            // ring slots (byte offsets) of A(j), A(j+1), A(j+2) and of B(j),
+            // B(j+1) during step j; they rotate at the end of every step
+            int sa0 = 0, sa1 = C::ASLOT, sa2 = 2 * C::ASLOT;
+            int sb0 = 0, sb1 = C::SLOT;
+            // fragment f (0 .. NT-1: weight tiles, NT ..: token tiles) of
+            // k-step ks from the A slot as / B slot bs
+            auto fread1 = [&](int as, int bs, int ks, int slot, int f) {
                 if (f < NT) {
-                    const unsigned char* sa = ring + (s % 3) * C::ASLOT + a_wave + xk[ks];
-                    fa[slot][f] = *reinterpret_cast<const bf16x8*>(sa + atile(f));
+                    fa[slot][f] = *reinterpret_cast<const bf16x8*>(ring + as + a_wave + xk[ks] + atile(f));
                 } else {
-                    const unsigned char* sb = ring + C::B_OFF + (s & 1) * C::SLOT + b_wave + xk[ks];
-                    fb[slot][f - NT] = *reinterpret_cast<const bf16x8*>(sb + (f - NT) * 32 * C::ROWB);
+                    fb[slot][f - NT] = *reinterpret_cast<const bf16x8*>(
+                        ring + C::B_OFF + bs + b_wave + xk[ks] + (f - NT) * 32 * C::ROWB);
                 }
             };
-            // 8-bit weights: token fragment m of k-step ks of step s, and the
-            // raw weight bytes of k-step pair q of step s for tile nt
-            auto fread_b = [&](int s, int ks, int slot, int m) {
-                if (m >= NMT) return;
-                const unsigned char* sb = ring + C::B_OFF + (s & 1) * C::SLOT + b_wave + xk[ks];
-                fb[slot][m] = *reinterpret_cast<const bf16x8*>(sb + m * 32 * C::ROWB);
+            // 8-bit weights: token fragment m of k-step ks, and the raw weight
+            // bytes of k-step pair q for tile nt
+            auto fread_b = [&](int bs, int ks, int slot, int m) {
+                fb[slot][m] = *reinterpret_cast<const bf16x8*>(ring + C::B_OFF + bs + b_wave + xk[ks] +
+                                                               m * 32 * C::ROWB);
             };
-            auto fread_q = [&](int s, int q, int nt) {
-                const unsigned char* sa = ring + (s % 3) * C::ASLOT + a_wave + xa[q];
-                fq[nt][q] = *reinterpret_cast<const u32x4*>(sa + atile(nt));
+            auto fread_q = [&](int as, int q, int nt) {
+                fq[nt][q] = *reinterpret_cast<const u32x4*>(ring + as + a_wave + xa[q] + atile(nt));
             };
             auto fence = [] { __builtin_amdgcn_sched_barrier(0); };
 
@@ -327,89 +347,117 @@ __global__ __launch_bounds__(256) void q_kernel(TiledParams p)
                 }
             }
 
-            // prologue: A(0), B(0), A(1), as the steady state would have issued
-            // them; A(0) and B(0) complete everywhere
+            // Prologue: A(0), A(1), B(0), B(1) -- the loads the steady state
+            // keeps ahead -- then A(0) and B(0) complete everywhere and the
+            // fragments of k-step 0 are read.
     #pragma unroll
-            for (int i = 0; i < LA; ++i) load_a(0, i);
+            for (int i = 0; i < LA; ++i) load_a(sa0, 0, i);
+    #pragma unroll
+            for (int i = 0; i < LA; ++i) load_a(sa1, 1, i);
             if (bload) {
     #pragma unroll
-                for (int i = 0; i < L; ++i) load_b(0, i);
-            }
+                for (int i = 0; i < L; ++i) load_b(sb0, 0, i);
     #pragma unroll
-            for (int i = 0; i < LA; ++i) load_a(1, i);
-            wait_vmem<LA>();
+                for (int i = 0; i < L; ++i) load_b(sb1, 1, i);
+                wait_vmem<L>();
+            } else {
+                wait_vmem<LA>();
+            }
             fence();
             __builtin_amdgcn_s_barrier();
             fence();
             if constexpr (F8) {
     #pragma unroll
-                for (int nt = 0; nt < NT; ++nt) fread_q(0, 0, nt);
+                for (int nt = 0; nt < NT; ++nt) fread_q(sa0, 0, nt);
     #pragma unroll
-                for (int m = 0; m < NMT; ++m) fread_b(0, 0, 0, m);
+                for (int m = 0; m < NMT; ++m) fread_b(sb0, 0, 0, m);
             } else {
     #pragma unroll
-                for (int f = 0; f < NT + NMT; ++f) fread1(0, 0, 0, f);
+                for (int f = 0; f < NT + NMT; ++f) fread1(sa0, sb0, 0, 0, f);
             }
 
-            // step j: k-step ks multiplies fragments slot ks & 1 while the other
-            // slot receives the next k-step's fragments (in k-step 3: k-step 0 of
-            // step j+1).  Loads: B(j+1) in k-step 0, A(j+2) in k-steps 1 and 2
-            // (8-bit weights: k-step 1).  8-bit weight bytes are read a pair of
-            // k-steps at a time (k-step 0: pair 1 of step j; k-step 3: pair 0
-            // of step j+1) and widened to bf16 just before their MFMAs.  After
-            // k-step 2 every wave waits for its reads of step j's last
-            // fragments and for its loads up to B(j+1), then one barrier makes
-            // A(j+1), B(j+1) complete and frees the slots of A(j), B(j).
+            // Step j, k-step ks: its NT x NMT MFMAs use the fragments in
+            // register slot ks & 1, and one memory operation follows each of
+            // the first MFMAs (several where a k-step has more memory
+            // operations than MFMAs): first the
+            // reads of the next k-step's fragments into the other slot (so they
+            // are complete long before that k-step starts), then this
+            // k-step's share of the loads: A(j+2) in k-steps 0 and 1, B(j+2) in
+            // k-step 3.  8-bit weights read their raw bytes a pair of k-steps
+            // at a time (k-step 0: pair 1 of step j; k-step 3: pair 0 of step
+            // j+1) and widen them to bf16 before the MFMAs of each weight tile.
+            // After k-step 2 every wave waits for its reads of step j's last
+            // fragments and for its loads up to B(j+1) (loads retire in order;
+            // only A(j+2) may stay in flight), then one barrier makes A(j+1)
+            // and B(j+1) complete for all waves and frees the slots of A(j)
+            // and B(j): B(j+2) takes B(j)'s slot in k-step 3 and A(j+3) A(j)'s
+            // in the next step.
             for (int j = 0; j < kn; ++j) {
-    #pragma unroll
-                for (int ks = 0; ks < 4; ++ks) {
-                    const int cur = ks & 1;
-                    // (in the last step k-step 3 reads step kn's slots, which hold
-                    // the redundant re-loads; the values are not used)
-                    const int rs = ks < 3 ? j : j + 1, rk = ks < 3 ? ks + 1 : 0;
-    #pragma unroll
-                    for (int g = 0; g < NT; ++g) {
-                        bf16x8 a;
-                        if constexpr (F8) {
-                            const u32x4 q = fq[g][ks >> 1];
-                            a = (ks & 1) ? e4m3x8_to_bf16(q[2], q[3]) : e4m3x8_to_bf16(q[0], q[1]);
-                        } else {
-                            a = fa[cur][g];
-                        }
-                        acc[g][0] = mfma32x32x16(a, fb[cur][0], acc[g][0]);
-                        if constexpr (NMT > 1) acc[g][1] = mfma32x32x16(a, fb[cur][1], acc[g][1]);
-                        fence();
-                        if constexpr (F8) {
-                            fread_b(rs, rk, cur ^ 1, g);
-                            if (ks == 0)
-                                fread_q(j, 1, g);
-                            else if (ks == 3)
-                                fread_q(j + 1, 0, g);
-                        } else {
-                            fread1(rs, rk, cur ^ 1, 2 * g);
-                            fread1(rs, rk, cur ^ 1, 2 * g + 1);
-                        }
-                        if (ks == 0) {
-                            if (bload) {
-                                load_b(j + 1, 2 * g);
-                                load_b(j + 1, 2 * g + 1);
+                static_for<4>([&](auto ks_tag) {
+                    constexpr int ks = decltype(ks_tag)::value;
+                    constexpr int cur = ks & 1;
+                    constexpr int rk = ks < 3 ? ks + 1 : 0;  // the k-step read next
+                    const int ras = ks < 3 ? sa0 : sa1;       // ... from these slots
+                    const int rbs = ks < 3 ? sb0 : sb1;
+                    constexpr int M = NT * NMT;
+                    constexpr int NR = F8 ? NMT + ((ks == 0 || ks == 3) ? NT : 0) : NT + NMT;
+                    constexpr int NLD = (ks == 0 || ks == 1) ? LA / 2 : (ks == 3 ? L : 0);
+                    constexpr int X = NR + NLD;
+                    auto extra = [&](auto x_tag) {
+                        constexpr int x = decltype(x_tag)::value;
+                        if constexpr (x < NR) {
+                            if constexpr (F8) {
+                                if constexpr (x < NMT)
+                                    fread_b(rbs, rk, cur ^ 1, x);
+                                else if constexpr (ks == 0)
+                                    fread_q(sa0, 1, x - NMT);
+                                else
+                                    fread_q(sa1, 0, x - NMT);
+                            } else {
+                                fread1(ras, rbs, rk, cur ^ 1, x);
                             }
-                        } else if (F8 ? ks == 1 : ks < 3) {
-                            load_a(j + 2, F8 ? g : (ks - 1) * 4 + g);
+                        } else if constexpr (ks == 3) {
+                            if (bload) load_b(sb0, j + 2, x - NR);
+                        } else {
+                            load_a(sa2, j + 2, ks * (LA / 2) + (x - NR));
                         }
+                    };
+                    bf16x8 a;
+                    static_for<M>([&](auto i_tag) {
+                        constexpr int i = decltype(i_tag)::value;
+                        constexpr int g = i / NMT, m = i % NMT;
+                        if constexpr (m == 0) {
+                            if constexpr (F8) {
+                                const u32x4 q = fq[g][ks >> 1];
+                                a = (ks & 1) ? e4m3x8_to_bf16(q[2], q[3]) : e4m3x8_to_bf16(q[0], q[1]);
+                            } else {
+                                a = fa[cur][g];
+                            }
+                        }
+                        acc[g][m] = mfma32x32x16(a, fb[cur][m], acc[g][m]);
+                        // extra x after MFMA x (after MFMA x * M / X when
+                        // there are more extras than MFMAs)
+                        static_for<X>([&](auto x_tag) {
+                            constexpr int x = decltype(x_tag)::value;
+                            if constexpr ((X <= M ? x : x * M / X) == i) extra(x_tag);
+                        });
                         fence();
-                        if constexpr (NMT > 2) acc[g][2] = mfma32x32x16(a, fb[cur][2], acc[g][2]);
-                        if constexpr (NMT > 3) acc[g][3] = mfma32x32x16(a, fb[cur][3], acc[g][3]);
-                        fence();
-                    }
-                    if (ks == 2) {
+                    });
+                    if constexpr (ks == 2) {
                         wait_lds();
                         wait_vmem<LA>();
                         fence();
                         __builtin_amdgcn_s_barrier();
                         fence();
                     }
-                }
+                });
+                const int ta = sa0;
+                sa0 = sa1;
+                sa1 = sa2;
+                sa2 = ta;
+                const int tb = sb0;
+                sb0 = sb1;
+                sb1 = tb;
             }
 
             // epilogue: lane holds, per 32x32 tile, column (token) lane % 32 and
