@@ -121,6 +121,16 @@ struct QCfg {
 
 __device__ __forceinline__ int q_swz(int r) { return (r >> 1) & 7; }
 
+// Relative cost of a tile by the 32-row token blocks each token wave
+// multiplies (NMT = ceil(blocks / 2)): a step still loads the whole weight
+// tile, so a tile of a few rows costs about half a full one.
+constexpr int kFullTileCost = 20;
+__device__ __forceinline__ int tile_cost(int rows)
+{
+    const int nmt = ((rows + 31) / 32 + 1) / 2;
+    return nmt >= 4 ? 20 : (nmt == 3 ? 16 : (nmt == 2 ? 12 : 9));
+}
+
 // s_waitcnt with only the vector-memory count constrained (expcnt/lgkmcnt at max)
 template <int N>
 __device__ __forceinline__ void wait_vmem()
@@ -181,8 +191,44 @@ __global__ __launch_bounds__(256) void q_kernel(TiledParams p)
     if (!UP && p.ksplit_out && blockIdx.x == 0 && tid == 0) *p.ksplit_out = nparts;
     const int ex_items = nparts * nbn * (in_tiles - my_tiles);
     const int total = nparts * nbn * __shfl(in_tiles, p.E - 1, 64);
-    const int beg = (int)((int64_t)total * xcd / 8);
-    const int end = (int)((int64_t)total * (xcd + 1) / 8);
+    // The items are cut into 8 contiguous ranges of about equal cost, one per
+    // XCD (equal counts leave the XCD whose experts end in full tiles with
+    // the most work: an expert's last token tile of a few rows costs a
+    // fraction of a full one).  Cost per (part, weight block) of expert e:
+    // its full tiles plus its last tile by the blocks it multiplies.
+    const int last_rows = my_tiles > 0 ? my_rows - C::BM * (my_tiles - 1) : 0;
+    const int cnb = my_tiles > 0 ? kFullTileCost * (my_tiles - 1) + tile_cost(last_rows) : 0;
+    const int64_t ce = (int64_t)nparts * nbn * cnb;
+    int64_t cin = ce;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const int64_t v = __shfl_up(cin, o, 64);
+        if (lane >= o) cin += v;
+    }
+    const int64_t cbefore = cin - ce;
+    const int64_t ctot = __shfl(cin, p.E - 1, 64);
+    // the first item whose cost prefix (at its start) is >= B
+    auto first_item_at = [&](int64_t B) -> int {
+        const uint64_t le = __ballot(lane < p.E && my_tiles > 0 && cbefore <= B);
+        if (!le) return 0;
+        const int ee = 63 - __builtin_clzll(le);
+        const int64_t rel = B - __shfl(cbefore, ee, 64);
+        const int cnb_e = __shfl(cnb, ee, 64);
+        const int mt_e = __shfl(my_tiles, ee, 64);
+        const int groups = nparts * nbn;
+        const int ex = __shfl(ex_items, ee, 64);
+        if (rel >= (int64_t)groups * cnb_e) return ex + groups * mt_e;
+        int blk = (int)(rel / cnb_e);
+        const int r2 = (int)(rel - (int64_t)blk * cnb_e);
+        int m = (r2 + kFullTileCost - 1) / kFullTileCost;  // tile m starts at m * kFullTileCost
+        if (m > mt_e - 1) {
+            ++blk;
+            m = 0;
+        }
+        return ex + blk * mt_e + m;
+    };
+    const int beg = first_item_at((ctot * xcd + 7) / 8);
+    const int end = xcd == 7 ? total : first_item_at((ctot * (xcd + 1) + 7) / 8);
 
     // a token load covers 8 rows starting at a multiple of 8: lane l takes row
     // l / 8 and the global chunk stored at slot l % 8 (odd loads start at 8
