@@ -48,6 +48,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-prefill", action="store_true",
                     help="decode_t64 only: skip the prefill_t4096 sub-record")
+    ap.add_argument("--no-library-reference", action="store_true",
+                    help="skip the hipBLASLt comparison on the tiled workloads' GEMMs")
     ap.add_argument("--prefill-steps", type=int, default=20,
                     help="timed steps of the prefill_t4096 sub-record")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
@@ -320,7 +322,65 @@ def measure_layer(args, w, steps, warmup):
         "cpu_baseline": None,
         "wall_s_timed": round(wall1 - wall0, 3),
     }
+    if variant == "tiled" and not w.fp8 and not args.no_library_reference:
+        rec["library_reference"] = library_reference(x, perm, offs, h, lay, k, up_avg_ms)
     return rec, (x, lay, T)
+
+
+def library_reference(x, perm, offs, h, lay, k, up_avg_ms, reps=10):
+    """hipBLASLt (torch.matmul, bf16) on the same expert GEMMs, on the same
+    GPU in the same run, for comparison with the tiled kernels: per expert e
+    with M_e routed rows, up = [M_e, d] x [d, 2 ffn] (w1 and w3 as one matrix,
+    the token rows already gathered, no SiLU) and down = [M_e, ffn] x [ffn, d]
+    (no gate weight, no scatter) -- less work than the fused kernels do."""
+    import numpy as np
+    import torch
+
+    counts = np.diff(offs.cpu().numpy())
+    starts = offs.cpu().numpy()[:-1]
+    src = (perm.long() // k)
+    E = len(counts)
+    xs, w13, hs, w2 = [], [], [], []
+    for e in range(E):
+        s, m = int(starts[e]), int(counts[e])
+        xs.append(x[src[s:s + m]].contiguous())
+        w13.append(torch.cat([lay["w1"][e], lay["w3"][e]], 0).t())
+        hs.append(h[s:s + m])
+        w2.append(lay["w2"][e].t())
+    u = [torch.empty(xs[e].shape[0], w13[e].shape[1], dtype=torch.bfloat16, device=x.device)
+         for e in range(E)]
+    yv = [torch.empty(hs[e].shape[0], w2[e].shape[1], dtype=torch.bfloat16, device=x.device)
+          for e in range(E)]
+
+    def up():
+        for e in range(E):
+            torch.matmul(xs[e], w13[e], out=u[e])
+
+    def down():
+        for e in range(E):
+            torch.matmul(hs[e], w2[e], out=yv[e])
+
+    d, ffn = x.shape[1], h.shape[1]
+    rows = int(counts.sum())
+    res = {}
+    for name, fn, flop in (("up", up, 4.0 * rows * d * ffn), ("down", down, 2.0 * rows * d * ffn)):
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) * 1e3 / reps
+        res[name] = {"us": round(us, 1), "tflops": round(flop / us / 1e6, 1)}
+    res["tiled_up_us"] = round(up_avg_ms * 1e3, 1)
+    res["tiled_up_vs_library"] = round(res["up"]["us"] / (up_avg_ms * 1e3), 3)
+    res["kind"] = ("torch.matmul (hipBLASLt) per expert, bf16, same rows per expert, dense "
+                   "pre-gathered operands, no epilogue")
+    del xs, w13, hs, w2, u, yv
+    return res
 
 
 def _oracle():
