@@ -26,7 +26,7 @@ hipError_t launch_stream_down(const DownArgs& a, int64_t rows_max, hipStream_t s
 hipError_t launch_tiled_up(const UpArgs& a, hipStream_t stream);
 hipError_t launch_tiled_down(const DownArgs& a, hipStream_t stream);
 int tiled_down_grid(const DownArgs& a);
-bool tiled_supported(int d, int ffn);
+bool tiled_supported(int d, int ffn, int64_t rows);
 }  // namespace moe
 
 namespace {
@@ -179,7 +179,7 @@ constexpr int64_t kLightRows = 64;
 int down_split_max(int64_t T, int32_t d, int32_t ffn, int32_t E, int32_t k)
 {
     const int64_t A = T * k;
-    if (!moe::tiled_supported(d, ffn)) return 1;
+    if (!moe::tiled_supported(d, ffn, A)) return 1;
     if (A <= 64LL * E) return T > kLightRows ? parts_cap(ffn, 2) : 1;
     const int64_t items = (int64_t)(d / 256) * (A / 256 + E);
     if (items >= 16 * 256) return 1;
@@ -443,7 +443,7 @@ bool split_by_rows(int64_t rows_max, int64_t A, int E)
 hipError_t run_up(const moe::UpArgs& a, int64_t T, hipStream_t stream, bool side = true)
 {
     const int64_t rmax = rows_bound(T, a.kslots);
-    const bool tiled_ok = moe::tiled_supported(a.d, a.ffn);
+    const bool tiled_ok = moe::tiled_supported(a.d, a.ffn, a.A);
     if (split_by_rows(rmax, a.A, a.E)) {
         moe::UpArgs light = a, heavy = a;
         light.mhi = kLightRows;
@@ -480,7 +480,7 @@ hipError_t run_down(const moe::DownArgs& a, int64_t T, int32_t k, hipStream_t st
         light.mhi = kLightRows;
         light.ksplit_out = nullptr;
         heavy.mlo = kLightRows + 1;
-        if (parts && a.ksplit_max > 1 && moe::tiled_supported(a.d, a.ffn)) {
+        if (parts && a.ksplit_max > 1 && moe::tiled_supported(a.d, a.ffn, a.A)) {
             // the fold recomputes the part count and sets *ksplit_out = 1
             heavy.ksplit_out = nullptr;
             return run_side_by_side(
@@ -502,7 +502,7 @@ hipError_t run_down(const moe::DownArgs& a, int64_t T, int32_t k, hipStream_t st
         return uncut(moe::launch_stream_down(heavy, rmax, stream));
     }
     const int v = moe::resolve_variant(g_variant.load(), a.A, a.E);
-    if (v == moe::VARIANT_TILED && moe::tiled_supported(a.d, a.ffn)) {
+    if (v == moe::VARIANT_TILED && moe::tiled_supported(a.d, a.ffn, a.A)) {
         if (sliced) *sliced = parts;
         return moe::launch_tiled_down(a, stream);
     }
@@ -1017,7 +1017,7 @@ moe_status_t moe_linear(const moe_bf16_t* x, const moe_bf16_t* w, int64_t T, int
     // below.  Measured, K = 4096, N = 6144: 2048 tokens 357 us streaming.
     moe::DownArgs a{x, nullptr, w, nullptr, nullptr, y, T, N, K, 1};
     const int64_t items = (int64_t)(N / 256) * ((T + 255) / 256);
-    hipError_t e = (items >= 128 && moe::tiled_supported(N, K)) ? moe::launch_tiled_down(a, stream)
+    hipError_t e = (items >= 128 && moe::tiled_supported(N, K, T)) ? moe::launch_tiled_down(a, stream)
                                                                 : moe::launch_stream_down(a, T, stream);
     return e == hipSuccess ? ok() : hip_fail(e, "linear kernel launch");
 }
@@ -1120,7 +1120,7 @@ int moe_gemm_variant_for(int64_t T, int32_t d, int32_t ffn, int32_t E, int32_t k
     if (moe_workspace_size(T, d, ffn, E, k) == 0 || d % 64 || ffn % 64) return 0;
     if (split_by_rows(rows_bound(T, k), T * k, E)) return 3;
     const int v = moe::resolve_variant(g_variant.load(), T * k, E);
-    return (v == moe::VARIANT_TILED && moe::tiled_supported(d, ffn)) ? moe::VARIANT_TILED
+    return (v == moe::VARIANT_TILED && moe::tiled_supported(d, ffn, T * k)) ? moe::VARIANT_TILED
                                                                      : moe::VARIANT_STREAM;
 }
 

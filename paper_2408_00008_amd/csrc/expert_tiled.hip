@@ -173,7 +173,10 @@ __global__ __launch_bounds__(256) void q_kernel(TiledParams p)
     // per-expert token tiles and their prefix, one expert per lane:
     // items before expert e = nbn * (token tiles of experts < e)
     // (offsets null: one matrix, E = 1, of all A rows -- a dense projection)
-    const int my_rows = lane < p.E ? (p.offsets ? p.offsets[lane + 1] - p.offsets[lane] : (int)p.A) : 0;
+    const int my_off = lane < p.E && p.offsets ? p.offsets[lane] : 0;
+    const int my_rows = lane < p.E ? (p.offsets ? p.offsets[lane + 1] - my_off : (int)p.A) : 0;
+    // complete on every path, so that no later counter wait is placed for them
+    wait_vmem<0>();
     const int my_tiles = (my_rows >= p.mlo && my_rows <= p.mhi) ? (my_rows + C::BM - 1) / C::BM : 0;
     int in_tiles = my_tiles;
 #pragma unroll
@@ -186,11 +189,14 @@ __global__ __launch_bounds__(256) void q_kernel(TiledParams p)
     const int local = blockIdx.x >> 3;
     const int nk = p.K / C::BK;
     // items: expert, reduction part, weight block, token tile
-    const int nparts = UP ? 1 : down_parts(nbn * __shfl(in_tiles, p.E - 1, 64), per_xcd, nk, p.A, p.N,
-                                           p.ksplit_max);
+    // (values read from one lane are uniform; readfirstlane keeps them, and
+    // the step counts and branches derived from them, in scalar registers)
+    auto uni = [](int v) { return __builtin_amdgcn_readfirstlane(v); };
+    const int all_tiles = uni(__shfl(in_tiles, p.E - 1, 64));
+    const int nparts = UP ? 1 : uni(down_parts(nbn * all_tiles, per_xcd, nk, p.A, p.N, p.ksplit_max));
     if (!UP && p.ksplit_out && blockIdx.x == 0 && tid == 0) *p.ksplit_out = nparts;
     const int ex_items = nparts * nbn * (in_tiles - my_tiles);
-    const int total = nparts * nbn * __shfl(in_tiles, p.E - 1, 64);
+    const int total = nparts * nbn * all_tiles;
     // The items are cut into 8 contiguous ranges of about equal cost, one per
     // XCD (equal counts leave the XCD whose experts end in full tiles with
     // the most work: an expert's last token tile of a few rows costs a
@@ -227,8 +233,11 @@ __global__ __launch_bounds__(256) void q_kernel(TiledParams p)
         }
         return ex + blk * mt_e + m;
     };
-    const int beg = first_item_at((ctot * xcd + 7) / 8);
-    const int end = xcd == 7 ? total : first_item_at((ctot * (xcd + 1) + 7) / 8);
+    // (uniform by construction; readfirstlane lets the compiler see it, so the
+    // item indices and everything derived from them stay in scalar registers)
+    const int beg = __builtin_amdgcn_readfirstlane(first_item_at((ctot * xcd + 7) / 8));
+    const int end = __builtin_amdgcn_readfirstlane(
+        xcd == 7 ? total : first_item_at((ctot * (xcd + 1) + 7) / 8));
 
     // a token load covers 8 rows starting at a multiple of 8: lane l takes row
     // l / 8 and the global chunk stored at slot l % 8 (odd loads start at 8
@@ -260,334 +269,450 @@ __global__ __launch_bounds__(256) void q_kernel(TiledParams p)
     const int a_wave = (UP ? wr * 64 : wr * 128) * C::AROWB;
     auto atile = [](int nt) { return (UP ? (nt >> 1) * (C::BN / 2) + (nt & 1) * 32 : nt * 32) * C::AROWB; };
 
-    for (int w = beg + local; w < end; w += per_xcd) {
-        // the expert of item w: the last one (with tiles) whose first item is <= w
+    // ---- items ----------------------------------------------------------------
+    //
+    // Items follow each other without a break in the load stream: the last two
+    // steps of an item load the first two steps of the workgroup's next item
+    // into the ring slots the steady state would use.  The next item's first
+    // step is complete everywhere after the barrier of its predecessor's last
+    // step and its second one lands during the predecessor's epilogue, so no
+    // barrier or prologue is needed between items.  What the next item's
+    // loads depend on through memory (its gathered token rows; DOWN: the
+    // output rows of its epilogue) is loaded when the item before it starts,
+    // and its gate weights when it starts itself, before the first step's
+    // counter wait, which completes them.  (Re-issuing these loads into the
+    // registers of the previous item's makes the compiler wait for all loads
+    // and stores in flight at that point, the previous epilogue's included.)
+    // An item of fewer than 3 steps (tiny reductions) is followed by a drain,
+    // a barrier and a fresh prologue.
+    struct Item {
+        int e, part, nb, k0, kn, row0, m0, Mp;
+        int src[L];    // this lane's token rows of its L token loads (UP: gathered slot ids)
+        int orow[4];   // DOWN: output row of each epilogue column block
+        float gw[4];   // DOWN: its gate weight
+    };
+    // the uniform part of item w
+    auto index_item = [&](int w, Item& it) {
         const uint64_t le = __ballot(lane < p.E && my_tiles > 0 && ex_items <= w);
         const int e = 63 - __builtin_clzll(le);
-        const int mt_e = __shfl(my_tiles, e, 64);
-        int r = w - __shfl(ex_items, e, 64);
+        const int mt_e = uni(__shfl(my_tiles, e, 64));
+        int r = w - uni(__shfl(ex_items, e, 64));
         const int part = r / (nbn * mt_e);
         r -= part * nbn * mt_e;
         const int nb = r / mt_e;
         const int mtile = r - nb * mt_e;
-        // this item's reduction steps [k0, k0 + kn)
-        const int k0 = (int)((int64_t)nk * part / nparts);
-        const int kn = (int)((int64_t)nk * (part + 1) / nparts) - k0;
-        const int row0 = p.offsets ? p.offsets[e] : 0;
-        const int M = p.offsets ? p.offsets[e + 1] - row0 : (int)p.A;
-        const int m0 = mtile * C::BM;
-        const int Mp = min(C::BM, M - m0);
-
-        // wave w loads A rows [64w, 64w + 64) and B rows [64w, 64w + 64); the
-        // 64 A rows are 64 consecutive rows of w1, w3 or w2
-        const bool a_second = UP && 64 * wave >= C::BN / 2;
-        const int64_t wrow = (int64_t)e * p.N + nb * C::NOUT + 64 * wave - (a_second ? C::BN / 2 : 0);
-        const unsigned char* aptr[2];
-        if constexpr (F8) {
-            const uint8_t* base = (a_second ? p.qb : p.qa) + wrow * p.K + k0 * C::BK;
-            aptr[0] = aptr[1] = base + (int64_t)(lane >> 2) * p.K + lchunk8 * 16;
-        } else {
-            const bf16_t* base = (a_second ? p.wb : p.wa) + wrow * p.K + k0 * C::BK;
-            aptr[0] = reinterpret_cast<const unsigned char*>(base + (int64_t)lrow * p.K + lchunk[0] * 8);
-            aptr[1] = reinterpret_cast<const unsigned char*>(base + (int64_t)lrow * p.K + lchunk[1] * 8);
-        }
-        const bf16_t* bptr[L];
+        it.e = e;
+        it.part = part;
+        it.nb = nb;
+        it.k0 = (int)((int64_t)nk * part / nparts);
+        it.kn = (int)((int64_t)nk * (part + 1) / nparts) - it.k0;
+        it.row0 = uni(__shfl(my_off, e, 64));
+        it.m0 = mtile * C::BM;
+        it.Mp = min(C::BM, uni(__shfl(my_rows, e, 64)) - it.m0);
+    };
+    // the loads item `it` depends on: wave w loads token rows [64w, 64w + 64)
+    // (rows past the expert's end repeat its last row); DOWN: the scatter row
+    // of each column block of the epilogue (with NMT = ceil(rows / 64) blocks
+    // per token wave, as the tile body below chooses)
+    auto fetch_rows = [&](Item& it) {
 #pragma unroll
         for (int i = 0; i < L; ++i) {
             const int tr = 64 * wave + 8 * i + lrow;
-            const int rowm = row0 + m0 + (tr < Mp ? tr : Mp - 1);
-            const int64_t src = (UP && p.gather) ? p.gather[rowm] / p.kslots : rowm;
-            bptr[i] = p.act + src * p.K + k0 * C::BK + lchunk[i & 1] * 8;
+            const int rowm = it.row0 + it.m0 + (tr < it.Mp ? tr : it.Mp - 1);
+            it.src[i] = (UP && p.gather) ? p.gather[rowm] : rowm;
         }
-        // bytes between a wave's consecutive weight loads (8 or 16 rows)
-        const int64_t astep = (int64_t)16 * p.K;
-        // the loads of step s into the ring slot at byte offset `slot`; steps
-        // past the last re-load the last step, so that the number of loads in
-        // flight, and with it every counter wait, is the same in every step
-        auto load_a = [&](int slot, int s, int i) {
-            const int64_t ko = (int64_t)(s < kn ? s : kn - 1) * C::BK * (F8 ? 1 : 2) + i * astep;
-            const int rows = F8 ? 16 : 8;
-            __builtin_amdgcn_global_load_lds(
-                (const void __attribute__((address_space(1)))*)(aptr[F8 ? 0 : (i & 1)] + ko),
-                (void __attribute__((address_space(3)))*)(ring + slot + (64 * wave + rows * i) * C::AROWB),
-                16, 0, 0);
-        };
-        auto load_b = [&](int slot, int s, int i) {
-            const int ko = (s < kn ? s : kn - 1) * C::BK;
-            __builtin_amdgcn_global_load_lds(
-                (const void __attribute__((address_space(1)))*)(bptr[i] + ko),
-                (void __attribute__((address_space(3)))*)(ring + C::B_OFF + slot + (64 * wave + 8 * i) * C::ROWB),
-                16, 0, 0);
-        };
-
-        // The tile body for NMT multiplied 32-token column blocks per wave
-        // (4: full tile).  The tile's blocks that hold rows are split evenly
-        // between the two token waves: wave wm multiplies blocks
-        // [wm NMT, wm NMT + NMT), NMT = ceil(blocks / 2), so a tile of an
-        // expert's last few rows (or of an expert with 65-192 rows) skips the
-        // MFMAs and fragment reads of empty blocks and both waves finish
-        // together.  Only computed blocks are stored; columns past the rows
-        // hold copies of the last row (see epilogue).
-        auto tile = [&](auto nmt_tag) {
-            constexpr int NMT = decltype(nmt_tag)::value;
-            const int b_wave = wm * NMT * 32 * C::ROWB;
-            // token rows [0, 64 NMT) are multiplied: wave w loads rows
-            // [64w, 64w + 64), so waves w >= NMT skip their token loads (in a
-            // full tile every wave loads, with no branch).  The counter waits
-            // stay exact for them: the loads younger than the ones a wait is
-            // for are A loads, which every wave issues.
-            const bool bload = NMT == 4 || wave < NMT;
-            floatx16 acc[NT][NMT];
-    #pragma unroll
-            for (int i = 0; i < NT; ++i)
-    #pragma unroll
-                for (int j = 0; j < NMT; ++j)
-    #pragma unroll
-                    for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.0f;
-
-            bf16x8 fa[2][NT], fb[2][NMT];
-            // 8-bit weights: raw 16-byte reads, k-steps (0,1) and (2,3).  A
-            // native vector type: an aggregate (HIP's uint4) load carries no
-            // memory operand the compiler can tell apart from the in-flight
-            // global->LDS loads, and it then waits for all of them (vmcnt(0))
-            // before each read.
-            u32x4 fq[NT][2];
-            // ring slots (byte offsets) of A(j), A(j+1), A(j+2) and of B(j),
-            // B(j+1) during step j; they rotate at the end of every step
-            int sa0 = 0, sa1 = C::ASLOT, sa2 = 2 * C::ASLOT;
-            int sb0 = 0, sb1 = C::SLOT;
-            // fragment f (0 .. NT-1: weight tiles, NT ..: token tiles) of
-            // k-step ks from the A slot as / B slot bs
-            auto fread1 = [&](int as, int bs, int ks, int slot, int f) {
-                if (f < NT) {
-                    fa[slot][f] = *reinterpret_cast<const bf16x8*>(ring + as + a_wave + xk[ks] + atile(f));
-                } else {
-                    fb[slot][f - NT] = *reinterpret_cast<const bf16x8*>(
-                        ring + C::B_OFF + bs + b_wave + xk[ks] + (f - NT) * 32 * C::ROWB);
-                }
-            };
-            // 8-bit weights: token fragment m of k-step ks, and the raw weight
-            // bytes of k-step pair q for tile nt
-            auto fread_b = [&](int bs, int ks, int slot, int m) {
-                fb[slot][m] = *reinterpret_cast<const bf16x8*>(ring + C::B_OFF + bs + b_wave + xk[ks] +
-                                                               m * 32 * C::ROWB);
-            };
-            auto fread_q = [&](int as, int q, int nt) {
-                fq[nt][q] = *reinterpret_cast<const u32x4*>(ring + as + a_wave + xa[q] + atile(nt));
-            };
-            auto fence = [] { __builtin_amdgcn_sched_barrier(0); };
-
-            // 8-bit weights: the row scales of this lane's accumulator rows
-            // (UP: w1 then w3 rows of its two 32-row tiles; DOWN: its four
-            // tiles), loaded before the prologue's loads so that they are the
-            // oldest memory operations and the counter waits below stay exact
-            floatx4 sc[4][4];
-            if constexpr (F8) {
-                const int n0 = nb * C::NOUT + (UP ? wr * 64 : wr * 128) + 4 * (lane >> 5);
-    #pragma unroll
-                for (int t = 0; t < 4; ++t) {
-                    const float* sp = UP ? (t < 2 ? p.sa : p.sb) + (int64_t)e * p.N + n0 + (t & 1) * 32
-                                         : p.sa + (int64_t)e * p.N + n0 + t * 32;
-    #pragma unroll
-                    for (int q = 0; q < 4; ++q) sc[t][q] = *reinterpret_cast<const floatx4*>(sp + 8 * q);
-                }
+        if constexpr (!UP) {
+            const int nmt = (it.Mp + 63) >> 6;
+#pragma unroll
+            for (int mt = 0; mt < 4; ++mt) {
+                const int mloc = (wm * nmt + mt) * 32 + (lane & 31);
+                const int rrow = it.row0 + it.m0 + (mloc < it.Mp ? mloc : it.Mp - 1);
+                it.orow[mt] = (p.topk_w && p.perm) ? p.perm[rrow] : rrow;
             }
+        }
+    };
+    auto fetch_gates = [&](Item& it) {
+        if constexpr (!UP) {
+#pragma unroll
+            for (int mt = 0; mt < 4; ++mt) it.gw[mt] = (p.topk_w && p.perm) ? p.topk_w[it.orow[mt]] : 1.0f;
+        }
+    };
+    // Load addresses: a uniform base per item (scalar registers) plus a
+    // 32-bit per-lane byte offset.  Wave w loads weight rows [64w, 64w + 64)
+    // of the item's block (64 consecutive rows of w1, w3 or w2); the lane's
+    // offset inside them does not depend on the item.  Token rows: the
+    // lane's row of each of its L loads times the row pitch (token buffers
+    // stay below 4 GiB; the launchers check).
+    uint32_t aoff[2];
+#pragma unroll
+    for (int q = 0; q < 2; ++q)
+        aoff[q] = F8 ? (uint32_t)((lane >> 2) * p.K + lchunk8 * 16) : (uint32_t)(lrow * p.K * 2 + lchunk[q] * 16);
+    auto abase_of = [&](const Item& it) -> const unsigned char* {
+        const bool a_second = UP && 64 * wave >= C::BN / 2;
+        const int64_t wrow = (int64_t)it.e * p.N + it.nb * C::NOUT + 64 * wave - (a_second ? C::BN / 2 : 0);
+        const unsigned char* wm8 = F8 ? (a_second ? p.qb : p.qa)
+                                      : reinterpret_cast<const unsigned char*>(a_second ? p.wb : p.wa);
+        return wm8 + (wrow * p.K + (int64_t)it.k0 * C::BK) * (F8 ? 1 : 2);
+    };
+    auto boff_of = [&](const Item& it, int i) -> uint32_t {
+        const uint32_t src = (UP && p.gather) ? (uint32_t)it.src[i] / (uint32_t)p.kslots : (uint32_t)it.src[i];
+        return src * (uint32_t)(p.K * 2) + (uint32_t)(lchunk[i & 1] * 16);
+    };
+    const unsigned char* const bbase = reinterpret_cast<const unsigned char*>(p.act);
 
-            // Prologue: A(0), A(1), B(0), B(1) -- the loads the steady state
-            // keeps ahead -- then A(0) and B(0) complete everywhere and the
-            // fragments of k-step 0 are read.
-    #pragma unroll
-            for (int i = 0; i < LA; ++i) load_a(sa0, 0, i);
-    #pragma unroll
-            for (int i = 0; i < LA; ++i) load_a(sa1, 1, i);
-            if (bload) {
-    #pragma unroll
-                for (int i = 0; i < L; ++i) load_b(sb0, 0, i);
-    #pragma unroll
-                for (int i = 0; i < L; ++i) load_b(sb1, 1, i);
-                wait_vmem<L>();
+    // The loads in flight come from one item at a time: la / lbk0 / lb
+    // address its step 0, and step s of the running item is its step
+    // s - lsh, clamped to its last step lkn - 1 (steps past the end re-load
+    // the last one, so that the number of loads in flight, and with it every
+    // counter wait, is the same in every step).
+    const unsigned char* la = nullptr;
+    int lbk0 = 0;
+    uint32_t lb[L];
+    int lsh = 0, lkn = 1;
+    uint32_t nbo[L];  // the next item's token row offsets
+    // bytes between a wave's consecutive weight loads (8 or 16 rows)
+    const int64_t astep = (int64_t)16 * p.K;
+    auto load_a = [&](int slot, int s, int i) {
+        const int st = min(s - lsh, lkn - 1);
+        const unsigned char* base = la + (int64_t)st * C::BK * (F8 ? 1 : 2) + i * astep;
+        const int rows = F8 ? 16 : 8;
+        __builtin_amdgcn_global_load_lds(
+            (const void __attribute__((address_space(1)))*)(base + aoff[F8 ? 0 : (i & 1)]),
+            (void __attribute__((address_space(3)))*)(ring + slot + (64 * wave + rows * i) * C::AROWB),
+            16, 0, 0);
+    };
+    auto load_b = [&](int slot, int s, int i) {
+        const int st = min(s - lsh, lkn - 1);
+        const unsigned char* base = bbase + (int64_t)(lbk0 + st) * C::BK * 2;
+        __builtin_amdgcn_global_load_lds(
+            (const void __attribute__((address_space(1)))*)(base + lb[i]),
+            (void __attribute__((address_space(3)))*)(ring + C::B_OFF + slot + (64 * wave + 8 * i) * C::ROWB),
+            16, 0, 0);
+    };
+    // ring slots (byte offsets) of A(j), A(j+1), A(j+2) and of B(j), B(j+1)
+    // during step j; they rotate at the end of every step and carry over from
+    // one item to the next
+    int sa0 = 0, sa1 = C::ASLOT, sa2 = 2 * C::ASLOT;
+    int sb0 = 0, sb1 = C::SLOT;
+    // steps 0 and 1 of `it` into the slots of A(0), A(1), B(0), B(1), by every
+    // wave, then complete everywhere
+    // (from_next: the token offsets were computed into nbo during the item
+    // before)
+    auto prologue = [&](const Item& it, bool from_next) {
+        la = abase_of(it);
+        lbk0 = it.k0;
+#pragma unroll
+        for (int i = 0; i < L; ++i) lb[i] = from_next ? nbo[i] : boff_of(it, i);
+        lsh = 0;
+        lkn = it.kn;
+#pragma unroll
+        for (int i = 0; i < LA; ++i) load_a(sa0, 0, i);
+#pragma unroll
+        for (int i = 0; i < LA; ++i) load_a(sa1, 1, i);
+#pragma unroll
+        for (int i = 0; i < L; ++i) load_b(sb0, 0, i);
+#pragma unroll
+        for (int i = 0; i < L; ++i) load_b(sb1, 1, i);
+        wait_vmem<0>();
+        __syncthreads();
+    };
+
+    Item cur, nxt;
+    int w = beg + local;
+    bool more = false, pipe = false;
+
+    // The tile body for NMT multiplied 32-token column blocks per wave
+    // (4: full tile).  The tile's blocks that hold rows are split evenly
+    // between the two token waves: wave wm multiplies blocks
+    // [wm NMT, wm NMT + NMT), NMT = ceil(blocks / 2), so a tile of an
+    // expert's last few rows (or of an expert with 65-192 rows) skips the
+    // MFMAs and fragment reads of empty blocks and both waves finish
+    // together.  Only computed blocks are stored; columns past the rows
+    // hold copies of the last row (see epilogue).
+    auto tile = [&](auto nmt_tag) {
+        constexpr int NMT = decltype(nmt_tag)::value;
+        const int kn = cur.kn;
+        const int b_wave = wm * NMT * 32 * C::ROWB;
+        // token rows [0, 64 NMT) are multiplied: wave w loads rows
+        // [64w, 64w + 64), so waves w >= NMT skip this item's token loads
+        // (in a full tile every wave loads, with no branch) -- but not the
+        // next item's.  The counter waits stay exact for them: the loads
+        // younger than the ones a wait is for are A loads, which every wave
+        // issues.
+        bool bl = NMT == 4 || wave < NMT;
+        lsh = 0;
+        lkn = kn;
+        floatx16 acc[NT][NMT];
+#pragma unroll
+        for (int i = 0; i < NT; ++i)
+#pragma unroll
+            for (int j = 0; j < NMT; ++j)
+#pragma unroll
+                for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.0f;
+
+        bf16x8 fa[2][NT], fb[2][NMT];
+        // 8-bit weights: raw 16-byte reads, k-steps (0,1) and (2,3).  A
+        // native vector type: an aggregate (HIP's uint4) load carries no
+        // memory operand the compiler can tell apart from the in-flight
+        // global->LDS loads, and it then waits for all of them (vmcnt(0))
+        // before each read.
+        u32x4 fq[NT][2];
+        // fragment f (0 .. NT-1: weight tiles, NT ..: token tiles) of
+        // k-step ks from the A slot as / B slot bs
+        auto fread1 = [&](int as, int bs, int ks, int slot, int f) {
+            if (f < NT) {
+                fa[slot][f] = *reinterpret_cast<const bf16x8*>(ring + as + a_wave + xk[ks] + atile(f));
             } else {
-                wait_vmem<LA>();
+                fb[slot][f - NT] = *reinterpret_cast<const bf16x8*>(
+                    ring + C::B_OFF + bs + b_wave + xk[ks] + (f - NT) * 32 * C::ROWB);
             }
-            fence();
-            __builtin_amdgcn_s_barrier();
-            fence();
-            if constexpr (F8) {
-    #pragma unroll
-                for (int nt = 0; nt < NT; ++nt) fread_q(sa0, 0, nt);
-    #pragma unroll
-                for (int m = 0; m < NMT; ++m) fread_b(sb0, 0, 0, m);
-            } else {
-    #pragma unroll
-                for (int f = 0; f < NT + NMT; ++f) fread1(sa0, sb0, 0, 0, f);
-            }
+        };
+        // 8-bit weights: token fragment m of k-step ks, and the raw weight
+        // bytes of k-step pair q for tile nt
+        auto fread_b = [&](int bs, int ks, int slot, int m) {
+            fb[slot][m] = *reinterpret_cast<const bf16x8*>(ring + C::B_OFF + bs + b_wave + xk[ks] +
+                                                           m * 32 * C::ROWB);
+        };
+        auto fread_q = [&](int as, int q, int nt) {
+            fq[nt][q] = *reinterpret_cast<const u32x4*>(ring + as + a_wave + xa[q] + atile(nt));
+        };
+        auto fence = [] { __builtin_amdgcn_sched_barrier(0); };
 
-            // Step j, k-step ks: its NT x NMT MFMAs use the fragments in
-            // register slot ks & 1, and one memory operation follows each of
-            // the first MFMAs (several where a k-step has more memory
-            // operations than MFMAs): first the
-            // reads of the next k-step's fragments into the other slot (so they
-            // are complete long before that k-step starts), then this
-            // k-step's share of the loads: A(j+2) in k-steps 0 and 1, B(j+2) in
-            // k-step 3.  8-bit weights read their raw bytes a pair of k-steps
-            // at a time (k-step 0: pair 1 of step j; k-step 3: pair 0 of step
-            // j+1) and widen them to bf16 before the MFMAs of each weight tile.
-            // After k-step 2 every wave waits for its reads of step j's last
-            // fragments and for its loads up to B(j+1) (loads retire in order;
-            // only A(j+2) may stay in flight), then one barrier makes A(j+1)
-            // and B(j+1) complete for all waves and frees the slots of A(j)
-            // and B(j): B(j+2) takes B(j)'s slot in k-step 3 and A(j+3) A(j)'s
-            // in the next step.
-            for (int j = 0; j < kn; ++j) {
-                static_for<4>([&](auto ks_tag) {
-                    constexpr int ks = decltype(ks_tag)::value;
-                    constexpr int cur = ks & 1;
-                    constexpr int rk = ks < 3 ? ks + 1 : 0;  // the k-step read next
-                    const int ras = ks < 3 ? sa0 : sa1;       // ... from these slots
-                    const int rbs = ks < 3 ? sb0 : sb1;
-                    constexpr int M = NT * NMT;
-                    constexpr int NR = F8 ? NMT + ((ks == 0 || ks == 3) ? NT : 0) : NT + NMT;
-                    constexpr int NLD = (ks == 0 || ks == 1) ? LA / 2 : (ks == 3 ? L : 0);
-                    constexpr int X = NR + NLD;
-                    auto extra = [&](auto x_tag) {
-                        constexpr int x = decltype(x_tag)::value;
-                        if constexpr (x < NR) {
-                            if constexpr (F8) {
-                                if constexpr (x < NMT)
-                                    fread_b(rbs, rk, cur ^ 1, x);
-                                else if constexpr (ks == 0)
-                                    fread_q(sa0, 1, x - NMT);
-                                else
-                                    fread_q(sa1, 0, x - NMT);
-                            } else {
-                                fread1(ras, rbs, rk, cur ^ 1, x);
-                            }
-                        } else if constexpr (ks == 3) {
-                            if (bload) load_b(sb0, j + 2, x - NR);
-                        } else {
-                            load_a(sa2, j + 2, ks * (LA / 2) + (x - NR));
-                        }
-                    };
-                    bf16x8 a;
-                    static_for<M>([&](auto i_tag) {
-                        constexpr int i = decltype(i_tag)::value;
-                        constexpr int g = i / NMT, m = i % NMT;
-                        if constexpr (m == 0) {
-                            if constexpr (F8) {
-                                const u32x4 q = fq[g][ks >> 1];
-                                a = (ks & 1) ? e4m3x8_to_bf16(q[2], q[3]) : e4m3x8_to_bf16(q[0], q[1]);
-                            } else {
-                                a = fa[cur][g];
-                            }
-                        }
-                        acc[g][m] = mfma32x32x16(a, fb[cur][m], acc[g][m]);
-                        // extra x after MFMA x (after MFMA x * M / X when
-                        // there are more extras than MFMAs)
-                        static_for<X>([&](auto x_tag) {
-                            constexpr int x = decltype(x_tag)::value;
-                            if constexpr ((X <= M ? x : x * M / X) == i) extra(x_tag);
-                        });
-                        fence();
-                    });
-                    if constexpr (ks == 2) {
-                        wait_lds();
-                        wait_vmem<LA>();
-                        fence();
-                        __builtin_amdgcn_s_barrier();
-                        fence();
-                    }
-                });
-                const int ta = sa0;
-                sa0 = sa1;
-                sa1 = sa2;
-                sa2 = ta;
-                const int tb = sb0;
-                sb0 = sb1;
-                sb1 = tb;
+        // Loads whose values the epilogue needs, issued before the first
+        // step's loads so that its counter wait completes them: 8-bit
+        // weights' row scales of this lane's accumulator rows (UP: w1 then
+        // w3 rows of its two 32-row tiles; DOWN: its four tiles), and DOWN's
+        // gate weights (their rows were loaded with the item before).
+        floatx4 sc[4][4];
+        if constexpr (F8) {
+            const int n0 = cur.nb * C::NOUT + (UP ? wr * 64 : wr * 128) + 4 * (lane >> 5);
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+                const float* sp = UP ? (t < 2 ? p.sa : p.sb) + (int64_t)cur.e * p.N + n0 + (t & 1) * 32
+                                     : p.sa + (int64_t)cur.e * p.N + n0 + t * 32;
+#pragma unroll
+                for (int q = 0; q < 4; ++q) sc[t][q] = *reinterpret_cast<const floatx4*>(sp + 8 * q);
             }
+        }
+        fetch_gates(cur);
 
-            // epilogue: lane holds, per 32x32 tile, column (token) lane % 32 and
-            // rows (weight rows) 8q + 4 * (lane / 32) + i, q, i < 4.  Straight-line
-            // code, one output tile at a time: any branch here makes the compiler
-            // copy all accumulators out of their registers at once.  Token columns
-            // past the expert's rows were loaded from its last row, so they hold
-            // exactly that row's results and store the same bits to the same place.
-            // 8-bit weights: each weight row's scale multiplies its accumulators.
-    #pragma unroll
-            for (int mt = 0; mt < NMT; ++mt) {
-                const int mloc = (wm * NMT + mt) * 32 + (lane & 31);
-                const int64_t rrow = row0 + m0 + (mloc < Mp ? mloc : Mp - 1);
-                if (UP) {
-                    const int n0 = nb * C::NOUT + wr * 64 + 4 * (lane >> 5);
-                    bf16_t* hrow = p.h_out + rrow * p.N + n0;
-    #pragma unroll
-                    for (int h = 0; h < 2; ++h) {
-                        // the accumulators are redefined here (in their AGPRs), so
-                        // their copies into VGPRs cannot move above this point
-                        asm volatile("" : "+a"(acc[h][mt]), "+a"(acc[h + 2][mt]));
-                        floatx16 u = acc[h][mt];
-                        floatx16 v = acc[h + 2][mt];
+        // k-step 0 of step 0: A(0) and B(0) are complete everywhere (the
+        // prologue's barrier, or the previous item's last step)
+        if constexpr (F8) {
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt) fread_q(sa0, 0, nt);
+#pragma unroll
+            for (int m = 0; m < NMT; ++m) fread_b(sb0, 0, 0, m);
+        } else {
+#pragma unroll
+            for (int f = 0; f < NT + NMT; ++f) fread1(sa0, sb0, 0, 0, f);
+        }
+
+        // Step j, k-step ks: its NT x NMT MFMAs use the fragments in
+        // register slot ks & 1, and one memory operation follows each of
+        // the first MFMAs (several where a k-step has more memory
+        // operations than MFMAs): first the
+        // reads of the next k-step's fragments into the other slot (so they
+        // are complete long before that k-step starts), then this
+        // k-step's share of the loads: A(j+2) in k-steps 0 and 1, B(j+2) in
+        // k-step 3.  8-bit weights read their raw bytes a pair of k-steps
+        // at a time (k-step 0: pair 1 of step j; k-step 3: pair 0 of step
+        // j+1) and widen them to bf16 before the MFMAs of each weight tile.
+        // After k-step 2 every wave waits for its reads of step j's last
+        // fragments and for its loads up to B(j+1) (loads retire in order;
+        // only A(j+2) may stay in flight), then one barrier makes A(j+1)
+        // and B(j+1) complete for all waves and frees the slots of A(j)
+        // and B(j): B(j+2) takes B(j)'s slot in k-step 3 and A(j+3) A(j)'s
+        // in the next step.  From step kn - 2 on, "step j + 2" is step
+        // j + 2 - kn of the next item.  (A do-while: the body runs at least
+        // once, so the compiler's counter tracking sees every value loaded
+        // before it as complete after the first step's wait.)
+        int j = 0;
+        do {
+            if (pipe && j == kn - 2) {
+                la = abase_of(nxt);
+                lbk0 = nxt.k0;
+#pragma unroll
+                for (int i = 0; i < L; ++i) lb[i] = nbo[i];
+                lsh = kn;
+                lkn = nxt.kn;
+                bl = true;
+            }
+            static_for<4>([&](auto ks_tag) {
+                constexpr int ks = decltype(ks_tag)::value;
+                constexpr int cur_s = ks & 1;
+                constexpr int rk = ks < 3 ? ks + 1 : 0;  // the k-step read next
+                const int ras = ks < 3 ? sa0 : sa1;       // ... from these slots
+                const int rbs = ks < 3 ? sb0 : sb1;
+                constexpr int M = NT * NMT;
+                constexpr int NR = F8 ? NMT + ((ks == 0 || ks == 3) ? NT : 0) : NT + NMT;
+                constexpr int NLD = (ks == 0 || ks == 1) ? LA / 2 : (ks == 3 ? L : 0);
+                constexpr int X = NR + NLD;
+                auto extra = [&](auto x_tag) {
+                    constexpr int x = decltype(x_tag)::value;
+                    if constexpr (x < NR) {
                         if constexpr (F8) {
-    #pragma unroll
-                            for (int q = 0; q < 4; ++q)
-    #pragma unroll
-                                for (int i = 0; i < 4; ++i) {
-                                    u[4 * q + i] *= sc[h][q][i];
-                                    v[4 * q + i] *= sc[h + 2][q][i];
-                                }
+                            if constexpr (x < NMT)
+                                fread_b(rbs, rk, cur_s ^ 1, x);
+                            else if constexpr (ks == 0)
+                                fread_q(sa0, 1, x - NMT);
+                            else
+                                fread_q(sa1, 0, x - NMT);
+                        } else {
+                            fread1(ras, rbs, rk, cur_s ^ 1, x);
                         }
-    #pragma unroll
-                        for (int q = 0; q < 4; ++q) {
-                            uint2 pk;
-                            pk.x = pack_bf16x2(silu(u[4 * q + 0]) * v[4 * q + 0], silu(u[4 * q + 1]) * v[4 * q + 1]);
-                            pk.y = pack_bf16x2(silu(u[4 * q + 2]) * v[4 * q + 2], silu(u[4 * q + 3]) * v[4 * q + 3]);
-                            *reinterpret_cast<uint2*>(hrow + h * 32 + 8 * q) = pk;
-                        }
-                        __builtin_amdgcn_sched_barrier(0);
+                    } else if constexpr (ks == 3) {
+                        if (bl) load_b(sb0, j + 2, x - NR);
+                    } else {
+                        load_a(sa2, j + 2, ks * (LA / 2) + (x - NR));
                     }
-                } else {
-                    int64_t orow = rrow;
-                    float gw = 1.0f;
-                    if (p.topk_w && p.perm) {
-                        orow = p.perm[rrow];
-                        gw = p.topk_w[orow];
-                    }
-                    const int n0 = nb * C::NOUT + wr * 128 + 4 * (lane >> 5);
-                    float* yrow = p.y_out + part * p.slice + orow * p.N + n0;
-    #pragma unroll
-                    for (int nt = 0; nt < NT; ++nt) {
-                        asm volatile("" : "+a"(acc[nt][mt]));
-    #pragma unroll
-                        for (int q = 0; q < 4; ++q) {
-                            floatx4 g4 = {gw, gw, gw, gw};
-                            if constexpr (F8) g4 = g4 * sc[nt][q];
-                            float4 v;
-                            v.x = g4[0] * acc[nt][mt][4 * q + 0];
-                            v.y = g4[1] * acc[nt][mt][4 * q + 1];
-                            v.z = g4[2] * acc[nt][mt][4 * q + 2];
-                            v.w = g4[3] * acc[nt][mt][4 * q + 3];
-                            *reinterpret_cast<float4*>(yrow + nt * 32 + 8 * q) = v;
+                };
+                bf16x8 a;
+                static_for<M>([&](auto i_tag) {
+                    constexpr int i = decltype(i_tag)::value;
+                    constexpr int g = i / NMT, m = i % NMT;
+                    if constexpr (m == 0) {
+                        if constexpr (F8) {
+                            const u32x4 q = fq[g][ks >> 1];
+                            a = (ks & 1) ? e4m3x8_to_bf16(q[2], q[3]) : e4m3x8_to_bf16(q[0], q[1]);
+                        } else {
+                            a = fa[cur_s][g];
                         }
-                        __builtin_amdgcn_sched_barrier(0);
+                    }
+                    acc[g][m] = mfma32x32x16(a, fb[cur_s][m], acc[g][m]);
+                    // extra x after MFMA x (after MFMA x * M / X when
+                    // there are more extras than MFMAs)
+                    static_for<X>([&](auto x_tag) {
+                        constexpr int x = decltype(x_tag)::value;
+                        if constexpr ((X <= M ? x : x * M / X) == i) extra(x_tag);
+                    });
+                    fence();
+                });
+                if constexpr (ks == 2) {
+                    wait_lds();
+                    wait_vmem<LA>();
+                    fence();
+                    __builtin_amdgcn_s_barrier();
+                    fence();
+                    // the next item's token rows were loaded before this
+                    // item's first step and are complete now
+                    if (more && j == 0) {
+#pragma unroll
+                        for (int i = 0; i < L; ++i) nbo[i] = boff_of(nxt, i);
                     }
                 }
+            });
+            const int ta = sa0;
+            sa0 = sa1;
+            sa1 = sa2;
+            sa2 = ta;
+            const int tb = sb0;
+            sb0 = sb1;
+            sb1 = tb;
+        } while (++j < kn);
+
+        // epilogue: lane holds, per 32x32 tile, column (token) lane % 32 and
+        // rows (weight rows) 8q + 4 * (lane / 32) + i, q, i < 4.  Straight-line
+        // code, one output tile at a time: any branch here makes the compiler
+        // copy all accumulators out of their registers at once.  Token columns
+        // past the expert's rows were loaded from its last row, so they hold
+        // exactly that row's results and store the same bits to the same place.
+        // 8-bit weights: each weight row's scale multiplies its accumulators.
+#pragma unroll
+        for (int mt = 0; mt < NMT; ++mt) {
+            if (UP) {
+                const int mloc = (wm * NMT + mt) * 32 + (lane & 31);
+                const int64_t rrow = cur.row0 + cur.m0 + (mloc < cur.Mp ? mloc : cur.Mp - 1);
+                const int n0 = cur.nb * C::NOUT + wr * 64 + 4 * (lane >> 5);
+                bf16_t* hrow = p.h_out + rrow * p.N + n0;
+#pragma unroll
+                for (int h = 0; h < 2; ++h) {
+                    // the accumulators are redefined here (in their AGPRs), so
+                    // their copies into VGPRs cannot move above this point
+                    asm volatile("" : "+a"(acc[h][mt]), "+a"(acc[h + 2][mt]));
+                    floatx16 u = acc[h][mt];
+                    floatx16 v = acc[h + 2][mt];
+                    if constexpr (F8) {
+#pragma unroll
+                        for (int q = 0; q < 4; ++q)
+#pragma unroll
+                            for (int i = 0; i < 4; ++i) {
+                                u[4 * q + i] *= sc[h][q][i];
+                                v[4 * q + i] *= sc[h + 2][q][i];
+                            }
+                    }
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        uint2 pk;
+                        pk.x = pack_bf16x2(silu(u[4 * q + 0]) * v[4 * q + 0], silu(u[4 * q + 1]) * v[4 * q + 1]);
+                        pk.y = pack_bf16x2(silu(u[4 * q + 2]) * v[4 * q + 2], silu(u[4 * q + 3]) * v[4 * q + 3]);
+                        *reinterpret_cast<uint2*>(hrow + h * 32 + 8 * q) = pk;
+                    }
+                    __builtin_amdgcn_sched_barrier(0);
+                }
+            } else {
+                int orow_mt = cur.orow[mt];
+                float gw = cur.gw[mt];
+                // (kept here: computed before the steps, the row addresses
+                // would occupy registers through all of them)
+                asm volatile("" : "+v"(orow_mt), "+v"(gw));
+                const int64_t orow = orow_mt;
+                const int n0 = cur.nb * C::NOUT + wr * 128 + 4 * (lane >> 5);
+                float* yrow = p.y_out + cur.part * p.slice + orow * p.N + n0;
+#pragma unroll
+                for (int nt = 0; nt < NT; ++nt) {
+                    asm volatile("" : "+a"(acc[nt][mt]));
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        floatx4 g4 = {gw, gw, gw, gw};
+                        if constexpr (F8) g4 = g4 * sc[nt][q];
+                        float4 v;
+                        v.x = g4[0] * acc[nt][mt][4 * q + 0];
+                        v.y = g4[1] * acc[nt][mt][4 * q + 1];
+                        v.z = g4[2] * acc[nt][mt][4 * q + 2];
+                        v.w = g4[3] * acc[nt][mt][4 * q + 3];
+                        *reinterpret_cast<float4*>(yrow + nt * 32 + 8 * q) = v;
+                    }
+                    __builtin_amdgcn_sched_barrier(0);
+                }
             }
-        };
-        static_assert(MT == 4, "the tile variants cover 1 to 4 blocks per wave");
-        if (Mp <= 64)
+        }
+    };
+    static_assert(MT == 4, "the tile variants cover 1 to 4 blocks per wave");
+
+    if (w >= end) return;
+    index_item(w, cur);
+    fetch_rows(cur);
+    prologue(cur, false);
+    while (true) {
+        const int wn = w + per_xcd;
+        more = wn < end;
+        if (more) {
+            index_item(wn, nxt);
+            fetch_rows(nxt);
+        }
+        pipe = more && cur.kn >= 3;
+        if (cur.Mp <= 64)
             tile(std::integral_constant<int, 1>{});
-        else if (Mp <= 128)
+        else if (cur.Mp <= 128)
             tile(std::integral_constant<int, 2>{});
-        else if (Mp <= 192)
+        else if (cur.Mp <= 192)
             tile(std::integral_constant<int, 3>{});
         else
             tile(std::integral_constant<int, 4>{});
-
-        // the next tile's loads reuse the rings: redundant tail loads and this
-        // tile's stores must be done, and every wave past its last read
-        wait_vmem<0>();
-        __syncthreads();
+        if (!more) break;
+        if (!pipe) {
+            // the ring is reused from scratch: this item's tail loads and
+            // stores done, every wave past its last read
+            wait_vmem<0>();
+            __syncthreads();
+            prologue(nxt, true);
+        }
+        cur = nxt;
+        w = wn;
     }
+    // no global->LDS load may still be in flight when the workgroup ends
+    wait_vmem<0>();
 }
 
 // persistent grid: one workgroup per CU, fewer for fewer items (a bound:
@@ -645,10 +770,13 @@ int cu_count()
 
 }  // namespace
 
-bool tiled_supported(int d, int ffn)
+// rows: token rows of the largest activation buffer the tiled kernels read
+// (x, the permuted rows or h); they address it with 32-bit byte offsets
+bool tiled_supported(int d, int ffn, int64_t rows)
 {
     return ffn % QCfg<true, false>::NOUT == 0 && d % QCfg<false, false>::NOUT == 0 &&
-           d % QCfg<true, false>::BK == 0 && ffn % QCfg<false, false>::BK == 0;
+           d % QCfg<true, false>::BK == 0 && ffn % QCfg<false, false>::BK == 0 &&
+           rows * 2 * (d > ffn ? d : ffn) < (int64_t(1) << 32);
 }
 
 hipError_t launch_tiled_up(const UpArgs& a, hipStream_t stream)
