@@ -3,12 +3,16 @@
 // The router of a Mixtral MoE layer (the model of the paper's engine, Sec. 4.1)
 // scores every token against every expert, keeps the k best experts and
 // weights them with a softmax over the kept scores.  Here:
-//   * one workgroup (8 wave64) per token, or per 64 / E tokens for long
-//     inputs: each lane multiplies 16-byte chunks of x against the same chunk
-//     of every expert's router row, accumulating in f32; the per-(token,
-//     expert) partial sums are combined by a transposed wave butterfly and a
+//   * up to 256 tokens (and for more than 16 experts): one workgroup (8
+//     wave64) per token, or per 64 / E tokens for long inputs: each lane
+//     multiplies 16-byte chunks of x against the same chunk of every
+//     expert's router row, accumulating in f32; the per-(token, expert)
+//     partial sums are combined by a transposed wave butterfly and a
 //     fixed-order sum over the waves, so results are bitwise reproducible and
 //     the same for any tokens per workgroup;
+//   * more tokens, up to 16 experts: 16 tokens per workgroup on the matrix
+//     cores (16x16x32 bf16 MFMAs, f32 accumulation), the reduction split over
+//     16 waves and their partial tiles summed in a fixed order;
 //   * the top k are then ranked on the key (logit, -expert) -- equal logits
 //     pick the lower expert -- by one lane for up to 16 experts, or by a
 //     wave-wide arg-max butterfly for more, and the softmax over the selected
