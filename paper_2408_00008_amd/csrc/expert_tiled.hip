@@ -509,12 +509,10 @@ __global__ __launch_bounds__(256) void q_kernel(TiledParams p)
         }
 
         // Step j, k-step ks: its NT x NMT MFMAs use the fragments in
-        // register slot ks & 1, and one memory operation follows each of
-        // the first MFMAs (several where a k-step has more memory
-        // operations than MFMAs): first the
-        // reads of the next k-step's fragments into the other slot (so they
-        // are complete long before that k-step starts), then this
-        // k-step's share of the loads: A(j+2) in k-steps 0 and 1, B(j+2) in
+        // register slot ks & 1, and memory operations follow the MFMAs:
+        // first the reads of the next k-step's fragments into the other
+        // slot, two per MFMA (so they are complete long before that k-step
+        // starts), then this k-step's share of the loads: A(j+2) in k-steps 0 and 1, B(j+2) in
         // k-step 3.  8-bit weights read their raw bytes a pair of k-steps
         // at a time (k-step 0: pair 1 of step j; k-step 3: pair 0 of step
         // j+1) and widen them to bf16 before the MFMAs of each weight tile.
@@ -580,11 +578,18 @@ __global__ __launch_bounds__(256) void q_kernel(TiledParams p)
                         }
                     }
                     acc[g][m] = mfma32x32x16(a, fb[cur_s][m], acc[g][m]);
-                    // extra x after MFMA x (after MFMA x * M / X when
-                    // there are more extras than MFMAs)
+                    // the fragment reads two after each of the first MFMAs,
+                    // then the loads spread over the remaining ones: the
+                    // next k-step waits for all of this one's reads, and
+                    // reads issued one per MFMA left too little time for
+                    // them behind the other waves' reads and the
+                    // global->LDS writes (prefill up GEMM 3.7% slower)
                     static_for<X>([&](auto x_tag) {
                         constexpr int x = decltype(x_tag)::value;
-                        if constexpr ((X <= M ? x : x * M / X) == i) extra(x_tag);
+                        constexpr int h = (NR + 1) / 2;
+                        constexpr int at = x < NR ? x / 2 : h + (x - NR) * (M - h) / (NLD > 0 ? NLD : 1);
+                        static_assert(at < M, "every extra follows an MFMA");
+                        if constexpr (at == i) extra(x_tag);
                     });
                     fence();
                 });
