@@ -17,9 +17,11 @@
 //     pick the lower expert -- by one lane for up to 16 experts, or by a
 //     wave-wide arg-max butterfly for more, and the softmax over the selected
 //     logits is formed in f32;
-//   * a single-workgroup dispatch kernel builds the expert histogram (LDS
-//     atomics), its exclusive scan, and the stable expert-major permutation
-//     with wave ballots (rank among equal experts = popcount of lower lanes).
+//   * a single-workgroup dispatch kernel builds the expert histogram, its
+//     exclusive scan and the stable expert-major permutation: up to 1024
+//     assignments one per thread (LDS-atomic histogram, ranks among equal
+//     experts by wave ballots), more eight per thread (packed per-thread
+//     counts and wave prefix sums).
 #include "common.hpp"
 #include "launch.hpp"
 
@@ -422,6 +424,158 @@ __global__ __launch_bounds__(DISPATCH_THREADS) void dispatch_kernel(
     }
 }
 
+// Dispatch with 8 consecutive assignments per thread: one workgroup places
+// up to 8192 assignments between two barriers.  Every thread counts its
+// assignments per expert, packed three experts to a 32-bit word (10 bits
+// each: a wave holds at most 512 of one expert), the waves take inclusive
+// prefix sums of the packed words by shuffles, one wave scans the wave
+// totals per expert, and each assignment goes to
+//   offsets[e] + (chunks before) + (waves before) + (lanes before) + (its
+//   rank among the thread's earlier assignments of e),
+// which is the stable expert-major order.  Inputs longer than 8192
+// assignments take a counting pass first and place chunk by chunk.
+constexpr int D8_THREADS = 1024;
+constexpr int D8_WAVES = D8_THREADS / 64;
+constexpr int D8_PER = 8;
+constexpr int D8_CHUNK = D8_THREADS * D8_PER;
+constexpr int D8_MAXW = 22;  // packed words for up to 64 experts
+
+template <int NW>
+__device__ __forceinline__ void d8_pack(const int (&id)[D8_PER], uint32_t (&pk)[NW])
+{
+#pragma unroll
+    for (int w = 0; w < NW; ++w) {
+        uint32_t v = 0;
+#pragma unroll
+        for (int i = 0; i < D8_PER; ++i) {
+            const int d = id[i] - 3 * w;
+            v += (id[i] >= 0 && d >= 0 && d < 3) ? (1u << (10 * d)) : 0u;
+        }
+        pk[w] = v;
+    }
+}
+
+template <int NW>
+__device__ __forceinline__ int d8_field(const uint32_t (&pk)[NW], int e)
+{
+    int r = 0;
+#pragma unroll
+    for (int w = 0; w < NW; ++w)
+        if (e / 3 == w) r = (pk[w] >> (10 * (e - 3 * w))) & 1023;
+    return r;
+}
+
+template <int NW>
+__global__ __launch_bounds__(D8_THREADS) void dispatch8_kernel(const int32_t* __restrict__ ids, int64_t A,
+                                                              int E, int32_t* __restrict__ offsets,
+                                                              int32_t* __restrict__ perm)
+{
+    __shared__ int wtot[D8_WAVES][64];   // per wave and expert, this chunk
+    __shared__ int ebase[64];            // next position of each expert
+    __shared__ int etot[64];             // whole-input counts (multi-chunk)
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int64_t nchunk = (A + D8_CHUNK - 1) / D8_CHUNK;
+    if (nchunk == 0) {
+        if (tid <= E) offsets[tid] = 0;
+        return;
+    }
+    auto load = [&](int64_t c, int (&id)[D8_PER]) {
+        const int64_t a0 = c * D8_CHUNK + (int64_t)tid * D8_PER;
+#pragma unroll
+        for (int i = 0; i < D8_PER; ++i) {
+            // ids come from the router and lie in [0, E); the clamp keeps a
+            // corrupted id from indexing past the histogram
+            id[i] = a0 + i < A ? min(max(ids[a0 + i], 0), E - 1) : -1;
+        }
+    };
+    // wave-inclusive prefix of the packed counts; wtot gets the wave totals
+    auto wave_scan = [&](uint32_t (&pk)[NW]) {
+#pragma unroll
+        for (int w = 0; w < NW; ++w) {
+#pragma unroll
+            for (int o = 1; o < 64; o <<= 1) {
+                const uint32_t v = __shfl_up(pk[w], o, 64);
+                if (lane >= o) pk[w] += v;
+            }
+        }
+        if (lane == 63) {
+            for (int e = 0; e < E; ++e) wtot[wave][e] = d8_field<NW>(pk, e);
+        }
+    };
+    int id[D8_PER];
+    uint32_t pk[NW];
+    if (nchunk > 1) {
+        // counting pass: whole-input totals per expert
+        if (tid < 64) etot[tid] = 0;
+        for (int64_t c = 0; c < nchunk; ++c) {
+            load(c, id);
+            d8_pack<NW>(id, pk);
+            wave_scan(pk);
+            __syncthreads();
+            if (tid < E) {
+                int t = 0;
+                for (int w = 0; w < D8_WAVES; ++w) t += wtot[w][tid];
+                etot[tid] += t;
+            }
+            __syncthreads();
+        }
+    }
+    for (int64_t c = 0; c < nchunk; ++c) {
+        load(c, id);
+        d8_pack<NW>(id, pk);
+        uint32_t own[NW];
+#pragma unroll
+        for (int w = 0; w < NW; ++w) own[w] = pk[w];
+        wave_scan(pk);
+        __syncthreads();
+        if (wave == 0) {
+            // lane e: the chunk's count of expert e and the waves' exclusive bases
+            int run = 0;
+            if (lane < E) {
+                for (int w = 0; w < D8_WAVES; ++w) {
+                    const int t = wtot[w][lane];
+                    wtot[w][lane] = run;
+                    run += t;
+                }
+            }
+            if (c == 0) {
+                // expert offsets: exclusive scan of the whole-input counts
+                const int cnt = lane < E ? (nchunk > 1 ? etot[lane] : run) : 0;
+                int incl = cnt;
+#pragma unroll
+                for (int o = 1; o < 64; o <<= 1) {
+                    const int v = __shfl_up(incl, o, 64);
+                    if (lane >= o) incl += v;
+                }
+                if (lane < E) {
+                    offsets[lane] = incl - cnt;
+                    ebase[lane] = incl - cnt;
+                }
+                if (lane == E - 1) offsets[E] = incl;
+            }
+            // (wtot now holds the waves' bases; etot the chunk's counts,
+            // added to ebase after the placement)
+            if (lane < E) etot[lane] = run;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int i = 0; i < D8_PER; ++i) {
+            const int e = id[i];
+            if (e >= 0) {
+                int r = 0;
+#pragma unroll
+                for (int i2 = 0; i2 < i; ++i2) r += id[i2] == e;
+                const int pre = d8_field<NW>(pk, e) - d8_field<NW>(own, e);  // lanes before
+                const int64_t a = c * D8_CHUNK + (int64_t)tid * D8_PER + i;
+                perm[ebase[e] + wtot[wave][e] + pre + r] = static_cast<int32_t>(a);
+            }
+        }
+        __syncthreads();
+        if (tid < E) ebase[tid] += etot[tid];
+        __syncthreads();
+    }
+}
+
 }  // namespace
 
 hipError_t launch_router_topk(const bf16_t* x, const bf16_t* router_w, const float* bias,
@@ -470,7 +624,22 @@ hipError_t launch_router_topk(const bf16_t* x, const bf16_t* router_w, const flo
 hipError_t launch_dispatch(const int32_t* topk_ids, int64_t A, int E, int32_t* offsets,
                            int32_t* perm, hipStream_t stream)
 {
-    dispatch_kernel<<<1, DISPATCH_THREADS, 0, stream>>>(topk_ids, A, E, offsets, perm);
+    // up to 1024 assignments (decode steps) the one-per-thread kernel, with
+    // one chunk and no counting pass; above, 8 per thread (Mixtral layer,
+    // 8192 assignments: route + dispatch 27.9 -> 19.3 us; 128 assignments:
+    // 10.4-11.0 us one per thread, 12.0 us eight per thread)
+    if (A <= DISPATCH_THREADS) {
+        dispatch_kernel<<<1, DISPATCH_THREADS, 0, stream>>>(topk_ids, A, E, offsets, perm);
+        return hipGetLastError();
+    }
+#define MOE_D8(NW_) dispatch8_kernel<NW_><<<1, D8_THREADS, 0, stream>>>(topk_ids, A, E, offsets, perm)
+    if (E <= 9)
+        MOE_D8(3);
+    else if (E <= 18)
+        MOE_D8(6);
+    else
+        MOE_D8(D8_MAXW);
+#undef MOE_D8
     return hipGetLastError();
 }
 
