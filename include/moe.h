@@ -133,12 +133,19 @@ moe_status_t moe_swiglu_down(const moe_bf16_t* h, const int32_t* expert_offsets,
  * scattered as in moe_swiglu_down.  The number of parts used (a power of two
  * up to 16, at most max_parts, each part at least 512 elements of ffn) is
  * chosen on the device from the routed row counts and stored to *parts
- * (device int32, 4-byte aligned).  In the streaming regime (up to 64 rows per
+ * (device int32, 4-byte aligned).  Where max_parts >= 4 and slices 1 ..
+ * max_parts-1 together hold at least 256 x 65536 floats plus a 4 KiB table
+ * (prefill sizes), the tiles are instead left uncut and only the tiles of
+ * the persistent grid's last, partial round are split across its idle
+ * workgroups; those pieces go to slices 1.. as scratch and a second kernel
+ * adds them into slice 0 (in piece order), so *parts = 1 on return and the
+ * rest of slices 1.. holds scratch.  In the streaming regime (up to 64 rows per
  * expert on average) with T > 64, the experts holding more than 64 rows take
  * the cut tiled kernel and their slices are then added into slice 0 in
  * ascending order, so *parts = 1 on return; the other experts stream uncut
- * into slice 0.  Where only the streaming kernel runs, *parts = 1.  Slices at
- * or past the count used are left as they were.  moe_combine_parts sums the
+ * into slice 0.  Where only the streaming kernel runs, *parts = 1.  Except
+ * with the tail split, slices at or past the count used are left as they
+ * were.  moe_combine_parts sums the
  * slices; moe_forward runs this pair.  Errors as moe_swiglu_down, and
  * MOE_ERR_INVALID_ARG for max_parts < 1 or parts NULL.
  */

@@ -65,7 +65,15 @@ struct TiledParams {
     int64_t slice;
     int* ksplit_out;
     int64_t A;
+    // DOWN, tail split (see the kernel): tiles uncut, the last round's tiles
+    // split across the workgroups; the pieces after each tile's first go to
+    // y_out + slice (kTailPiece floats each, one slot per workgroup), a table
+    // of the split tiles after them
+    int tail;
 };
+
+// one piece of a split tile: 256 rows x 256 columns of f32
+constexpr int kTailPiece = 256 * 256;
 
 int cu_count();
 
@@ -193,7 +201,7 @@ __global__ __launch_bounds__(256) void q_kernel(TiledParams p)
     // the step counts and branches derived from them, in scalar registers)
     auto uni = [](int v) { return __builtin_amdgcn_readfirstlane(v); };
     const int all_tiles = uni(__shfl(in_tiles, p.E - 1, 64));
-    const int nparts = UP ? 1 : uni(down_parts(nbn * all_tiles, per_xcd, nk, p.A, p.N, p.ksplit_max));
+    const int nparts = (UP || p.tail) ? 1 : uni(down_parts(nbn * all_tiles, per_xcd, nk, p.A, p.N, p.ksplit_max));
     if (!UP && p.ksplit_out && blockIdx.x == 0 && tid == 0) *p.ksplit_out = nparts;
     const int ex_items = nparts * nbn * (in_tiles - my_tiles);
     const int total = nparts * nbn * all_tiles;
@@ -238,6 +246,22 @@ __global__ __launch_bounds__(256) void q_kernel(TiledParams p)
     const int beg = __builtin_amdgcn_readfirstlane(first_item_at((ctot * xcd + 7) / 8));
     const int end = __builtin_amdgcn_readfirstlane(
         xcd == 7 ? total : first_item_at((ctot * (xcd + 1) + 7) / 8));
+    // The workgroups of an XCD take its items in rounds (workgroup j: items
+    // j, j + P, j + 2P, ...).  DOWN with tail split: the last, partial round
+    // of rem < P tiles would leave P - rem workgroups idle for a whole tile,
+    // so each of those tiles is cut into `pieces` = P / rem reduction ranges
+    // taken by consecutive workgroups; piece 0 writes the tile's output as
+    // usual, the others write f32 pieces that fold_tail_kernel adds to it.
+    const int n_xcd = end - beg;
+    const int rounds = n_xcd / per_xcd;
+    const int rem = (!UP && p.tail) ? n_xcd - rounds * per_xcd : 0;
+    // (at most one piece per reduction step: every piece has a step)
+    const int pieces = rem > 0 ? min(per_xcd / rem, nk) : 1;
+    const int units = rem > 0 ? rounds + (local < rem * pieces ? 1 : 0)
+                              : (local < n_xcd ? (n_xcd - local + per_xcd - 1) / per_xcd : 0);
+    int* const tail_tab = (!UP && p.tail)
+        ? reinterpret_cast<int*>(p.y_out + p.slice + (int64_t)gridDim.x * kTailPiece) : nullptr;
+    if (tail_tab && local == 0 && tid == 0) tail_tab[4 * gridDim.x + xcd] = pieces > 1 ? rem : 0;
 
     // a token load covers 8 rows starting at a multiple of 8: lane l takes row
     // l / 8 and the global chunk stored at slot l % 8 (odd loads start at 8
@@ -287,12 +311,21 @@ __global__ __launch_bounds__(256) void q_kernel(TiledParams p)
     // a barrier and a fresh prologue.
     struct Item {
         int e, part, nb, k0, kn, row0, m0, Mp;
+        int slot;      // DOWN tail split: this workgroup's piece slot, or -1 (output to y)
         int src[L];    // this lane's token rows of its L token loads (UP: gathered slot ids)
         int orow[4];   // DOWN: output row of each epilogue column block
         float gw[4];   // DOWN: its gate weight
     };
-    // the uniform part of item w
-    auto index_item = [&](int w, Item& it) {
+    // the uniform part of this workgroup's u-th unit of work: item
+    // beg + local + u P, or in the tail-split round a piece of a tile
+    auto index_item = [&](int u, Item& it) {
+        int w = beg + local + u * per_xcd;
+        int pc = 0;
+        if (u == rounds && rem > 0) {
+            const int i = local / pieces;
+            pc = local - i * pieces;
+            w = beg + rounds * per_xcd + i;
+        }
         const uint64_t le = __ballot(lane < p.E && my_tiles > 0 && ex_items <= w);
         const int e = 63 - __builtin_clzll(le);
         const int mt_e = uni(__shfl(my_tiles, e, 64));
@@ -304,8 +337,19 @@ __global__ __launch_bounds__(256) void q_kernel(TiledParams p)
         it.e = e;
         it.part = part;
         it.nb = nb;
-        it.k0 = (int)((int64_t)nk * part / nparts);
-        it.kn = (int)((int64_t)nk * (part + 1) / nparts) - it.k0;
+        const bool tail_unit = u == rounds && rem > 0;
+        const int np = tail_unit ? pieces : nparts;  // (tail split: nparts = 1)
+        const int pp = tail_unit ? pc : part;
+        it.k0 = (int)((int64_t)nk * pp / np);
+        it.kn = (int)((int64_t)nk * (pp + 1) / np) - it.k0;
+        it.slot = pc > 0 ? (int)blockIdx.x : -1;
+        if (tail_unit && pc == 0 && pieces > 1 && tid == 0) {
+            int* t = tail_tab + 4 * (xcd * per_xcd + (local / pieces));
+            t[0] = e;
+            t[1] = nb;
+            t[2] = mtile;
+            t[3] = pieces;
+        }
         it.row0 = uni(__shfl(my_off, e, 64));
         it.m0 = mtile * C::BM;
         it.Mp = min(C::BM, uni(__shfl(my_rows, e, 64)) - it.m0);
@@ -418,7 +462,7 @@ __global__ __launch_bounds__(256) void q_kernel(TiledParams p)
     };
 
     Item cur, nxt;
-    int w = beg + local;
+    int u = 0;
     bool more = false, pipe = false;
 
     // The tile body for NMT multiplied 32-token column blocks per wave
@@ -663,7 +707,13 @@ __global__ __launch_bounds__(256) void q_kernel(TiledParams p)
                 asm volatile("" : "+v"(orow_mt), "+v"(gw));
                 const int64_t orow = orow_mt;
                 const int n0 = cur.nb * C::NOUT + wr * 128 + 4 * (lane >> 5);
-                float* yrow = p.y_out + cur.part * p.slice + orow * p.N + n0;
+                // (a split tile's later pieces: tile-local rows of 256 in
+                // this workgroup's slot; a select, not a branch)
+                const int mloc = (wm * NMT + mt) * 32 + (lane & 31);
+                float* const ypiece = p.y_out + p.slice + (int64_t)(cur.slot < 0 ? 0 : cur.slot) * kTailPiece +
+                                      mloc * 256 + (n0 - cur.nb * C::NOUT);
+                float* const yout = p.y_out + cur.part * p.slice + orow * p.N + n0;
+                float* yrow = cur.slot < 0 ? yout : ypiece;
 #pragma unroll
                 for (int nt = 0; nt < NT; ++nt) {
                     asm volatile("" : "+a"(acc[nt][mt]));
@@ -685,15 +735,14 @@ __global__ __launch_bounds__(256) void q_kernel(TiledParams p)
     };
     static_assert(MT == 4, "the tile variants cover 1 to 4 blocks per wave");
 
-    if (w >= end) return;
-    index_item(w, cur);
+    if (units == 0) return;
+    index_item(0, cur);
     fetch_rows(cur);
     prologue(cur, false);
     while (true) {
-        const int wn = w + per_xcd;
-        more = wn < end;
+        more = u + 1 < units;
         if (more) {
-            index_item(wn, nxt);
+            index_item(u + 1, nxt);
             fetch_rows(nxt);
         }
         pipe = more && cur.kn >= 3;
@@ -714,10 +763,56 @@ __global__ __launch_bounds__(256) void q_kernel(TiledParams p)
             prologue(nxt, true);
         }
         cur = nxt;
-        w = wn;
+        ++u;
     }
     // no global->LDS load may still be in flight when the workgroup ends
     wait_vmem<0>();
+}
+
+// Adds the later pieces of every tile that the down GEMM split in its last
+// round (table written by the tiles' first pieces) to the tile's output in
+// y: rows scattered through perm as in the down epilogue, the gate weights
+// already applied, pieces added in order after piece 0's value.  Workgroup
+// (slot, block of 16 rows), slot = xcd * P + i for split tile i of an XCD
+// (grid = the down launch's grid x 16); each thread 4 rows of one 16-byte
+// column chunk, all loads of a row issued together.
+constexpr int kFoldRows = 16;
+__global__ __launch_bounds__(256) void fold_tail_kernel(float* __restrict__ y, int64_t slice,
+                                                        const int32_t* __restrict__ offsets,
+                                                        const int32_t* __restrict__ perm,
+                                                        const float* __restrict__ topk_w, int N,
+                                                        int q_grid)
+{
+    const int per_xcd = q_grid >> 3;
+    const int b = blockIdx.x / (256 / kFoldRows);
+    const int rb = blockIdx.x - b * (256 / kFoldRows);
+    const int xcd = b / per_xcd, i = b - xcd * per_xcd;
+    const float* pieces = y + slice;
+    const int* tab = reinterpret_cast<const int*>(pieces + (int64_t)q_grid * kTailPiece);
+    if (i >= tab[4 * q_grid + xcd]) return;
+    const int e = tab[4 * b], nb = tab[4 * b + 1], mtile = tab[4 * b + 2], np = tab[4 * b + 3];
+    const int row0 = offsets[e] + mtile * 256;
+    const int Mp = min(256, offsets[e + 1] - row0);
+    const int c4 = threadIdx.x & 63;
+#pragma unroll
+    for (int j = 0; j < kFoldRows / 4; ++j) {
+        const int lr = rb * kFoldRows + 4 * j + (threadIdx.x >> 6);
+        if (lr >= Mp) continue;
+        const int64_t a = (topk_w && perm) ? perm[row0 + lr] : row0 + lr;
+        float4* yr = reinterpret_cast<float4*>(y + a * N + nb * 256) + c4;
+        float4 v = *yr;
+        for (int pc = 1; pc < np; ++pc) {
+            // piece pc of tile i was computed by workgroup (i np + pc) * 8 + xcd
+            const int slot = (i * np + pc) * 8 + xcd;
+            const float4 w =
+                reinterpret_cast<const float4*>(pieces + (int64_t)slot * kTailPiece + lr * 256)[c4];
+            v.x += w.x;
+            v.y += w.y;
+            v.z += w.z;
+            v.w += w.w;
+        }
+        *yr = v;
+    }
 }
 
 // persistent grid: one workgroup per CU, fewer for fewer items (a bound:
@@ -833,7 +928,18 @@ hipError_t launch_tiled_down(const DownArgs& a, hipStream_t stream)
     p.slice = a.A * a.d;
     p.ksplit_out = a.ksplit_out;
     p.A = a.A;
-    return a.q2 ? run_q<false, true>(p, a.A, stream) : run_q<false, false>(p, a.A, stream);
+    // Tail split where the caller's slices 1.. hold a piece per workgroup and
+    // the table (the prefill shapes): the tiles stay uncut, so the combine
+    // reads one slice; otherwise the reduction may be cut into uniform parts.
+    const int grid = q_grid<false>(a.d, a.E, a.A, p.ksplit_max);
+    p.tail = (p.ksplit_max >= 4 && a.ksplit_out && a.offsets &&
+              (int64_t)(p.ksplit_max - 1) * p.slice >= (int64_t)grid * kTailPiece + 4 * grid + 8)
+                 ? 1 : 0;
+    hipError_t e = a.q2 ? run_q<false, true>(p, a.A, stream) : run_q<false, false>(p, a.A, stream);
+    if (e != hipSuccess || !p.tail) return e;
+    fold_tail_kernel<<<static_cast<unsigned>(grid * (256 / kFoldRows)), 256, 0, stream>>>(
+        a.y, p.slice, a.offsets, a.topk_w ? a.perm : nullptr, a.topk_w, a.d, grid);
+    return hipGetLastError();
 }
 
 }  // namespace moe

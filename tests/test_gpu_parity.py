@@ -273,6 +273,10 @@ def test_forward_split_by_rows(shape):
     ((288, 256, 2048, 8, 2), 4),   # one token tile per expert, 4 parts of 8 steps
     ((600, 512, 1024, 8, 2), 2),   # 2 weight blocks per expert, 2 parts of 8 steps
     ((600, 256, 2048, 64, 8), None),  # E = 64, k = 8: 64 ragged tiles (count not pinned)
+    # slices large enough for the tail split: tiles uncut (count 1), the
+    # last round's tiles (here all of them: ~12 per XCD) cut in 2 pieces
+    # across the workgroups and folded back into slice 0
+    ((3000, 1024, 2048, 8, 2), 1),
 ])
 def test_forward_down_split(shape, parts):
     """Prefill-regime sizes with few token tiles: the tiled down GEMM cuts its
@@ -390,6 +394,17 @@ def test_forward_tiled_parts_graph():
     the bits of the eager runs, which match the oracle."""
     say("[forward] tiled step with reduction parts: graph capture")
     c = small_case(288, 256, 2048, 8, 2, seed=38)
+    assert B.moe_gemm_variant_for(c.T, c.d, c.ffn, c.E, c.k) == 2
+    _forward_check(c, variant=0)
+    _graph_replays_match_eager(c)
+
+
+def test_forward_tiled_tail_graph():
+    """A prefill-regime step whose down GEMM splits its last round's tiles
+    across workgroups (pieces folded back by a second kernel): graph replays
+    give the bits of the eager runs, which match the oracle."""
+    say("[forward] tiled step with a split last round: graph capture")
+    c = small_case(3000, 1024, 2048, 8, 2, seed=39)
     assert B.moe_gemm_variant_for(c.T, c.d, c.ffn, c.E, c.k) == 2
     _forward_check(c, variant=0)
     _graph_replays_match_eager(c)
