@@ -443,6 +443,8 @@ bool split_by_rows(int64_t rows_max, int64_t A, int E)
 hipError_t run_up(const moe::UpArgs& a, int64_t T, hipStream_t stream, bool side = true)
 {
     const int64_t rmax = rows_bound(T, a.kslots);
+    // routing from the top-k ids exists on the streaming kernel only
+    if (a.ids) return moe::launch_stream_up(a, rmax, stream);
     const bool tiled_ok = moe::tiled_supported(a.d, a.ffn, a.A);
     if (split_by_rows(rmax, a.A, a.E)) {
         moe::UpArgs light = a, heavy = a;
@@ -475,6 +477,7 @@ hipError_t run_down(const moe::DownArgs& a, int64_t T, int32_t k, hipStream_t st
         return moe::launch_fill_i32(a.ksplit_out, 1, stream);
     };
     const int64_t rmax = rows_bound(T, k);
+    if (a.ids) return uncut(moe::launch_stream_down(a, rmax, stream));
     if (split_by_rows(rmax, a.A, a.E)) {
         moe::DownArgs light = a, heavy = a;
         light.mhi = kLightRows;
@@ -668,14 +671,31 @@ moe_status_t forward_impl(const moe_bf16_t* x, const moe_bf16_t* router_w,
     hipError_t e = moe::launch_router_topk(x, router_w, router_bias, T, d, E, k, ids, gw, nullptr,
                                            stream);
     if (e != hipSuccess) return hip_fail(e, "router kernel launch");
-    e = moe::launch_dispatch(ids, A, E, offs, perm, stream);
-    if (e != hipSuccess) return hip_fail(e, "dispatch kernel launch");
+    // Both GEMMs on the streaming kernels and few assignments: each of their
+    // workgroups builds the expert offsets and row order from the top-k ids
+    // in LDS, and no dispatch kernel runs.
+    const bool by_ids = A <= moe::kStreamListMax && !split_by_rows(rows_bound(T, k), A, E) &&
+                        moe::resolve_variant(g_variant.load(), A, E) == moe::VARIANT_STREAM;
+    if (!by_ids) {
+        e = moe::launch_dispatch(ids, A, E, offs, perm, stream);
+        if (e != hipSuccess) return hip_fail(e, "dispatch kernel launch");
+    }
     moe::UpArgs ua{x, perm, k, offs, w.w1, w.w3, h, A, d, ffn, E};
     ua.q1 = w.q1, ua.s1 = w.s1, ua.q3 = w.q3, ua.s3 = w.s3;
+    if (by_ids) {
+        ua.ids = ids;
+        ua.gather = nullptr;
+        ua.offsets = nullptr;
+    }
     e = run_up(ua, T, stream, side);
     if (e != hipSuccess) return hip_fail(e, "expert up kernel launch");
     moe::DownArgs da{h, offs, w.w2, gw, perm, y, A, d, ffn, E};
     da.q2 = w.q2, da.s2 = w.s2;
+    if (by_ids) {
+        da.ids = ids;
+        da.perm = nullptr;
+        da.offsets = nullptr;
+    }
     da.ksplit_max = L.nsplit;
     // the part count is only needed (and only written) where y has slices
     da.ksplit_out = L.nsplit > 1 ? reinterpret_cast<int*>(b + L.ns) : nullptr;

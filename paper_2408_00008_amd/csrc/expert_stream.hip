@@ -26,16 +26,24 @@
 //     order, so results are bitwise reproducible.
 //
 // Per-expert row counts come from the device-side offsets; experts with no
-// rows exit at once and no host synchronisation is needed.  An expert with
-// more than 16*G rows is cut into several passes over its slab, which run as
-// separate workgroups placed to share the slab's weights through L2.  With
-// null offsets the kernels take one matrix of all rows (a dense projection).
+// rows exit at once and no host synchronisation is needed.  Up to 1024
+// assignments a workgroup keeps the routing in LDS: the offsets and the row
+// order are read in one round trip, or built from the top-k ids (counts by
+// LDS atomics, each row's place by wave ballots, the stable expert-major
+// order of the dispatch), so that a decode step needs no dispatch kernel.  An
+// expert with more than 16*G rows is cut into several passes over its slab,
+// which run as separate workgroups placed to share the slab's weights through
+// L2.  With null offsets and no ids the kernels take one matrix of all rows (a
+// dense projection).
 #include "common.hpp"
 #include "launch.hpp"
 
 namespace moe {
 
 namespace {
+
+// assignments (tokens x k) up to which the routing tables live in LDS
+constexpr int kListMax = kStreamListMax;
 
 struct StreamParams {
     const bf16_t* act;       // token rows (UP: x, DOWN: h)
@@ -57,6 +65,11 @@ struct StreamParams {
     int passes;              // workgroups per slab (each takes every passes-th pass)
     int mlo, mhi;            // experts with mlo <= rows <= mhi only
     int rows;                // dense (offsets null): one matrix, rows [0, rows)
+    // top-k expert of each assignment [A] (A <= kListMax): the row offsets
+    // and the expert-major row order are built in LDS from them, and
+    // offsets / gather / perm are not read
+    const int32_t* ids;
+    int A;                   // assignments (rows of all experts)
 };
 
 // rows of expert e and its first row (dense: one matrix holding every row)
@@ -98,6 +111,11 @@ struct ChunkRegs {
 
 struct PassCtx {
     int e, n0, row0, m0, Mp, ks, ns, gt, lane, kbeg, nchunks, rot;
+    // the assignment behind each expert-major row, in LDS (null: read perm /
+    // gather from global memory); gather: UP rows come from x[assignment / k];
+    // scatter: DOWN rows go to y[assignment], gate-weighted
+    const int* list;
+    bool gather, scatter;
     const bf16_t* pa;
     const bf16_t* pb;
     const uint8_t* qa;  // 8-bit kernels: this lane's weight bytes
@@ -143,7 +161,8 @@ __device__ __forceinline__ void stream_pass(const StreamParams& p, unsigned char
         const int c8 = live ? q % (KC / 8) : 0;
         const int mm = m < x.Mp ? m : x.Mp - 1;  // rows past the end repeat the last row
         const int r = x.row0 + x.m0 + mm;
-        const int64_t sr = (UP && p.gather) ? p.gather[r] / p.kslots : r;
+        int64_t sr = r;
+        if (UP && x.gather) sr = (x.list ? x.list[r] : p.gather[r]) / p.kslots;
         src[it] = p.act + sr * p.K + x.kbeg + c8 * 8;
         ldsoff[it] = live ? m * C::LDK + c8 * 8 : -1;
     }
@@ -326,8 +345,8 @@ __device__ __forceinline__ void stream_pass(const StreamParams& p, unsigned char
                 } else {
                     int64_t orow = r;
                     float gw = 1.0f;
-                    if (p.topk_w && p.perm) {
-                        orow = p.perm[r];
+                    if (x.scatter) {
+                        orow = x.list ? x.list[r] : p.perm[r];
                         gw = p.topk_w[orow];
                     }
                     float4 v;
@@ -366,24 +385,70 @@ __global__ __launch_bounds__(64 * NS * KS) void stream_kernel(StreamParams p)
     // two XCDs.  The workgroups past the last item (the grid is sized for the
     // worst case) exit at once.
     __shared__ int s_first[65];  // first item of expert e
+    // Routing tables in LDS, for up to kListMax assignments: the expert row
+    // offsets and the assignment behind each expert-major row.  Loaded
+    // together (one memory round trip where the offsets and then the row
+    // order would take two), or built here from the top-k ids, which spares
+    // the step a separate dispatch kernel.
+    __shared__ int s_off[65];
+    __shared__ int s_list[kListMax];
+    __shared__ int s_wc[C::THREADS / 64];
+    constexpr int IPT = (kListMax + C::THREADS - 1) / C::THREADS;  // ids per thread
     const int nbn = p.N / C::ROWS;
     const int nbn8 = (nbn + 7) & ~7;
-    if (threadIdx.x < 64) {
-        const int t = threadIdx.x;
+    const int tid = threadIdx.x;
+    const bool by_ids = p.ids != nullptr;
+    const bool tab = by_ids || (p.offsets && p.A <= kListMax);
+    // UP: the gather source of each row; DOWN: the scatter target
+    const int32_t* const rperm = UP ? p.gather : ((p.topk_w && p.perm) ? p.perm : nullptr);
+    int myid[IPT];
+    if (by_ids) {
+        // s_off counts first, then holds the offsets
+        if (tid < 64) s_off[tid] = 0;
+#pragma unroll
+        for (int i = 0; i < IPT; ++i) {
+            const int a = i * C::THREADS + tid;
+            // ids come from the router and lie in [0, E); the clamp keeps a
+            // corrupted id from indexing past the counts
+            myid[i] = a < p.A ? min(max(p.ids[a], 0), p.E - 1) : -1;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int i = 0; i < IPT; ++i)
+            if (myid[i] >= 0) atomicAdd(&s_off[myid[i]], 1);
+        __syncthreads();
+    } else if (tab) {
+        if (tid <= p.E) s_off[tid] = p.offsets[tid];
+        if (rperm)
+            for (int a = tid; a < p.A; a += C::THREADS) s_list[a] = rperm[a];
+        __syncthreads();
+    }
+    if (tid < 64) {
+        const int t = tid;
+        int Mt = 0;
+        if (t < p.E) Mt = by_ids ? s_off[t] : (tab ? s_off[t + 1] - s_off[t] : expert_rows(p, t));
         int items = 0;
         if (t < p.E) {
-            const int Mt = expert_rows(p, t);
             const int P = (Mt + C::MT - 1) / C::MT;
             if (Mt >= p.mlo && Mt <= p.mhi) items = nbn8 * (P < p.passes ? P : p.passes);
         }
-        // inclusive scan over the wave
+        // inclusive scans over the wave: items, and (from ids) rows
+        int rows = Mt;
 #pragma unroll
         for (int o = 1; o < 64; o <<= 1) {
             const int v = __shfl_up(items, o, 64);
-            if (t >= o) items += v;
+            const int w = __shfl_up(rows, o, 64);
+            if (t >= o) {
+                items += v;
+                rows += w;
+            }
         }
         if (t < p.E) s_first[t + 1] = items;
         if (t == 0) s_first[0] = 0;
+        if (by_ids) {
+            if (t < p.E) s_off[t] = rows - Mt;
+            if (t == p.E - 1) s_off[p.E] = rows;
+        }
     }
     __syncthreads();
     const int total = s_first[p.E];
@@ -398,8 +463,8 @@ __global__ __launch_bounds__(64 * NS * KS) void stream_kernel(StreamParams p)
     }
     int e = 0;
     while (s_first[e + 1] <= b) ++e;
-    const int row0 = expert_row0(p, e);
-    const int M = expert_rows(p, e);
+    const int row0 = tab ? s_off[e] : expert_row0(p, e);
+    const int M = tab ? s_off[e + 1] - s_off[e] : expert_rows(p, e);
     const int npass = (M + C::MT - 1) / C::MT;
     const int nslot = npass < p.passes ? npass : p.passes;
     const int local = b - s_first[e];
@@ -411,7 +476,35 @@ __global__ __launch_bounds__(64 * NS * KS) void stream_kernel(StreamParams p)
     const int rp = (M + npass - 1) / npass;  // rows per pass, balanced
 
     PassCtx x;
-    const int tid = threadIdx.x;
+    x.gather = UP && (by_ids || p.gather);
+    x.scatter = !UP && p.topk_w && (by_ids || p.perm);
+    x.list = tab ? s_list : nullptr;
+    if (by_ids && (x.gather || x.scatter)) {
+        // this expert's rows in assignment order (stable): a wave ballot and
+        // the counts of the waves before give each of its assignments a row
+        const int lane = tid & 63, wv = tid >> 6;
+        const uint64_t lt = lane == 0 ? 0ull : (~0ull >> (64 - lane));
+        int base = row0;
+#pragma unroll
+        for (int i = 0; i < IPT; ++i) {
+            if (i * C::THREADS < p.A) {
+                const bool mine = myid[i] == e;
+                const uint64_t bal = __ballot(mine);
+                if (lane == 0) s_wc[wv] = __popcll(bal);
+                __syncthreads();
+                int before = 0, tot = 0;
+#pragma unroll
+                for (int w = 0; w < C::THREADS / 64; ++w) {
+                    const int c = s_wc[w];
+                    tot += c;
+                    before += w < wv ? c : 0;
+                }
+                if (mine) s_list[base + before + __popcll(bal & lt)] = i * C::THREADS + tid;
+                base += tot;
+                __syncthreads();
+            }
+        }
+    }
     x.lane = tid & 63;
     const int wave = tid >> 6;
     x.ns = wave % NS;
@@ -504,6 +597,9 @@ hipError_t launch_stream_up(const UpArgs& a, int64_t rows_max, hipStream_t strea
     p.act = a.x;
     p.gather = a.gather;
     p.kslots = a.kslots;
+    p.ids = a.ids;
+    p.A = static_cast<int>(a.A < 0x7fffffff ? a.A : 0x7fffffff);
+    if (a.ids && a.A > kListMax) return hipErrorInvalidValue;
     p.offsets = a.offsets;
     p.wa = a.w1;
     p.wb = a.w3;
@@ -559,11 +655,16 @@ hipError_t launch_stream_down(const DownArgs& a, int64_t rows_max, hipStream_t s
     p.y_out = a.y;
     p.topk_w = a.topk_w;
     p.perm = a.perm;
+    p.ids = a.ids;
+    p.A = static_cast<int>(a.A < 0x7fffffff ? a.A : 0x7fffffff);
+    if (a.ids && a.A > kListMax) return hipErrorInvalidValue;
     p.mlo = a.mlo;
     p.mhi = a.mhi;
     p.rows = static_cast<int>(a.A);
     const int G = a.groups ? a.groups : stream_groups(a.A, a.E, rows_max);
-    if (!a.offsets) {
+    if (!a.offsets && !a.ids) {
+        // the dense shapes below exist for bf16 weights only
+        if (a.q2) return hipErrorInvalidValue;
         // dense projection (one matrix): several reduction shares per
         // workgroup, so that a single matrix still spreads over the CUs.
         // Measured on MI355X, K = 4096: more than 4096 output rows, 2 row

@@ -84,6 +84,10 @@ struct UpArgs {
     int mlo = 0, mhi = 0x7fffffff;
     // streaming kernels: 16-row token groups per pass (0 = by rows per expert)
     int groups = 0;
+    // streaming kernels: top-k expert of each assignment [A] (A <=
+    // kStreamListMax); the kernel builds the offsets and the row order from
+    // it, and offsets / gather are not read
+    const int32_t* ids = nullptr;
 };
 
 struct DownArgs {
@@ -105,7 +109,13 @@ struct DownArgs {
     // *ksplit_out (device int, may be null)
     int ksplit_max = 1;
     int* ksplit_out = nullptr;
+    // streaming kernels: as in UpArgs (offsets / perm are then not read)
+    const int32_t* ids = nullptr;
 };
+
+// Assignments up to which the streaming kernels keep the routing tables in
+// LDS (and can build them from the top-k ids).
+constexpr int kStreamListMax = 1024;
 
 enum GemmVariant { VARIANT_AUTO = 0, VARIANT_STREAM = 1, VARIANT_TILED = 2 };
 

@@ -410,6 +410,57 @@ def test_forward_tiled_tail_graph():
     _graph_replays_match_eager(c)
 
 
+def _staged_out(c):
+    """route -> up -> down -> combine through the stage entry points (the
+    dispatch kernel's offsets and row order), as bf16 output bits"""
+    T, d, ffn, k = c.T, c.d, c.ffn, c.k
+    ids, gw, offs, perm, _ = gpu_route(c)
+    h = torch.empty(T * k, ffn, dtype=torch.bfloat16, device=DEV)
+    y = torch.empty(T * k, d, dtype=torch.float32, device=DEV)
+    out = torch.empty(T, d, dtype=torch.bfloat16, device=DEV)
+    B.moe_swiglu_up(c.x, offs, c.w1, c.w3, T, k, h, perm=perm)
+    B.moe_swiglu_down(h, offs, c.w2, T, k, y, topk_w=gw, perm=perm)
+    B.moe_combine(y, T, d, k, out=out)
+    torch.cuda.synchronize()
+    return out
+
+
+@pytest.mark.parametrize("shape,bias", [
+    ((64, 4096, 1792, 8, 2), None),            # one GPU's TP8 share of a decode step
+    ((1, 128, 256, 8, 2), None),               # a single token
+    ((64, 256, 512, 64, 8), None),             # E = 64, k = 8: 512 assignments
+    ((48, 128, 256, 8, 2), [0, 0, 50, 0, 0, 40, 0, 0]),  # six experts idle
+    ((64, 256, 256, 4, 1), [60, 0, 0, 0]),     # one expert takes every token
+    ((512, 256, 256, 16, 2), None),            # 1024 assignments: the LDS table limit
+    ((333, 128, 384, 8, 3), [30, 0, 0, 0, 0, 0, 0, 0]),  # 999 assignments, 333 rows on expert 0
+])
+def test_forward_routes_from_ids_bitwise(shape, bias):
+    """With both GEMMs on the streaming kernels and at most 1024 assignments,
+    the forward skips the dispatch kernel and every workgroup builds the
+    expert offsets and row order from the top-k ids in LDS.  Its output must
+    be bitwise the output of the stage entry points fed by the dispatch
+    kernel (same kernels, same row order), and match the oracle."""
+    say(f"[forward] routing from ids: {shape} bias {bias}")
+    c = small_case(*shape, seed=41, bias=bias)
+    prev = B.moe_set_gemm_variant(1)
+    try:
+        got = gpu_forward(c)
+        ref = _staged_out(c)
+    finally:
+        B.moe_set_gemm_variant(prev)
+    assert torch.equal(got.view(torch.int16), ref.view(torch.int16))
+    _forward_check(c, variant=1)
+
+
+def test_forward_routes_from_ids_graph():
+    """The decode step that routes from ids, captured into a graph: replays
+    (with the workspace cleared in between) give the eager bits."""
+    say("[forward] routing from ids: graph capture")
+    c = small_case(64, 512, 1024, 8, 2, seed=42)
+    assert B.moe_gemm_variant_for(c.T, c.d, c.ffn, c.E, c.k) == 1
+    _graph_replays_match_eager(c)
+
+
 def _graph_replays_match_eager(c):
     T, d, k = c.T, c.d, c.k
     ws = torch.empty(B.moe_workspace_size(T, d, c.ffn, c.E, k), dtype=torch.uint8, device=DEV)
