@@ -14,9 +14,10 @@
 //     cores (16x16x32 bf16 MFMAs, f32 accumulation), the reduction split over
 //     16 waves and their partial tiles summed in a fixed order;
 //   * the top k are then ranked on the key (logit, -expert) -- equal logits
-//     pick the lower expert -- by one lane for up to 16 experts, or by a
-//     wave-wide arg-max butterfly for more, and the softmax over the selected
-//     logits is formed in f32;
+//     pick the lower expert -- by k arg-max butterflies over each token's
+//     expert lanes (up to 16 experts; one lane per token in the matrix-core
+//     kernel), or by a wave-wide arg-max butterfly for more, and the softmax
+//     over the selected logits is formed in f32;
 //   * a single-workgroup dispatch kernel builds the expert histogram, its
 //     exclusive scan and the stable expert-major permutation: up to 1024
 //     assignments one per thread (LDS-atomic histogram, ranks among equal
@@ -139,6 +140,69 @@ __global__ __launch_bounds__(ROUTE_THREADS) void router_topk_kernel(
         for (int m = LANES_PER_V / 2; m >= 1; m >>= 1) tot += wave_shfl_xor(tot, m);
         if ((lane % LANES_PER_V) == 0) red[wave][lane / LANES_PER_V] = tot;
         __syncthreads();
+        if (EMAX <= 16) {
+            // few experts: wave 0's lane j * EMAX + e finishes the logit of
+            // (token j, expert e), and k arg-max butterflies over each token's
+            // EMAX lanes pick its experts on the key (logit, -expert), so an
+            // equal logit keeps the lower index; no LDS round trip
+            if (wave == 0) {
+                const int j = lane / EMAX, e = lane - j * EMAX;
+                const bool live = lane < NV && j < nt && e < E;
+                Cand me;
+                me.v = -INFINITY;
+                me.i = 0x7fffffff;
+                if (live) {
+                    float s = red[0][lane];
+#pragma unroll
+                    for (int w = 1; w < ROUTE_THREADS / 64; ++w) s += red[w][lane];
+                    if (bias) s += bias_e;
+                    if (logits_out) logits_out[(t0 + j) * E + e] = s;
+                    me.v = rank_key(s);
+                    me.i = e;
+                }
+                float selv[8];
+                int seli[8];
+#pragma unroll
+                for (int q = 0; q < 8; ++q) {
+                    if (q < k) {
+                        Cand b = me;
+#pragma unroll
+                        for (int m = EMAX / 2; m >= 1; m >>= 1) {
+                            Cand o;
+                            o.v = wave_shfl_xor(b.v, m);
+                            o.i = wave_shfl_xor(b.i, m);
+                            if (ahead(o, b)) b = o;
+                        }
+                        selv[q] = b.v;
+                        seli[q] = b.i;
+                        if (live && e == b.i) {
+                            me.v = -INFINITY;
+                            me.i = 0x7fffffff;
+                        }
+                    }
+                }
+                if (e == 0 && j < nt) {
+                    const int64_t t = t0 + j;
+                    float ex[8], den = 0.0f;
+#pragma unroll
+                    for (int q = 0; q < 8; ++q) {
+                        if (q < k) {
+                            ex[q] = expf(selv[q] - selv[0]);
+                            den += ex[q];
+                        }
+                    }
+#pragma unroll
+                    for (int q = 0; q < 8; ++q) {
+                        if (q < k) {
+                            topk_ids[t * k + q] = seli[q];
+                            topk_w[t * k + q] = ex[q] / den;
+                        }
+                    }
+                }
+            }
+            __syncthreads();
+            continue;
+        }
         if (tid < NV) {
             const int j = tid / EMAX, e = tid - j * EMAX;
             if (j < nt && e < E) {
@@ -151,53 +215,6 @@ __global__ __launch_bounds__(ROUTE_THREADS) void router_topk_kernel(
             }
         }
         __syncthreads();
-        if (EMAX <= 16) {
-            // few experts: one lane per token ranks them directly
-            if (tid < nt) {
-                const int64_t t = t0 + tid;
-                int seli[8];
-                float selv[8];
-                uint32_t taken = 0;
-#pragma unroll
-                for (int j = 0; j < 8; ++j) {
-                    if (j < k) {
-                        int best = -1;
-                        float bv = 0.0f;
-#pragma unroll
-                        for (int e = 0; e < EMAX; ++e) {
-                            if (e < E && !(taken & (1u << e))) {
-                                const float le = rank_key(lg[tid][e]);
-                                // strict: an equal logit keeps the lower index
-                                if (best < 0 || le > bv) {
-                                    best = e;
-                                    bv = le;
-                                }
-                            }
-                        }
-                        taken |= 1u << best;
-                        seli[j] = best;
-                        selv[j] = bv;
-                    }
-                }
-                float ex[8], den = 0.0f;
-#pragma unroll
-                for (int j = 0; j < 8; ++j) {
-                    if (j < k) {
-                        ex[j] = expf(selv[j] - selv[0]);
-                        den += ex[j];
-                    }
-                }
-#pragma unroll
-                for (int j = 0; j < 8; ++j) {
-                    if (j < k) {
-                        topk_ids[t * k + j] = seli[j];
-                        topk_w[t * k + j] = ex[j] / den;
-                    }
-                }
-            }
-            __syncthreads();
-            continue;
-        }
         // more experts: wave j ranks token j with a wave-wide arg-max
         if (wave < nt) {
             const int64_t t = t0 + wave;
