@@ -198,7 +198,11 @@ moe_status_t moe_combine_parts(const float* y, const int32_t* parts, int32_t max
  * Engine": the engine work targets Mixture-of-Experts models; Sec. 5:
  * Mixtral-8x7B, up to 256 concurrent requests per step under continuous
  * batching): route -> SwiGLU experts (the gather of token rows is fused
- * into the first expert GEMM) -> combine.  out [T,d] bf16, must not overlap
+ * into the first expert GEMM) -> combine.  Where both expert GEMMs run on the
+ * weight-streaming kernels with at most 1024 assignments (decode steps), the
+ * expert offsets and row order are built from the top-k ids inside those
+ * kernels and no separate dispatch runs; the results are bitwise those of the
+ * stage-by-stage calls.  out [T,d] bf16, must not overlap
  * any input.  Scratch is owned by the library, cached per device and grown on
  * demand (a growth is refused with MOE_ERR_NO_MEMORY while `stream` is being
  * captured into a graph; call once outside capture first).  A buffer that was
