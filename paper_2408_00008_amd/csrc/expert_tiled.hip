@@ -65,10 +65,10 @@ struct TiledParams {
     int64_t slice;
     int* ksplit_out;
     int64_t A;
-    // DOWN, tail split (see the kernel): tiles uncut, the last round's tiles
-    // split across the workgroups; the pieces after each tile's first go to
-    // y_out + slice (kTailPiece floats each, one slot per workgroup), a table
-    // of the split tiles after them
+    // DOWN, tail split (see the kernel): tiles uncut, the tiles past the
+    // grid's whole rounds split across all the workgroups; the pieces after
+    // each tile's first go to y_out + slice (kTailPiece floats each, one slot
+    // per workgroup), a table of the split tiles and their count after them
     int tail;
 };
 
@@ -241,27 +241,37 @@ __global__ __launch_bounds__(256) void q_kernel(TiledParams p)
         }
         return ex + blk * mt_e + m;
     };
+    // The workgroups of an XCD take its items in rounds (workgroup j: items
+    // j, j + P, j + 2P, ...).  DOWN with tail split: the items of whole
+    // rounds of the grid are dealt in equal counts, XCD x taking the x-th
+    // range; the rem < grid tiles left over would leave grid - rem
+    // workgroups idle for a whole tile, so each of them is cut into `pieces`
+    // = grid / rem reduction ranges spread over all the workgroups (piece g
+    // to the g-th workgroup in XCD-major order, so the pieces of neighbouring
+    // tiles of one weight block share an XCD); piece 0 writes the tile's
+    // output as usual, the others write f32 pieces that fold_tail_kernel
+    // adds to it.  Otherwise the ranges are of about equal cost and the last
+    // round is left partial.
+    const bool gtail = !UP && p.tail;
+    const int grounds = gtail ? total / (int)gridDim.x : 0;
     // (uniform by construction; readfirstlane lets the compiler see it, so the
     // item indices and everything derived from them stay in scalar registers)
-    const int beg = __builtin_amdgcn_readfirstlane(first_item_at((ctot * xcd + 7) / 8));
-    const int end = __builtin_amdgcn_readfirstlane(
-        xcd == 7 ? total : first_item_at((ctot * (xcd + 1) + 7) / 8));
-    // The workgroups of an XCD take its items in rounds (workgroup j: items
-    // j, j + P, j + 2P, ...).  DOWN with tail split: the last, partial round
-    // of rem < P tiles would leave P - rem workgroups idle for a whole tile,
-    // so each of those tiles is cut into `pieces` = P / rem reduction ranges
-    // taken by consecutive workgroups; piece 0 writes the tile's output as
-    // usual, the others write f32 pieces that fold_tail_kernel adds to it.
+    const int beg = gtail ? xcd * grounds * per_xcd
+                          : __builtin_amdgcn_readfirstlane(first_item_at((ctot * xcd + 7) / 8));
+    const int end = gtail ? beg + grounds * per_xcd
+                          : __builtin_amdgcn_readfirstlane(
+                                xcd == 7 ? total : first_item_at((ctot * (xcd + 1) + 7) / 8));
     const int n_xcd = end - beg;
     const int rounds = n_xcd / per_xcd;
-    const int rem = (!UP && p.tail) ? n_xcd - rounds * per_xcd : 0;
+    const int rem = gtail ? total - grounds * (int)gridDim.x : 0;
     // (at most one piece per reduction step: every piece has a step)
-    const int pieces = rem > 0 ? min(per_xcd / rem, nk) : 1;
-    const int units = rem > 0 ? rounds + (local < rem * pieces ? 1 : 0)
-                              : (local < n_xcd ? (n_xcd - local + per_xcd - 1) / per_xcd : 0);
-    int* const tail_tab = (!UP && p.tail)
+    const int pieces = rem > 0 ? min((int)gridDim.x / rem, nk) : 1;
+    const int gpiece = xcd * per_xcd + local;  // this workgroup's tail piece
+    const int units = gtail ? rounds + (gpiece < rem * pieces ? 1 : 0)
+                            : (local < n_xcd ? (n_xcd - local + per_xcd - 1) / per_xcd : 0);
+    int* const tail_tab = gtail
         ? reinterpret_cast<int*>(p.y_out + p.slice + (int64_t)gridDim.x * kTailPiece) : nullptr;
-    if (tail_tab && local == 0 && tid == 0) tail_tab[4 * gridDim.x + xcd] = pieces > 1 ? rem : 0;
+    if (tail_tab && blockIdx.x == 0 && tid == 0) tail_tab[4 * gridDim.x] = pieces > 1 ? rem : 0;
 
     // a token load covers 8 rows starting at a multiple of 8: lane l takes row
     // l / 8 and the global chunk stored at slot l % 8 (odd loads start at 8
@@ -320,11 +330,11 @@ __global__ __launch_bounds__(256) void q_kernel(TiledParams p)
     // beg + local + u P, or in the tail-split round a piece of a tile
     auto index_item = [&](int u, Item& it) {
         int w = beg + local + u * per_xcd;
-        int pc = 0;
+        int pc = 0, ti = 0;
         if (u == rounds && rem > 0) {
-            const int i = local / pieces;
-            pc = local - i * pieces;
-            w = beg + rounds * per_xcd + i;
+            ti = gpiece / pieces;
+            pc = gpiece - ti * pieces;
+            w = grounds * (int)gridDim.x + ti;
         }
         const uint64_t le = __ballot(lane < p.E && my_tiles > 0 && ex_items <= w);
         const int e = 63 - __builtin_clzll(le);
@@ -342,9 +352,9 @@ __global__ __launch_bounds__(256) void q_kernel(TiledParams p)
         const int pp = tail_unit ? pc : part;
         it.k0 = (int)((int64_t)nk * pp / np);
         it.kn = (int)((int64_t)nk * (pp + 1) / np) - it.k0;
-        it.slot = pc > 0 ? (int)blockIdx.x : -1;
+        it.slot = pc > 0 ? gpiece : -1;
         if (tail_unit && pc == 0 && pieces > 1 && tid == 0) {
-            int* t = tail_tab + 4 * (xcd * per_xcd + (local / pieces));
+            int* t = tail_tab + 4 * ti;
             t[0] = e;
             t[1] = nb;
             t[2] = mtile;
@@ -773,9 +783,9 @@ __global__ __launch_bounds__(256) void q_kernel(TiledParams p)
 // round (table written by the tiles' first pieces) to the tile's output in
 // y: rows scattered through perm as in the down epilogue, the gate weights
 // already applied, pieces added in order after piece 0's value.  Workgroup
-// (slot, block of 16 rows), slot = xcd * P + i for split tile i of an XCD
-// (grid = the down launch's grid x 16); each thread 4 rows of one 16-byte
-// column chunk, all loads of a row issued together.
+// (split tile i, block of 16 rows) (grid = the down launch's grid x 16);
+// each thread 4 rows of one 16-byte column chunk, all loads of a row issued
+// together.
 constexpr int kFoldRows = 16;
 __global__ __launch_bounds__(256) void fold_tail_kernel(float* __restrict__ y, int64_t slice,
                                                         const int32_t* __restrict__ offsets,
@@ -783,14 +793,12 @@ __global__ __launch_bounds__(256) void fold_tail_kernel(float* __restrict__ y, i
                                                         const float* __restrict__ topk_w, int N,
                                                         int q_grid)
 {
-    const int per_xcd = q_grid >> 3;
-    const int b = blockIdx.x / (256 / kFoldRows);
-    const int rb = blockIdx.x - b * (256 / kFoldRows);
-    const int xcd = b / per_xcd, i = b - xcd * per_xcd;
+    const int i = blockIdx.x / (256 / kFoldRows);
+    const int rb = blockIdx.x - i * (256 / kFoldRows);
     const float* pieces = y + slice;
     const int* tab = reinterpret_cast<const int*>(pieces + (int64_t)q_grid * kTailPiece);
-    if (i >= tab[4 * q_grid + xcd]) return;
-    const int e = tab[4 * b], nb = tab[4 * b + 1], mtile = tab[4 * b + 2], np = tab[4 * b + 3];
+    if (i >= tab[4 * q_grid]) return;
+    const int e = tab[4 * i], nb = tab[4 * i + 1], mtile = tab[4 * i + 2], np = tab[4 * i + 3];
     const int row0 = offsets[e] + mtile * 256;
     const int Mp = min(256, offsets[e + 1] - row0);
     const int c4 = threadIdx.x & 63;
@@ -802,8 +810,8 @@ __global__ __launch_bounds__(256) void fold_tail_kernel(float* __restrict__ y, i
         float4* yr = reinterpret_cast<float4*>(y + a * N + nb * 256) + c4;
         float4 v = *yr;
         for (int pc = 1; pc < np; ++pc) {
-            // piece pc of tile i was computed by workgroup (i np + pc) * 8 + xcd
-            const int slot = (i * np + pc) * 8 + xcd;
+            // piece pc of split tile i has slot i np + pc
+            const int slot = i * np + pc;
             const float4 w =
                 reinterpret_cast<const float4*>(pieces + (int64_t)slot * kTailPiece + lr * 256)[c4];
             v.x += w.x;
