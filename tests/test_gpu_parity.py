@@ -273,10 +273,15 @@ def test_forward_split_by_rows(shape):
     ((288, 256, 2048, 8, 2), 4),   # one token tile per expert, 4 parts of 8 steps
     ((600, 512, 1024, 8, 2), 2),   # 2 weight blocks per expert, 2 parts of 8 steps
     ((600, 256, 2048, 64, 8), None),  # E = 64, k = 8: 64 ragged tiles (count not pinned)
-    # slices large enough for the tail split: tiles uncut (count 1), the
-    # last round's tiles (here all of them: ~12 per XCD) cut in 2 pieces
-    # across the workgroups and folded back into slice 0
+    # slices large enough for the tail split: tiles uncut (count 1); the
+    # tiles past the grid's whole rounds are cut into pieces over all the
+    # workgroups and folded back into slice 0.  96 tiles, no whole round:
+    # every tile in 2 pieces
     ((3000, 1024, 2048, 8, 2), 1),
+    # 320 tiles: one whole round, the 64 left in 4 pieces each
+    ((4800, 2048, 2048, 8, 2), 1),
+    # 192 tiles, no whole round and more than half the grid: uncut, no pieces
+    ((6000, 1024, 2048, 8, 2), 1),
 ])
 def test_forward_down_split(shape, parts):
     """Prefill-regime sizes with few token tiles: the tiled down GEMM cuts its
