@@ -254,6 +254,26 @@ __global__ __launch_bounds__(256) void q_kernel(TiledParams p)
     // round is left partial.
     const bool gtail = !UP && p.tail;
     const int grounds = gtail ? total / (int)gridDim.x : 0;
+    // With the tail split the items are ordered in two classes: first every
+    // tile but the experts' short last tiles (cost below a full tile), then
+    // those short tiles.  The whole rounds then hold full-cost tiles where
+    // they can, and the short ones (a few rows streaming a whole weight
+    // block) go to the split tail; each class is expert-major, a weight
+    // block's token tiles next to each other.
+    const int short_e = (gtail && my_tiles > 0 && tile_cost(last_rows) < kFullTileCost) ? 1 : 0;
+    const int a_tiles = my_tiles - short_e;
+    int in_a = nbn * a_tiles, in_b = nbn * short_e;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const int va = __shfl_up(in_a, o, 64);
+        const int vb = __shfl_up(in_b, o, 64);
+        if (lane >= o) {
+            in_a += va;
+            in_b += vb;
+        }
+    }
+    const int ex_a = in_a - nbn * a_tiles, ex_b = in_b - nbn * short_e;
+    const int n_a = uni(__shfl(in_a, p.E - 1, 64));
     // (uniform by construction; readfirstlane lets the compiler see it, so the
     // item indices and everything derived from them stay in scalar registers)
     const int beg = gtail ? xcd * grounds * per_xcd
@@ -336,14 +356,34 @@ __global__ __launch_bounds__(256) void q_kernel(TiledParams p)
             pc = gpiece - ti * pieces;
             w = grounds * (int)gridDim.x + ti;
         }
-        const uint64_t le = __ballot(lane < p.E && my_tiles > 0 && ex_items <= w);
-        const int e = 63 - __builtin_clzll(le);
-        const int mt_e = uni(__shfl(my_tiles, e, 64));
-        int r = w - uni(__shfl(ex_items, e, 64));
-        const int part = r / (nbn * mt_e);
-        r -= part * nbn * mt_e;
-        const int nb = r / mt_e;
-        const int mtile = r - nb * mt_e;
+        int e, part, nb, mtile;
+        if (gtail) {
+            // (one reduction part in the tail split)
+            part = 0;
+            if (w < n_a) {
+                const uint64_t le = __ballot(lane < p.E && a_tiles > 0 && ex_a <= w);
+                e = 63 - __builtin_clzll(le);
+                const int ma = uni(__shfl(a_tiles, e, 64));
+                const int r = w - uni(__shfl(ex_a, e, 64));
+                nb = r / ma;
+                mtile = r - nb * ma;
+            } else {
+                const int wb = w - n_a;
+                const uint64_t le = __ballot(lane < p.E && short_e > 0 && ex_b <= wb);
+                e = 63 - __builtin_clzll(le);
+                nb = wb - uni(__shfl(ex_b, e, 64));
+                mtile = uni(__shfl(my_tiles, e, 64)) - 1;
+            }
+        } else {
+            const uint64_t le = __ballot(lane < p.E && my_tiles > 0 && ex_items <= w);
+            e = 63 - __builtin_clzll(le);
+            const int mt_e = uni(__shfl(my_tiles, e, 64));
+            int r = w - uni(__shfl(ex_items, e, 64));
+            part = r / (nbn * mt_e);
+            r -= part * nbn * mt_e;
+            nb = r / mt_e;
+            mtile = r - nb * mt_e;
+        }
         it.e = e;
         it.part = part;
         it.nb = nb;
