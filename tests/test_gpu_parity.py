@@ -282,6 +282,9 @@ def test_forward_split_by_rows(shape):
     ((4800, 2048, 2048, 8, 2), 1),
     # 192 tiles, no whole round and more than half the grid: uncut, no pieces
     ((6000, 1024, 2048, 8, 2), 1),
+    # E = 64, k = 8, ~256 rows per expert: many experts' short last tiles
+    # ordered after the full ones, two whole rounds, the rest split
+    ((2048, 1024, 1024, 64, 8), 1),
 ])
 def test_forward_down_split(shape, parts):
     """Prefill-regime sizes with few token tiles: the tiled down GEMM cuts its
