@@ -23,6 +23,12 @@
 //     the caller's limit; items then ordered expert, part, weight block,
 //     token tile), chosen on the device from the tile count by a cost model,
 //     where that evens out the rounds of the persistent grid;
+//   * or, where the caller's spare slices hold one 256 x 256 f32 piece per
+//     workgroup, DOWN leaves the tiles uncut (the tail split): the tiles of
+//     the grid's whole rounds, every tile but the experts' short last tiles
+//     first, go to the XCDs in equal counts, and each tile left over is cut
+//     into contiguous reduction ranges spread over all the workgroups, its
+//     pieces added into y by fold_tail_kernel in piece order;
 //   * 8-bit weights (E4M3 bytes, one f32 scale per weight row) are staged in
 //     LDS as bytes, widened to bf16 at the fragment reads, and their scales
 //     multiply the accumulators in the epilogue;
