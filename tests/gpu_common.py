@@ -246,6 +246,31 @@ def oracle_out_fp8(c: Fp8Case, rows, gpu_ids_rows=None):
     return out, logits, ids, gates
 
 
+def random_large_shapes(n=12, seed=2409):
+    """Seeded draws of larger layers: T from 1 to 6000 in three bands, d and
+    ffn multiples of 64 or 256 up to 2048 (1024 above 16 experts), E in
+    1..64 with k in 1..min(E, 8), and on every other draw a +2 router bias on
+    one expert (skewed rows).  These reach the paths that only larger shapes
+    take: the split of a step by rows per expert, the tiled down GEMM's
+    reduction parts and its tail split.  Each draw: (T, d, ffn, E, k, skewed
+    expert or -1)."""
+    rng = np.random.default_rng(seed)
+    out = []
+    while len(out) < n:
+        E = int(rng.choice([1, 2, 4, 8, 8, 16, 32, 64]))
+        k = int(rng.integers(1, min(E, 8) + 1))
+        unit = int(rng.choice([64, 256, 256]))
+        top = 2048 if E <= 16 else 1024
+        d = unit * int(rng.integers(1, top // unit + 1))
+        ffn = unit * int(rng.integers(1, top // unit + 1))
+        band = len(out) % 3
+        T = int(rng.integers(1, 65) if band == 0 else
+                (rng.integers(65, 1025) if band == 1 else rng.integers(1025, 6001)))
+        hot = int(rng.integers(0, E)) if (len(out) % 2 and E > 1) else -1
+        out.append((T, d, ffn, E, k, hot))
+    return out
+
+
 def random_shapes(n=16, seed=2408):
     """Seeded draws over the supported space: E in 1..64, k in 1..min(E, 8),
     d and ffn multiples of 64 up to 768 (every other draw multiples of 256,

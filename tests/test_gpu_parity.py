@@ -5,7 +5,8 @@ import pytest
 import torch
 
 from gpu_common import (DEV, bf16_to_f64, full_logits, full_reference, gpu_forward, gpu_route,
-                        oracle_logits, oracle_out, orc, random_shapes, say, small_case,
+                        oracle_logits, oracle_out, orc, random_large_shapes, random_shapes, say,
+                        small_case,
                         tile_cover_rows, workload_case)
 from parity import OUT_TOL, check_routing, rowwise_rel
 from paper_2408_00008_amd import binding as B
@@ -223,6 +224,46 @@ def test_forward_random_shapes(shape):
     cut reduction) on seeded random shapes, every token against the oracle."""
     say(f"[forward] random shape {shape} (auto: {B.moe_gemm_variant_for(*shape)})")
     _forward_check(small_case(*shape, seed=31), variant=0)
+
+
+@pytest.mark.parametrize("shape", random_large_shapes(), ids=lambda s: "x".join(map(str, s)))
+def test_forward_random_large_shapes(shape):
+    """Seeded larger layers (up to 6000 tokens, skewed routing on every other
+    draw), every kernel family, on tokens that cover every (expert, 256-row
+    tile) work item; then moe_forward_ex with the caller's workspace (where
+    the down GEMM may cut its reduction or split its last tiles) against the
+    same oracle rows, and twice for the same bits."""
+    T, d, ffn, E, k, hot = shape
+    bias = None
+    if hot >= 0:
+        bias = [0.0] * E
+        bias[hot] = 2.0
+    say(f"[forward] large random shape {shape} (auto: {B.moe_gemm_variant_for(T, d, ffn, E, k)})")
+    c = small_case(T, d, ffn, E, k, seed=37, bias=bias)
+    ids, *_ = gpu_route(c)
+    g_ids = ids.cpu().numpy()
+    rows = tile_cover_rows(g_ids, k, E, seed=5)
+    if len(rows) > 96:
+        pick = np.random.default_rng(6).choice(rows, 96, replace=False)
+        rows = np.array(sorted(set(pick.tolist()) | {0, T - 1}))
+    check_routing(g_ids[rows], oracle_logits(c, rows), k)
+    ref, *_ = oracle_out(c, rows, g_ids[rows])
+    for variant in (0, 1, 2):
+        err = rowwise_rel(bf16_to_f64(gpu_forward(c, variant))[rows], ref)
+        say(f"  variant {variant}: rowwise rel {err:.3e} over {len(rows)} tokens")
+        assert err < OUT_TOL
+    ws = torch.empty(B.moe_workspace_size(T, d, ffn, E, k), dtype=torch.uint8, device=DEV)
+    outs = []
+    for _ in range(2):
+        of = torch.empty(T, d, dtype=torch.float32, device=DEV)
+        B.moe_forward_ex(c.x, c.router_w, c.w1, c.w3, c.w2, k, out_f32=of,
+                         router_bias=c.router_bias, workspace=ws)
+        outs.append(of)
+    torch.cuda.synchronize()
+    err = rowwise_rel(outs[0].double().cpu().numpy()[rows], ref)
+    say(f"  forward_ex with workspace: rowwise rel {err:.3e}")
+    assert err < OUT_TOL
+    assert torch.equal(outs[0], outs[1])
 
 
 def test_forward_empty_experts():
