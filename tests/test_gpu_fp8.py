@@ -12,7 +12,7 @@ import torch
 
 from gpu_common import (DEV, bf16_to_f64, fp8_small_case, fp8_workload_case, full_logits,
                         full_reference, gpu_forward_fp8, gpu_route, orc, oracle_out_fp8,
-                        random_shapes, say)
+                        random_large_shapes, random_shapes, say, tile_cover_rows)
 from parity import OUT_TOL, check_routing, rowwise_rel
 from paper_2408_00008_amd import binding as B
 
@@ -122,6 +122,50 @@ def test_fp8_forward_random_shapes(shape):
     every token against the oracle."""
     say(f"[fp8 forward] random shape {shape} (auto: {B.moe_gemm_variant_for(*shape)})")
     _forward_check(fp8_small_case(*shape, seed=32))
+
+
+@pytest.mark.parametrize("shape", random_large_shapes(8, seed=2410), ids=lambda s: "x".join(map(str, s)))
+def test_fp8_forward_random_large_shapes(shape):
+    """8-bit weights on seeded larger layers (skewed routing on every other
+    draw): every kernel family on tokens that cover every (expert, 256-row
+    tile) work item, then moe_forward_fp8_ex with the caller's workspace,
+    twice for the same bits."""
+    T, d, ffn, E, k, hot = shape
+    bias = None
+    if hot >= 0:
+        bias = [0.0] * E
+        bias[hot] = 2.0
+    say(f"[fp8 forward] large random shape {shape}")
+    c = fp8_small_case(T, d, ffn, E, k, seed=38, bias=bias)
+    ids, *_ = gpu_route(c)
+    g_ids = ids.cpu().numpy()
+    rows = tile_cover_rows(g_ids, k, E, seed=7)
+    if len(rows) > 96:
+        pick = np.random.default_rng(8).choice(rows, 96, replace=False)
+        rows = np.array(sorted(set(pick.tolist()) | {0, T - 1}))
+    ref, logits, *_ = oracle_out_fp8(c, rows, g_ids[rows])
+    check_routing(g_ids[rows], logits, k)
+    for variant in (0, 1, 2):
+        prev = B.moe_set_gemm_variant(variant)
+        try:
+            out = gpu_forward_fp8(c)
+        finally:
+            B.moe_set_gemm_variant(prev)
+        err = rowwise_rel(bf16_to_f64(out)[rows], ref)
+        say(f"  variant {variant}: rowwise rel {err:.3e} over {len(rows)} tokens")
+        assert err < OUT_TOL
+    ws = torch.empty(B.moe_workspace_size(T, d, ffn, E, k), dtype=torch.uint8, device=DEV)
+    outs = []
+    for _ in range(2):
+        of = torch.empty(T, d, dtype=torch.float32, device=DEV)
+        B.moe_forward_fp8_ex(c.x, c.router_w, c.w1q, c.w1s, c.w3q, c.w3s, c.w2q, c.w2s, k,
+                             out_f32=of, router_bias=c.router_bias, workspace=ws)
+        outs.append(of)
+    torch.cuda.synchronize()
+    err = rowwise_rel(outs[0].double().cpu().numpy()[rows], ref)
+    say(f"  forward_fp8_ex with workspace: rowwise rel {err:.3e}")
+    assert err < OUT_TOL
+    assert torch.equal(outs[0], outs[1])
 
 
 @pytest.mark.parametrize("shape,bias", [
